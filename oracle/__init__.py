@@ -1,0 +1,138 @@
+"""CPU oracle for RITA group attention -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The GPU library never loads it, and the
+two share no code: the oracle is plain fp64 C (``ga_oracle.c``) written from
+the paper's definitions, wrapped here with ctypes.
+
+Functions take/return numpy arrays; inputs may be any float array holding the
+exact values of the bf16 / fp32 tensors (they are widened to float64 here).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ga_oracle.c")
+# GA_ORACLE_LIB lets the mutation test point the wrapper at a deliberately
+# broken build of the same source.
+_LIB = os.environ.get("GA_ORACLE_LIB") or os.path.join(_HERE, "libga_oracle.so")
+
+DTYPES = {"f32": 0, "bf16": 1}
+
+
+def build(force: bool = True, src: str = _SRC, out: str | None = None) -> str:
+    """Compile the oracle with gcc (strict IEEE: no fast-math, no x87)."""
+    out = out or _LIB
+    if force or not os.path.exists(out):
+        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+               "-fno-fast-math", "-o", out + ".tmp", src, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(out + ".tmp", out)
+    return out
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
+        lib.ga_oracle_cluster.argtypes = [i32, i32, i32, i32, i32, P, i32, i32, P, P, P, P, P, P, P]
+        lib.ga_oracle_cluster.restype = i64
+        lib.ga_oracle_aggregate.argtypes = [i32, i32, i32, i32, P, P, i32, P]
+        lib.ga_oracle_aggregate.restype = i64
+        lib.ga_oracle_attend.argtypes = [i32, i32, i32, i32, i32, P, P, P, P, i32, f64, P]
+        lib.ga_oracle_attend.restype = None
+        lib.ga_oracle_threads.argtypes = [i32]
+        lib.ga_oracle_threads.restype = i32
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p) if a is not None else None
+
+
+def _f64(x):
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+
+
+def threads(n: int = 0) -> int:
+    """Set (n > 0) and return the OpenMP thread count the oracle uses."""
+    return _load().ga_oracle_threads(int(n))
+
+
+def cluster(K, N: int, iters: int, dtype: str, init=None, trace: bool = False):
+    """Lloyd grouping of the keys of every (b, h) slice (Section 4.4).
+
+    K: [B, H, n, d].  Returns dict with belong [B,H,n] int32, count [B,H,N]
+    int32, centroid [B,H,N,d] float32, inexact (count of inexact fp64 adds in
+    the centroid sums) and, if trace, per-iteration belong / margin (second
+    best minus best canonical score) / centroid, each with a leading iters axis.
+    """
+    K = _f64(K)
+    B, H, n, d = K.shape
+    belong = np.empty((B, H, n), np.int32)
+    count = np.empty((B, H, N), np.int32)
+    centroid = np.empty((B, H, N, d), np.float32)
+    init_a = None if init is None else np.ascontiguousarray(np.asarray(init, np.float32))
+    tb = tm = tc = None
+    if trace:
+        tb = np.empty((iters, B, H, n), np.int32)
+        tm = np.empty((iters, B, H, n), np.float64)
+        tc = np.empty((iters, B, H, N, d), np.float32)
+    inexact = _load().ga_oracle_cluster(B, H, n, d, DTYPES[dtype], _ptr(K), N, iters, _ptr(init_a),
+                                        _ptr(belong), _ptr(count), _ptr(centroid), _ptr(tb), _ptr(tm),
+                                        _ptr(tc))
+    out = dict(belong=belong, count=count, centroid=centroid, inexact=int(inexact))
+    if trace:
+        out.update(trace_belong=tb, trace_margin=tm, trace_centroid=tc)
+    return out
+
+
+def aggregate(V, belong, N: int):
+    """Per-group fp64 sums of the value vectors (embedding aggregation)."""
+    V = _f64(V)
+    B, H, n, d = V.shape
+    bel = np.ascontiguousarray(np.asarray(belong, np.int32))
+    vsum = np.empty((B, H, N, d), np.float64)
+    inexact = _load().ga_oracle_aggregate(B, H, n, d, _ptr(V), _ptr(bel), N, _ptr(vsum))
+    return vsum, int(inexact)
+
+
+def attend(Q, centroid, count, vsum, N: int, scale: float, dtype: str):
+    """Group softmax (Eq. 3) and output combine; returns O [B,H,n,d] float64."""
+    Q = _f64(Q)
+    B, H, n, d = Q.shape
+    cen = np.ascontiguousarray(np.asarray(centroid, np.float32))
+    cnt = np.ascontiguousarray(np.asarray(count, np.int32))
+    vs = _f64(vsum)
+    O = np.empty((B, H, n, d), np.float64)
+    _load().ga_oracle_attend(B, H, n, d, DTYPES[dtype], _ptr(Q), _ptr(cen), _ptr(cnt), _ptr(vs), N,
+                             float(scale), _ptr(O))
+    return O
+
+
+def forward(Q, K, V, N: int, iters: int, scale: float, dtype: str, init=None):
+    """Whole group-attention forward: grouping, aggregation, attention."""
+    cl = cluster(K, N, iters, dtype, init=init)
+    vsum, inexact_v = aggregate(V, cl["belong"], N)
+    O = attend(Q, cl["centroid"], cl["count"], vsum, N, scale, dtype)
+    return dict(O=O, vsum=vsum, inexact_v=inexact_v, **cl)
+
+
+def round_bf16(x):
+    """bf16 RNE of float32 values, as float32 (numpy, for test expectations)."""
+    u = np.ascontiguousarray(np.asarray(x, np.float32)).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32)
