@@ -1,0 +1,185 @@
+#!/usr/bin/env python
+"""Group-attention forward throughput on one MI355X.
+
+One step = one whole group-attention forward (grouping rounds, aggregation,
+group softmax + combine) over one batch of synthetic input already resident in
+HBM.  Two input sets alternate so consecutive steps do not hit in the 256 MB
+last-level cache.  Prints one JSON line (see the contract in the design doc).
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA
+METRIC = "group-attention queries/sec (B·H·n) at n=8000,N=128; % HBM roofline"
+
+
+def kernel_work(name, w, N, BH):
+    """(bound, algorithmic work per launch, unit, peak) of each kernel.
+
+    assign:  the n x N x d score contraction, 2 n N d flop per slice.
+    attend:  Q read + O write, 2 n d storage elements per slice (HBM-bound:
+             4 N d = 32768 flop per 256 B query is below the MFMA ridge).
+    update / valuesum: one read of K (or V), n d elements per slice.
+    bucket:  belong read twice + perm write, 12 B per key.
+    """
+    es = 2 if w.dtype == "bf16" else 4
+    n, d = w.n, w.d
+    if name == "assign":
+        return "mfma", 2.0 * n * N * d * BH / 1e12, "TFLOP/s", MFMA_BF16_PEAK_TFS
+    if name == "attend":
+        return "hbm", 2.0 * n * d * es * BH / 1e9, "GB/s", HBM_PEAK_GBS
+    if name in ("update", "valuesum"):
+        return "hbm", 1.0 * n * d * es * BH / 1e9, "GB/s", HBM_PEAK_GBS
+    if name == "bucket":
+        return "hbm", 12.0 * n * BH / 1e9, "GB/s", HBM_PEAK_GBS
+    return "hbm", 1.0 * N * d * 4 * BH / 1e9, "GB/s", HBM_PEAK_GBS
+
+
+def traffic_for(kernel, workload):
+    """Measured HBM bytes per launch from a committed rocprofv3 counter summary,
+    or None if there is none or the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    src = os.path.join(ROOT, "paper_2306_01926_amd", "csrc", "ga_kernels.hip")
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if rec.get("kernel_source_sha256") != digest:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="n8000_N128_bf16")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-slices", type=int, default=16, help="(b,h) slices the oracle times")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU: this build runs group attention on a single MI355X "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}); see DESIGN.md for how it would shard.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2306_01926_amd import ga, inputs
+
+    dev = torch.device("cuda:0")
+    w = inputs.WORKLOADS[args.workload]
+    N = inputs.draw_group_count(w, args.seed, 0)
+    BH = w.B * w.H
+    scale = 1.0 / math.sqrt(w.d)
+    print(f"bench: workload {w.name} B={w.B} H={w.H} n={w.n} d={w.d} N={N} iters={w.iters} {w.dtype}",
+          file=sys.stderr, flush=True)
+    host_sets = [inputs.workload_inputs(w, args.seed + k) for k in range(2)]
+    sets = [tuple(t.to(dev) for t in s) for s in host_sets]
+    outs = [torch.empty_like(s[0]) for s in sets]
+    ws = ga.workspace(ga.shape_of(sets[0][0]), N, dev)[0]
+
+    def step(k):
+        Q, K, V = sets[k % 2]
+        ga.forward(Q, K, V, N, w.iters, scale, out=outs[k % 2], ws=ws)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+
+    # timed region: K whole-forward steps, events on the launch stream
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for k in range(args.steps):
+        step(k)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+
+    # same steps again with every kernel launch bracketed by hipEvents
+    ga.timing_enable(True)
+    t0.record()
+    for k in range(args.steps):
+        step(k)
+    t1.record()
+    torch.cuda.synchronize()
+    ga.timing_enable(False)
+    per_kernel = ga.timing_collect()
+    ms_timed = t0.elapsed_time(t1) / args.steps
+
+    queries = BH * w.n
+    es = 2 if w.dtype == "bf16" else 4
+    compulsory = 4.0 * queries * w.d * es  # read Q, K, V once, write O once
+    value = queries / (ms / 1e3)
+    pct_hbm = compulsory / (ms / 1e3) / (HBM_PEAK_GBS * 1e9)
+
+    kernels = {}
+    for name, (launches, tot) in per_kernel.items():
+        bound, work, unit, peak = kernel_work(name, w, N, BH)
+        avg = tot / launches
+        ach = work / (avg / 1e3)
+        kernels[name] = dict(launches_per_step=launches / args.steps, avg_ms=avg, bound=bound,
+                             achieved=ach, unit=unit, frac=ach / peak)
+    dom = max(per_kernel, key=lambda k: per_kernel[k][1])
+    kd = kernels[dom]
+    _, work, _, peak = kernel_work(dom, w, N, BH)
+    roofline = dict(kernel=dom, bound=kd["bound"], achieved=round(kd["achieved"], 3), peak=peak, unit=kd["unit"],
+                    frac=round(kd["frac"], 4), traffic=traffic_for(dom, w.name),
+                    avg_launch_ms=round(kd["avg_ms"], 5))
+
+    # parity spot-check and CPU baseline on a bounded sample of slices (oracle)
+    cpu = None
+    parity = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        S = max(1, min(args.cpu_slices, BH))
+        Q0, K0, V0 = host_sets[0]
+        flat = lambda t: t.reshape(1, BH, w.n, w.d)[:, :S]
+        Qs, Ks, Vs = (inputs.as_float64(flat(t)) for t in (Q0, K0, V0))
+        threads = oracle.threads()
+        c0 = time.perf_counter()
+        ref = oracle.forward(Qs, Ks, Vs, N, w.iters, scale, w.dtype)
+        cpu_s = time.perf_counter() - c0
+        cpu = dict(value=S * w.n / cpu_s, unit="queries/s", cores=threads, kind="oracle",
+                   sample=f"{S} of {BH} (b,h) slices of input set 0 at full n={w.n}, all {w.iters} grouping "
+                          f"rounds + aggregation + attention, fp64, {cpu_s:.1f} s wall on {threads} threads")
+        O, bel, cnt, cen = ga.forward(*sets[0], N, w.iters, scale, return_groups=True, ws=ws)
+        torch.cuda.synchronize()
+        bel = bel.reshape(1, BH, w.n)[:, :S].cpu().numpy()
+        Og = O.reshape(1, BH, w.n, w.d)[:, :S].float().cpu().numpy().astype(np.float64)
+        rel = float(np.abs(Og - ref["O"]).max() / np.abs(ref["O"]).max())
+        parity = dict(slices=S, assign_mismatches=int((bel != ref["belong"]).sum()),
+                      centroid_bit_exact=bool(np.array_equal(
+                          cen.reshape(1, BH, N, w.d)[:, :S].cpu().numpy(), ref["centroid"])),
+                      out_max_rel_err=rel)
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "queries/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "n": w.n, "d": w.d, "N": N, "iters": w.iters,
+                   "input_sets": 2},
+        "pct_hbm_roofline": pct_hbm, "compulsory_bytes": compulsory,
+        "roofline": roofline, "cpu_baseline": cpu,
+        "kernels": kernels, "ms_per_step_with_kernel_events": ms_timed, "parity_sample": parity,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,155 @@
+/*
+ * ga.h -- C ABI of the MI355X (gfx950) group-attention library, libga.so.
+ *
+ * Group attention is the attention mechanism of RITA ("Group Attention is All
+ * You Need for Timeseries Analytics", Liang et al., arXiv 2306.01926):
+ *
+ *   - Grouping (Section 4.4): the n keys of each (batch, head) slice are
+ *     clustered into N groups by Lloyd K-means iterations; the distance is
+ *     evaluated in the expanded form |c|^2 - 2 k.c so that its bulk is a
+ *     matrix product.  The group centroid is the representative key
+ *     (Section 4.1) and BELONG / COUNT record membership (Algorithm 1 inputs).
+ *   - Embedding aggregation (Section 4.2, Algorithm 1): per-group SUM of the
+ *     value vectors.
+ *   - Group softmax (Eq. 3) and combine (Algorithm 1): for query q_i,
+ *     p_ij = scale * q_i . r_j,  s_i = sum_j COUNT_j exp(p_ij - m_i),
+ *     o_i = sum_j exp(p_ij - m_i) vsum_j / s_i,
+ *     with m_i the largest p_ij over non-empty groups.
+ *
+ * Conventions for every entry point
+ *   - Tensors are dense and row-major with the feature axis innermost:
+ *     Q, K, V, O: [B, H, n, d];  centroid, vsum, init: [B, H, N, d] (fp32);
+ *     belong: [B, H, n] (int32);  count: [B, H, N] (int32).
+ *   - Every pointer except the stream is a DEVICE pointer to memory the
+ *     caller owns and that stays valid until the stream work completes.  The
+ *     library allocates nothing, keeps no pointer after returning, and never
+ *     synchronises: work is enqueued in order on `stream` (a hipStream_t; NULL
+ *     is the default stream), and results are valid once the caller has
+ *     synchronised with that stream.
+ *   - All argument checks run on the host before any HIP call; on failure the
+ *     call returns a status other than GA_OK, enqueues nothing and records a
+ *     message retrievable with ga_last_error() (thread-local).
+ *   - Pointers must be 16-byte aligned; the workspace 256-byte aligned.
+ *   - d must be 64 (GA_ERR_UNSUPPORTED otherwise).  1 <= N <= min(n, 1024);
+ *     the bf16 attention (ga_attend, ga_forward) holds N <= 256 groups on
+ *     chip (GA_ERR_UNSUPPORTED above).  B*H <= 65535.  B = 0 or H = 0 is an
+ *     empty batch: GA_OK, nothing enqueued.  n must be >= 1.
+ *   - Inputs must be finite with |x| < 2^60 (not checked; results undefined
+ *     otherwise).
+ *   - Determinism: repeated calls with the same inputs give identical bits.
+ *
+ * Representatives: R = round_dt(centroid), where round_dt is the identity for
+ * GA_F32 and round-to-nearest-even to bfloat16 for GA_BF16.  R is used both
+ * for assignment and for the attention scores.
+ */
+#ifndef GA_H
+#define GA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { GA_F32 = 0, GA_BF16 = 1 } ga_dtype_t;
+
+typedef enum {
+    GA_OK = 0,
+    GA_ERR_INVALID_ARG = 1, /* bad shape, null/misaligned pointer, N or iters out of range */
+    GA_ERR_UNSUPPORTED = 2, /* valid but not implemented (d != 64) */
+    GA_ERR_WORKSPACE = 3,   /* workspace missing or smaller than ga_workspace_bytes() */
+    GA_ERR_HIP = 4          /* a HIP launch failed; ga_last_error() names it */
+} ga_status_t;
+
+/* Shape of Q/K/V: B batches, H heads, n tokens (windows), d features; dtype
+ * of Q/K/V/O storage (fp32 accumulation for both). */
+typedef struct {
+    int32_t B, H, n, d;
+    int32_t dtype; /* ga_dtype_t */
+} ga_shape_t;
+
+/* Bytes of device workspace any entry point needs for shape s and N groups
+ * (0 if the shape is invalid).  One workspace of this size serves all calls. */
+size_t ga_workspace_bytes(ga_shape_t s, int32_t N);
+
+/*
+ * Grouping (Section 4.4): `iters` rounds of Lloyd K-means on the keys of every
+ * (b, h) slice, independently.
+ *   K         [B,H,n,d] keys in s.dtype.
+ *   N         groups, 1 <= N <= min(n, 1024).   iters >= 1.
+ *   init      optional [B,H,N,d] fp32 initial centroids; NULL selects the
+ *             strided init C0_j = k_{floor(j*n/N)}.
+ *   belong    out [B,H,n]: group of each key, assigned against the
+ *             representatives of the previous round (lowest index on ties of
+ *             the canonical score fma(-2, k.r_j, |r_j|^2) evaluated in fp64).
+ *   count     out [B,H,N]: members per group.
+ *   centroid  out [B,H,N,d] fp32: (float)(fp64 member sum / count); a group
+ *             that ends empty keeps its previous centroid.
+ * belong, count and centroid match the fp64 CPU definition bit for bit.
+ */
+int ga_cluster(ga_shape_t s, const void *K, int32_t N, int32_t iters, const float *init,
+               int32_t *belong, int32_t *count, float *centroid, void *workspace,
+               size_t workspace_bytes, void *stream);
+
+/*
+ * Embedding aggregation (Section 4.2, Algorithm 1): vsum_j = sum of v_i over
+ * the keys i with belong_i == j, accumulated in fp64 in ascending i and
+ * rounded once to fp32.  Entries of belong outside [0, N) are ignored.
+ *   V [B,H,n,d] in s.dtype;  belong [B,H,n];  vsum out [B,H,N,d] fp32.
+ */
+int ga_aggregate(ga_shape_t s, const void *V, const int32_t *belong, int32_t N, float *vsum,
+                 void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Group softmax and combine (Eq. 3, Algorithm 1) for every query.
+ *   Q         [B,H,n,d] in s.dtype.
+ *   centroid  [B,H,N,d] fp32 (representatives are round_dt(centroid)).
+ *   count     [B,H,N]; groups with count <= 0 are left out entirely.
+ *   vsum      [B,H,N,d] fp32 per-group value sums.
+ *   scale     finite score scale (1/sqrt(d) reproduces Eq. 1).
+ *   O         out [B,H,n,d] in s.dtype.  A slice with no non-empty group
+ *             gets zeros.
+ * Accuracy versus the fp64 definition: 1e-4 relative (GA_F32), 2e-2
+ * relative (GA_BF16: bf16 operands, fp32 accumulation).
+ */
+int ga_attend(ga_shape_t s, const void *Q, const float *centroid, const int32_t *count,
+              const float *vsum, int32_t N, float scale, void *O, void *workspace,
+              size_t workspace_bytes, void *stream);
+
+/*
+ * Whole forward: ga_cluster (strided init), ga_aggregate, ga_attend.
+ * belong / count / centroid are optional outputs (NULL: kept internal).
+ */
+int ga_forward(ga_shape_t s, const void *Q, const void *K, const void *V, int32_t N,
+               int32_t iters, float scale, void *O, int32_t *belong, int32_t *count,
+               float *centroid, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Per-kernel timing for measurement tools.  While enabled (per calling
+ * thread), every kernel launch of this library is bracketed by a pair of
+ * hipEvents recorded on the launch stream.  ga_timing_collect waits for the
+ * recorded events, writes up to max_entries per-kernel totals (launch count
+ * and summed event time in milliseconds, in first-launch order), sets
+ * *n_entries and forgets the records.  Timing never changes results.
+ */
+typedef struct {
+    char name[32];
+    int32_t launches;
+    double total_ms;
+} ga_kernel_time_t;
+
+int ga_timing_enable(int on);
+int ga_timing_collect(ga_kernel_time_t *out, int32_t max_entries, int32_t *n_entries);
+
+/* Static description of a status code. */
+const char *ga_status_string(int status);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char *ga_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GA_H */

@@ -1,0 +1,295 @@
+// C ABI of libga.so (declared in include/ga.h): argument validation on the
+// host, workspace carve-up and the launch sequence of each entry point.
+#include "ga.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "ga_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(GA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Shape checks shared by every entry point.  *empty is set for B == 0 or H == 0.
+int check_shape(const ga_shape_t& s, int32_t N, bool* empty) {
+  *empty = false;
+  if (s.dtype != GA_F32 && s.dtype != GA_BF16) return fail(GA_ERR_INVALID_ARG, "unknown dtype %d", s.dtype);
+  if (s.B < 0 || s.H < 0) return fail(GA_ERR_INVALID_ARG, "negative batch/head count (B=%d, H=%d)", s.B, s.H);
+  if (s.n < 1) return fail(GA_ERR_INVALID_ARG, "n must be >= 1 (got %d)", s.n);
+  if (s.d != ga::kD) return fail(GA_ERR_UNSUPPORTED, "only d = 64 is supported (got %d)", s.d);
+  if (N < 1 || N > s.n || N > ga::kMaxGroups)
+    return fail(GA_ERR_INVALID_ARG, "N must satisfy 1 <= N <= min(n, %d) (N=%d, n=%d)", ga::kMaxGroups, N, s.n);
+  const int64_t BH = (int64_t)s.B * s.H;
+  if (BH > 65535) return fail(GA_ERR_UNSUPPORTED, "B*H = %lld exceeds 65535", (long long)BH);
+  if (s.n > (1 << 30)) return fail(GA_ERR_UNSUPPORTED, "n = %d too large", s.n);
+  *empty = BH == 0;
+  return GA_OK;
+}
+
+int check_ptr(const void* p, const char* name, bool required) {
+  if (!p) return required ? fail(GA_ERR_INVALID_ARG, "%s is NULL", name) : GA_OK;
+  if (!aligned16(p)) return fail(GA_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return GA_OK;
+}
+
+int check_ws(const ga::Dims& d, void* ws, size_t bytes, ga::Workspace* w) {
+  const size_t need = ga::workspace_layout(d, nullptr, nullptr);
+  if (!ws) return fail(GA_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (((uintptr_t)ws & 255u) != 0) return fail(GA_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (bytes < need) return fail(GA_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", bytes, need);
+  ga::workspace_layout(d, w, ws);
+  return GA_OK;
+}
+
+ga::Dims dims_of(const ga_shape_t& s, int32_t N) {
+  return ga::Dims{(int64_t)s.B * s.H, s.n, N, s.dtype};
+}
+
+#define GA_TRY(expr)              \
+  do {                            \
+    const int rc_ = (expr);       \
+    if (rc_ != GA_OK) return rc_; \
+  } while (0)
+
+#define GA_LAUNCH(expr, what)                     \
+  do {                                            \
+    const hipError_t e_ = (expr);                 \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+// Grouping on validated arguments.
+int run_cluster(const ga::Dims& d, const void* K, int32_t iters, const float* init, int32_t* belong,
+                int32_t* count, float* C, const ga::Workspace& w, hipStream_t st) {
+  GA_LAUNCH(ga::launch_init(d, K, init, C, w.R, w.nrm64, w.nrm32, st), "init launch");
+  for (int t = 0; t < iters; ++t) {
+    GA_LAUNCH(ga::launch_assign(d, K, w.R, w.nrm32, w.nrm64, w.knorm, belong, t == 0, st), "assign launch");
+    GA_LAUNCH(ga::launch_bucket(d, belong, w.perm, w.goff, count, st), "bucket launch");
+    GA_LAUNCH(ga::launch_update(d, K, w.perm, w.goff, count, C, w.R, w.nrm64, w.nrm32, st), "update launch");
+  }
+  return GA_OK;
+}
+
+// ---------------------------------------------------------------- kernel timing
+struct TimingRec {
+  const char* name;
+  hipEvent_t start, stop;
+};
+struct TimingState {
+  bool on = false;
+  std::vector<TimingRec> recs;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t take() {
+    hipEvent_t e = nullptr;
+    if (!pool.empty()) {
+      e = pool.back();
+      pool.pop_back();
+    } else if (hipEventCreate(&e) != hipSuccess) {
+      e = nullptr;
+    }
+    return e;
+  }
+};
+thread_local TimingState g_timing;
+
+}  // namespace
+
+namespace ga {
+
+TimedLaunch::TimedLaunch(const char* name, hipStream_t st) : slot_(-1), st_(st) {
+  if (!g_timing.on) return;
+  TimingRec r{name, g_timing.take(), g_timing.take()};
+  if (!r.start || !r.stop) return;
+  (void)hipEventRecord(r.start, st);
+  slot_ = (int)g_timing.recs.size();
+  g_timing.recs.push_back(r);
+}
+
+TimedLaunch::~TimedLaunch() {
+  if (slot_ >= 0) (void)hipEventRecord(g_timing.recs[slot_].stop, st_);
+}
+
+}  // namespace ga
+
+extern "C" {
+
+int ga_timing_enable(int on) {
+  g_timing.on = on != 0;
+  return GA_OK;
+}
+
+int ga_timing_collect(ga_kernel_time_t* out, int32_t max_entries, int32_t* n_entries) {
+  std::vector<ga_kernel_time_t> acc;
+  int status = GA_OK;
+  for (const TimingRec& r : g_timing.recs) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.stop);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess && status == GA_OK) status = hip_fail(e, "timing event");
+    size_t k = 0;
+    while (k < acc.size() && strncmp(acc[k].name, r.name, sizeof acc[k].name) != 0) ++k;
+    if (k == acc.size()) {
+      ga_kernel_time_t t{};
+      snprintf(t.name, sizeof t.name, "%s", r.name);
+      acc.push_back(t);
+    }
+    acc[k].launches += 1;
+    acc[k].total_ms += ms;
+    g_timing.pool.push_back(r.start);
+    g_timing.pool.push_back(r.stop);
+  }
+  g_timing.recs.clear();
+  const int32_t m = (int32_t)acc.size() < max_entries ? (int32_t)acc.size() : max_entries;
+  for (int32_t i = 0; i < m; ++i) out[i] = acc[i];
+  if (n_entries) *n_entries = m;
+  return status;
+}
+
+size_t ga_workspace_bytes(ga_shape_t s, int32_t N) {
+  bool empty;
+  const std::string keep = g_last_error;
+  if (check_shape(s, N, &empty) != GA_OK) {
+    g_last_error = keep;
+    return 0;
+  }
+  return ga::workspace_layout(dims_of(s, N), nullptr, nullptr);
+}
+
+int ga_cluster(ga_shape_t s, const void* K, int32_t N, int32_t iters, const float* init, int32_t* belong,
+               int32_t* count, float* centroid, void* workspace, size_t workspace_bytes, void* stream) {
+  bool empty;
+  GA_TRY(check_shape(s, N, &empty));
+  if (iters < 1) return fail(GA_ERR_INVALID_ARG, "iters must be >= 1 (got %d)", iters);
+  GA_TRY(check_ptr(K, "K", true));
+  GA_TRY(check_ptr(init, "init", false));
+  GA_TRY(check_ptr(belong, "belong", true));
+  GA_TRY(check_ptr(count, "count", true));
+  GA_TRY(check_ptr(centroid, "centroid", true));
+  if (empty) return GA_OK;
+  const ga::Dims d = dims_of(s, N);
+  ga::Workspace w;
+  GA_TRY(check_ws(d, workspace, workspace_bytes, &w));
+  return run_cluster(d, K, iters, init, belong, count, centroid, w, (hipStream_t)stream);
+}
+
+int ga_aggregate(ga_shape_t s, const void* V, const int32_t* belong, int32_t N, float* vsum, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  bool empty;
+  GA_TRY(check_shape(s, N, &empty));
+  GA_TRY(check_ptr(V, "V", true));
+  GA_TRY(check_ptr(belong, "belong", true));
+  GA_TRY(check_ptr(vsum, "vsum", true));
+  if (empty) return GA_OK;
+  const ga::Dims d = dims_of(s, N);
+  ga::Workspace w;
+  GA_TRY(check_ws(d, workspace, workspace_bytes, &w));
+  hipStream_t st = (hipStream_t)stream;
+  GA_LAUNCH(ga::launch_bucket(d, belong, w.perm, w.goff, w.count, st), "bucket launch");
+  GA_LAUNCH(ga::launch_valuesum(d, V, w.perm, w.goff, w.count, vsum, st), "value-sum launch");
+  return GA_OK;
+}
+
+int ga_attend(ga_shape_t s, const void* Q, const float* centroid, const int32_t* count, const float* vsum,
+              int32_t N, float scale, void* O, void* workspace, size_t workspace_bytes, void* stream) {
+  bool empty;
+  GA_TRY(check_shape(s, N, &empty));
+  if (!isfinite(scale)) return fail(GA_ERR_INVALID_ARG, "scale must be finite");
+  GA_TRY(check_ptr(Q, "Q", true));
+  GA_TRY(check_ptr(centroid, "centroid", true));
+  GA_TRY(check_ptr(count, "count", true));
+  GA_TRY(check_ptr(vsum, "vsum", true));
+  GA_TRY(check_ptr(O, "O", true));
+  if (s.dtype == GA_BF16 && N > 256)
+    return fail(GA_ERR_UNSUPPORTED, "bf16 attention supports N <= 256 (got %d)", N);
+  if (empty) return GA_OK;
+  const ga::Dims d = dims_of(s, N);
+  ga::Workspace w;
+  GA_TRY(check_ws(d, workspace, workspace_bytes, &w));
+  hipStream_t st = (hipStream_t)stream;
+  if (s.dtype == GA_BF16) {
+    GA_LAUNCH(ga::launch_attend_prep(d, centroid, count, vsum, scale, w.Rq, w.Vt, w.ginit, true, st),
+              "attention prep launch");
+    GA_LAUNCH(ga::launch_attend(d, Q, w.Rq, w.Vt, w.ginit, centroid, count, vsum, scale, O, st),
+              "attention launch");
+  } else {
+    GA_LAUNCH(ga::launch_attend(d, Q, nullptr, nullptr, nullptr, centroid, count, vsum, scale, O, st),
+              "attention launch");
+  }
+  return GA_OK;
+}
+
+int ga_forward(ga_shape_t s, const void* Q, const void* K, const void* V, int32_t N, int32_t iters,
+               float scale, void* O, int32_t* belong, int32_t* count, float* centroid, void* workspace,
+               size_t workspace_bytes, void* stream) {
+  bool empty;
+  GA_TRY(check_shape(s, N, &empty));
+  if (iters < 1) return fail(GA_ERR_INVALID_ARG, "iters must be >= 1 (got %d)", iters);
+  if (!isfinite(scale)) return fail(GA_ERR_INVALID_ARG, "scale must be finite");
+  GA_TRY(check_ptr(Q, "Q", true));
+  GA_TRY(check_ptr(K, "K", true));
+  GA_TRY(check_ptr(V, "V", true));
+  GA_TRY(check_ptr(O, "O", true));
+  GA_TRY(check_ptr(belong, "belong", false));
+  GA_TRY(check_ptr(count, "count", false));
+  GA_TRY(check_ptr(centroid, "centroid", false));
+  if (s.dtype == GA_BF16 && N > 256)
+    return fail(GA_ERR_UNSUPPORTED, "bf16 attention supports N <= 256 (got %d)", N);
+  if (empty) return GA_OK;
+  const ga::Dims d = dims_of(s, N);
+  ga::Workspace w;
+  GA_TRY(check_ws(d, workspace, workspace_bytes, &w));
+  hipStream_t st = (hipStream_t)stream;
+  int32_t* a = belong ? belong : w.belong;
+  int32_t* cnt = count ? count : w.count;
+  float* C = centroid ? centroid : w.C;
+  GA_TRY(run_cluster(d, K, iters, nullptr, a, cnt, C, w, st));
+  // the last bucket pass sorted the keys by the final assignment: reuse it
+  GA_LAUNCH(ga::launch_valuesum(d, V, w.perm, w.goff, cnt, w.vsum, st), "value-sum launch");
+  if (s.dtype == GA_BF16) {
+    GA_LAUNCH(ga::launch_attend_prep(d, C, cnt, w.vsum, scale, w.Rq, w.Vt, w.ginit, false, st),
+              "attention prep launch");
+    GA_LAUNCH(ga::launch_attend(d, Q, w.R, w.Vt, w.ginit, C, cnt, w.vsum, scale, O, st), "attention launch");
+  } else {
+    GA_LAUNCH(ga::launch_attend(d, Q, nullptr, nullptr, nullptr, C, cnt, w.vsum, scale, O, st),
+              "attention launch");
+  }
+  return GA_OK;
+}
+
+const char* ga_status_string(int status) {
+  switch (status) {
+    case GA_OK: return "GA_OK";
+    case GA_ERR_INVALID_ARG: return "GA_ERR_INVALID_ARG";
+    case GA_ERR_UNSUPPORTED: return "GA_ERR_UNSUPPORTED";
+    case GA_ERR_WORKSPACE: return "GA_ERR_WORKSPACE";
+    case GA_ERR_HIP: return "GA_ERR_HIP";
+    default: return "GA_ERR_UNKNOWN";
+  }
+}
+
+const char* ga_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,71 @@
+// Internal interface between the C ABI (ga_abi.cpp) and the gfx950 kernels
+// (ga_kernels.hip).  Every launcher enqueues on `st` and returns the
+// hipError_t of the launch.
+#pragma once
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ga {
+
+constexpr int kD = 64;          // supported feature width
+constexpr int kMaxGroups = 1024;
+
+// Device workspace carved from the caller's buffer (all 256-byte aligned).
+struct Workspace {
+  float* C;          // [BH][N][64] fp32 centroids (used when the caller passes none)
+  void* R;           // [BH][N][64] representatives in the storage dtype
+  double* nrm64;     // [BH][N] canonical fp64 |r_j|^2
+  float* nrm32;      // [BH][N] fp32 rounding of nrm64
+  float* knorm;      // [BH][n] upper bound of |k_i| (bf16 path)
+  int32_t* belong;   // [BH][n]
+  int32_t* perm;     // [BH][n] keys sorted by group, ascending key index inside a group
+  int32_t* goff;     // [BH][N] first position of each group in perm
+  int32_t* count;    // [BH][N]
+  float* vsum;       // [BH][N][64]
+  uint16_t* Rq;      // [BH][N][64] bf16 representatives for the scores
+  uint16_t* Vt;      // [BH][64][vt_stride] bf16 per-group value means, transposed
+  float* ginit;      // [BH][Npad] score-accumulator init, log2(count)/(|scale| log2 e)
+};
+
+struct Dims {
+  int64_t BH;
+  int n, N, dtype;   // dtype: 0 fp32, 1 bf16
+};
+
+// Kernel timing (see ga_timing_enable): brackets one launch with events when
+// enabled on this thread.
+class TimedLaunch {
+ public:
+  TimedLaunch(const char* name, hipStream_t st);
+  ~TimedLaunch();
+
+ private:
+  int slot_;
+  hipStream_t st_;
+};
+
+int vt_stride(int N);  // row stride (elements) of Vt
+size_t workspace_layout(const Dims& d, Workspace* ws, void* base);  // returns bytes
+
+hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C, void* R,
+                       double* nrm64, float* nrm32, hipStream_t st);
+hipError_t launch_assign(const Dims& d, const void* K, const void* R, const float* nrm32,
+                         const double* nrm64, float* knorm, int32_t* belong, bool first,
+                         hipStream_t st);
+hipError_t launch_bucket(const Dims& d, const int32_t* belong, int32_t* perm, int32_t* goff,
+                         int32_t* count, hipStream_t st);
+hipError_t launch_update(const Dims& d, const void* K, const int32_t* perm, const int32_t* goff,
+                         const int32_t* count, float* C, void* R, double* nrm64, float* nrm32,
+                         hipStream_t st);
+hipError_t launch_valuesum(const Dims& d, const void* V, const int32_t* perm,
+                           const int32_t* goff, const int32_t* count, float* vsum,
+                           hipStream_t st);
+hipError_t launch_attend_prep(const Dims& d, const float* centroid, const int32_t* count,
+                              const float* vsum, float scale, uint16_t* Rq, uint16_t* Vt,
+                              float* ginit, bool make_rq, hipStream_t st);
+hipError_t launch_attend(const Dims& d, const void* Q, const void* R, const uint16_t* Vt,
+                         const float* ginit, const float* centroid, const int32_t* count,
+                         const float* vsum, float scale, void* O, hipStream_t st);
+
+}  // namespace ga

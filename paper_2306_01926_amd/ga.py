@@ -1,0 +1,194 @@
+"""Python binding of libga.so: argument marshalling only.
+
+Every function takes torch CUDA tensors, allocates outputs (and a cached
+workspace) with torch, and calls the C ABI declared in include/ga.h on the
+current torch stream.  All computation happens in the HIP kernels; there is no
+CPU fallback: if the library is missing the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libga.so")
+
+GA_F32, GA_BF16 = 0, 1
+STATUS = {0: "GA_OK", 1: "GA_ERR_INVALID_ARG", 2: "GA_ERR_UNSUPPORTED", 3: "GA_ERR_WORKSPACE", 4: "GA_ERR_HIP"}
+SYMBOLS = ("ga_workspace_bytes", "ga_cluster", "ga_aggregate", "ga_attend", "ga_forward",
+           "ga_timing_enable", "ga_timing_collect", "ga_status_string", "ga_last_error")
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("n", ctypes.c_int32),
+                ("d", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class KernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
+
+
+class GAError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libga.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(_LIB_PATH)
+        P, i32 = ctypes.c_void_p, ctypes.c_int32
+        L.ga_workspace_bytes.argtypes = [Shape, i32]
+        L.ga_workspace_bytes.restype = ctypes.c_size_t
+        L.ga_cluster.argtypes = [Shape, P, i32, i32, P, P, P, P, P, ctypes.c_size_t, P]
+        L.ga_aggregate.argtypes = [Shape, P, P, i32, P, P, ctypes.c_size_t, P]
+        L.ga_attend.argtypes = [Shape, P, P, P, P, i32, ctypes.c_float, P, P, ctypes.c_size_t, P]
+        L.ga_forward.argtypes = [Shape, P, P, P, i32, i32, ctypes.c_float, P, P, P, P, P, ctypes.c_size_t, P]
+        for f in ("ga_cluster", "ga_aggregate", "ga_attend", "ga_forward"):
+            getattr(L, f).restype = ctypes.c_int
+        L.ga_timing_enable.argtypes = [ctypes.c_int]
+        L.ga_timing_enable.restype = ctypes.c_int
+        L.ga_timing_collect.argtypes = [ctypes.POINTER(KernelTime), i32, ctypes.POINTER(i32)]
+        L.ga_timing_collect.restype = ctypes.c_int
+        L.ga_status_string.argtypes = [ctypes.c_int]
+        L.ga_status_string.restype = ctypes.c_char_p
+        L.ga_last_error.argtypes = []
+        L.ga_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return GA_BF16
+    if t.dtype == torch.float32:
+        return GA_F32
+    raise TypeError(f"unsupported dtype {t.dtype} (bf16 or fp32)")
+
+
+def shape_of(X: torch.Tensor) -> Shape:
+    if X.dim() != 4:
+        raise ValueError("expected a [B, H, n, d] tensor")
+    B, H, n, d = X.shape
+    return Shape(B, H, n, d, _dtype_code(X))
+
+
+def _p(t):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise GAError(rc, lib().ga_last_error().decode())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+_ws_cache: dict = {}
+
+
+def workspace_bytes(shape: Shape, N: int) -> int:
+    return int(lib().ga_workspace_bytes(shape, int(N)))
+
+
+def workspace(shape: Shape, N: int, device) -> tuple:
+    """A cached device workspace (uint8 tensor) large enough for (shape, N)."""
+    nbytes = max(workspace_bytes(shape, N), 256)
+    key = torch.device(device)
+    ws = _ws_cache.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        _ws_cache[key] = ws
+    return ws, ws.numel()
+
+
+def _ws_args(shape, N, device, ws):
+    if ws is None:
+        ws, nb = workspace(shape, N, device)
+    else:
+        nb = ws.numel() * ws.element_size()
+    return _p(ws), nb
+
+
+def cluster(K: torch.Tensor, N: int, iters: int, init: torch.Tensor | None = None, ws=None):
+    """Grouping of the keys: returns (belong [B,H,n] int32, count [B,H,N] int32,
+    centroid [B,H,N,d] fp32)."""
+    s = shape_of(K)
+    dev = K.device
+    belong = torch.empty(K.shape[:3], dtype=torch.int32, device=dev)
+    count = torch.empty((*K.shape[:2], N), dtype=torch.int32, device=dev)
+    centroid = torch.empty((*K.shape[:2], N, K.shape[3]), dtype=torch.float32, device=dev)
+    wp, nb = _ws_args(s, N, dev, ws)
+    _check(lib().ga_cluster(s, _p(K), int(N), int(iters), _p(init), _p(belong), _p(count), _p(centroid),
+                            wp, nb, _stream(dev)))
+    return belong, count, centroid
+
+
+def aggregate(V: torch.Tensor, belong: torch.Tensor, N: int, ws=None) -> torch.Tensor:
+    """Per-group fp32 sums of the values (fp64 accumulation)."""
+    s = shape_of(V)
+    dev = V.device
+    vsum = torch.empty((*V.shape[:2], N, V.shape[3]), dtype=torch.float32, device=dev)
+    wp, nb = _ws_args(s, N, dev, ws)
+    _check(lib().ga_aggregate(s, _p(V), _p(belong), int(N), _p(vsum), wp, nb, _stream(dev)))
+    return vsum
+
+
+def attend(Q: torch.Tensor, centroid: torch.Tensor, count: torch.Tensor, vsum: torch.Tensor, N: int,
+           scale: float | None = None, ws=None) -> torch.Tensor:
+    """Group softmax and combine; returns O [B,H,n,d] in Q's dtype."""
+    s = shape_of(Q)
+    dev = Q.device
+    scale = 1.0 / math.sqrt(Q.shape[3]) if scale is None else float(scale)
+    O = torch.empty_like(Q)
+    wp, nb = _ws_args(s, N, dev, ws)
+    _check(lib().ga_attend(s, _p(Q), _p(centroid), _p(count), _p(vsum), int(N), scale, _p(O), wp, nb,
+                           _stream(dev)))
+    return O
+
+
+def forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, N: int, iters: int,
+            scale: float | None = None, return_groups: bool = False, out: torch.Tensor | None = None,
+            ws=None):
+    """Whole group-attention forward; optionally also (belong, count, centroid)."""
+    s = shape_of(Q)
+    dev = Q.device
+    scale = 1.0 / math.sqrt(Q.shape[3]) if scale is None else float(scale)
+    O = torch.empty_like(Q) if out is None else out
+    belong = count = centroid = None
+    if return_groups:
+        belong = torch.empty(K.shape[:3], dtype=torch.int32, device=dev)
+        count = torch.empty((*K.shape[:2], N), dtype=torch.int32, device=dev)
+        centroid = torch.empty((*K.shape[:2], N, K.shape[3]), dtype=torch.float32, device=dev)
+    wp, nb = _ws_args(s, N, dev, ws)
+    _check(lib().ga_forward(s, _p(Q), _p(K), _p(V), int(N), int(iters), scale, _p(O), _p(belong), _p(count),
+                            _p(centroid), wp, nb, _stream(dev)))
+    return (O, belong, count, centroid) if return_groups else O
+
+
+def timing_enable(on: bool = True) -> None:
+    """Bracket every kernel launch (this thread) with hipEvents on its stream."""
+    _check(lib().ga_timing_enable(1 if on else 0))
+
+
+def timing_collect() -> dict:
+    """{kernel: (launches, total_ms)} since the last collect; waits for the events."""
+    buf = (KernelTime * 64)()
+    n = ctypes.c_int32(0)
+    _check(lib().ga_timing_collect(buf, 64, ctypes.byref(n)))
+    return {buf[i].name.decode(): (int(buf[i].launches), float(buf[i].total_ms)) for i in range(n.value)}

@@ -1,0 +1,107 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+libga.so must load and export every function include/ga.h declares.  Every
+argument check runs on the host before any HIP call, so each error status can
+be forced here with fake (never dereferenced) device pointers.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2306_01926_amd import ga
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000000  # 16-byte aligned, never dereferenced (validation returns first)
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "ga.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ga_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = ga.lib()
+    names = header_functions()
+    assert set(names) == set(ga.SYMBOLS)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def P(x=FAKE):
+    return ctypes.c_void_p(x)
+
+
+def shape(B=2, H=2, n=100, d=64, dtype=ga.GA_BF16):
+    return ga.Shape(B, H, n, d, dtype)
+
+
+def call_forward(s, N=8, iters=2, scale=0.125, Q=FAKE, K=FAKE, V=FAKE, O=FAKE, belong=None, ws=FAKE,
+                 ws_bytes=None):
+    L = ga.lib()
+    if ws_bytes is None:
+        ws_bytes = max(L.ga_workspace_bytes(s, N), 1)
+    return L.ga_forward(s, P(Q), P(K), P(V), N, iters, scale, P(O), None if belong is None else P(belong), None,
+                        None, P(ws) if ws else None, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(s=shape(dtype=7)), 1),
+    (dict(s=shape(B=-1)), 1),
+    (dict(s=shape(n=0)), 1),
+    (dict(s=shape(d=32)), 2),
+    (dict(s=shape(), N=0), 1),
+    (dict(s=shape(n=10), N=11), 1),
+    (dict(s=shape(n=5000), N=1025), 1),
+    (dict(s=shape(), iters=0), 1),
+    (dict(s=shape(), scale=float("inf")), 1),
+    (dict(s=shape(), scale=float("nan")), 1),
+    (dict(s=shape(), Q=0), 1),
+    (dict(s=shape(), K=FAKE + 4), 1),
+    (dict(s=shape(), belong=FAKE + 8), 1),
+    (dict(s=shape(), ws=0), 3),
+    (dict(s=shape(), ws=FAKE + 16), 3),
+    (dict(s=shape(), ws_bytes=1000), 3),
+    (dict(s=shape(B=300, H=300)), 2),
+    (dict(s=shape(n=1000), N=300), 2),  # bf16 attention keeps N <= 256 groups on chip
+])
+def test_forward_argument_errors(kw, status):
+    rc = call_forward(**kw)
+    assert rc == status, ga.lib().ga_last_error().decode()
+    assert ga.lib().ga_last_error().decode() != ""
+    assert ga.lib().ga_status_string(rc).decode() == ga.STATUS[status]
+
+
+def test_empty_batch_is_a_no_op():
+    assert call_forward(shape(B=0)) == 0
+    assert call_forward(shape(H=0), ws=0) == 0
+
+
+def test_other_entry_points_validate():
+    L = ga.lib()
+    s = shape()
+    nb = L.ga_workspace_bytes(s, 8)
+    assert L.ga_cluster(s, P(), 8, 0, None, P(), P(), P(), P(), nb, None) == 1          # iters
+    assert L.ga_cluster(s, P(), 8, 3, P(FAKE + 4), P(), P(), P(), P(), nb, None) == 1   # init misaligned
+    assert L.ga_cluster(s, P(), 8, 3, None, None, P(), P(), P(), nb, None) == 1          # belong NULL
+    assert L.ga_cluster(s, P(), 8, 3, None, P(), P(), P(), P(), 10, None) == 3           # workspace
+    assert L.ga_aggregate(s, P(), None, 8, P(), P(), nb, None) == 1
+    assert L.ga_aggregate(shape(d=128), P(), P(), 8, P(), P(), nb, None) == 2
+    assert L.ga_attend(s, P(), P(), P(), P(), 8, float("nan"), P(), P(), nb, None) == 1
+    assert L.ga_attend(s, P(), P(), None, P(), 8, 1.0, P(), P(), nb, None) == 1
+    assert L.ga_attend(shape(dtype=ga.GA_F32), P(), P(), P(), P(), 8, 1.0, P(), P(), 10, None) == 3
+
+
+def test_workspace_bytes():
+    L = ga.lib()
+    assert L.ga_workspace_bytes(shape(d=32), 8) == 0
+    assert L.ga_workspace_bytes(shape(), 0) == 0
+    a = L.ga_workspace_bytes(shape(n=100), 8)
+    b = L.ga_workspace_bytes(shape(n=200), 8)
+    c = L.ga_workspace_bytes(shape(n=200), 64)
+    assert 0 < a < b < c
+    # the metric workload's workspace stays modest next to 288 GB of HBM
+    big = L.ga_workspace_bytes(ga.Shape(16, 8, 8000, 64, ga.GA_BF16), 128)
+    assert big < 64 * 2**20

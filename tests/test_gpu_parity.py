@@ -1,0 +1,263 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bars: group assignments, counts and fp32 centroids bit-exact; value sums equal
+to the fp32 rounding of the oracle's fp64 sums; outputs within 1e-4 (fp32) or
+2e-2 (bf16) relative, both per (b, h) slice (max |err| / max |ref|) and per
+row (||err_i|| / ||ref_i||).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2306_01926_amd import ga, inputs
+
+pytestmark = pytest.mark.gpu
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    ga.lib()
+    return torch.device("cuda:0")
+
+
+def say(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+def f64(t):
+    return inputs.as_float64(t)
+
+
+def check_close(O_gpu, O_ref, tol):
+    Og = O_gpu.float().cpu().numpy().astype(np.float64)
+    err = np.abs(Og - O_ref)
+    B, H = O_ref.shape[:2]
+    worst = 0.0
+    for b in range(B):
+        for h in range(H):
+            den = np.abs(O_ref[b, h]).max()
+            r = err[b, h].max() / den if den > 0 else err[b, h].max()
+            worst = max(worst, r)
+            assert r <= tol, f"slice ({b},{h}) max relative error {r:.3g} > {tol}"
+    rn = np.linalg.norm(O_ref, axis=-1)
+    en = np.linalg.norm(Og - O_ref, axis=-1)
+    scale = np.abs(O_ref).max()
+    bad = en > tol * np.where(rn > 0, rn, scale)
+    assert not bad.any(), f"{bad.sum()} rows exceed relative error {tol}"
+    return worst
+
+
+def cluster_both(oracle_mod, K, N, iters, dtype, dev, init=None, trace=False):
+    bel, cnt, cen = ga.cluster(K.to(dev), N, iters, init=None if init is None else init.to(dev))
+    torch.cuda.synchronize()
+    ref = oracle_mod.cluster(f64(K), N, iters, dtype, init=None if init is None else init.numpy(), trace=trace)
+    return (bel.cpu().numpy(), cnt.cpu().numpy(), cen.cpu().numpy()), ref
+
+
+def assert_groups_equal(got, ref):
+    bel, cnt, cen = got
+    mism = (bel != ref["belong"]).sum()
+    assert mism == 0, f"{mism} assignments differ"
+    assert np.array_equal(cnt, ref["count"]), "counts differ"
+    assert np.array_equal(cen.view(np.uint32), ref["centroid"].view(np.uint32)), "centroids differ"
+
+
+CLUSTER_CASES = [
+    # dtype, B, H, n, N, iters, M (mixture components), sigma range
+    ("bf16", 1, 2, 300, 16, 3, 12, (0.05, 0.3)),
+    ("bf16", 2, 2, 1000, 64, 5, 64, (0.05, 0.3)),
+    ("bf16", 1, 1, 97, 32, 4, 8, (0.1, 0.1)),        # ragged tail, n < 4 tiles
+    ("bf16", 1, 2, 31, 31, 2, 4, (0.3, 0.3)),        # N = n < 32
+    ("bf16", 1, 1, 64, 64, 2, 8, (0.2, 0.2)),        # N = n, full tiles
+    ("bf16", 1, 1, 600, 1, 2, 8, (0.2, 0.2)),        # one group
+    ("bf16", 1, 1, 2000, 256, 3, 256, (0.05, 0.3)),
+    ("bf16", 1, 1, 1500, 1024, 2, 256, (0.05, 0.3)), # largest N
+    ("bf16", 1, 1, 4000, 100, 4, 300, (0.3, 0.3)),   # N not a multiple of 32, heavy overlap
+    ("f32", 1, 1, 512, 32, 5, 32, (0.05, 0.05)),     # the fp32 workload at full size
+    ("f32", 1, 2, 200, 20, 4, 30, (0.05, 0.3)),
+    ("f32", 1, 1, 130, 130, 2, 8, (0.1, 0.1)),
+]
+
+
+@pytest.mark.parametrize("case", CLUSTER_CASES, ids=lambda c: "-".join(map(str, c[:6])))
+def test_cluster_bit_exact(oracle_mod, dev, case):
+    dtype, B, H, n, N, iters, M, (slo, shi) = case
+    say(f"cluster {case}")
+    _, K, _ = inputs.make_qkv(B, H, n, 64, dtype, 1000 + n + N, M, slo, shi)
+    got, ref = cluster_both(oracle_mod, K, N, iters, dtype, dev)
+    assert_groups_equal(got, ref)
+
+
+def test_cluster_with_caller_init(oracle_mod, dev):
+    say("cluster with caller init")
+    _, K, _ = inputs.make_qkv(2, 1, 700, 64, "bf16", 5, 40, 0.05, 0.3)
+    init = torch.from_numpy(np.random.default_rng(0).standard_normal((2, 1, 40, 64)).astype(np.float32) * 0.2)
+    got, ref = cluster_both(oracle_mod, K, 40, 3, "bf16", dev, init=init)
+    assert_groups_equal(got, ref)
+
+
+def test_cluster_stepwise_against_trace(oracle_mod, dev):
+    """Round t fed the oracle's C^(t-1): isolates each round from earlier ones."""
+    say("stepwise cluster rounds")
+    _, K, _ = inputs.make_qkv(2, 2, 2000, 64, "bf16", 7, 128, 0.05, 0.3)
+    T = 6
+    ref = oracle_mod.cluster(f64(K), 128, T, "bf16", trace=True)
+    Kd = K.to(dev)
+    n, N = 2000, 128
+    prev = np.ascontiguousarray(f64(K)[:, :, (np.arange(N) * n) // N, :].astype(np.float32))
+    for t in range(T):
+        bel, cnt, cen = ga.cluster(Kd, N, 1, init=torch.from_numpy(prev).to(dev))
+        torch.cuda.synchronize()
+        assert np.array_equal(bel.cpu().numpy(), ref["trace_belong"][t]), f"round {t}"
+        assert np.array_equal(cen.cpu().numpy().view(np.uint32), ref["trace_centroid"][t].view(np.uint32))
+        prev = ref["trace_centroid"][t]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_aggregate_bit_exact(oracle_mod, dev, dtype):
+    say(f"aggregate {dtype}")
+    rng = np.random.default_rng(3)
+    B, H, n, N = 2, 3, 1500, 70
+    _, _, V = inputs.make_qkv(B, H, n, 64, dtype, 9, 8, 0.1, 0.1)
+    belong = rng.integers(0, N - 3, size=(B, H, n)).astype(np.int32)
+    belong[0, 0, 5] = -1       # ignored
+    belong[1, 2, 7] = N        # ignored
+    vs = ga.aggregate(V.to(dev), torch.from_numpy(belong).to(dev), N)
+    torch.cuda.synchronize()
+    ref, _ = oracle_mod.aggregate(f64(V), belong, N)
+    assert np.array_equal(vs.cpu().numpy().view(np.uint32), ref.astype(np.float32).view(np.uint32))
+
+
+ATTEND_CASES = [
+    ("bf16", 2, 2, 1000, 64, 0.125),
+    ("bf16", 1, 2, 97, 33, 0.125),     # ragged tiles, partial group block
+    ("bf16", 1, 1, 3000, 256, 0.125),
+    ("bf16", 1, 2, 500, 40, -0.3),     # negative scale
+    ("bf16", 1, 1, 300, 20, 0.0),      # zero scale: o_i = mean of values
+    ("bf16", 1, 1, 400, 50, 2.0),      # sharp softmax
+    ("f32", 1, 1, 512, 32, 0.125),
+    ("f32", 2, 1, 333, 100, -0.7),
+]
+
+
+@pytest.mark.parametrize("case", ATTEND_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_attend_given_groups(oracle_mod, dev, case):
+    """Random groupings with empty groups and non-representable centroids."""
+    dtype, B, H, n, N, scale = case
+    say(f"attend {case}")
+    rng = np.random.default_rng(n + N)
+    Q, _, V = inputs.make_qkv(B, H, n, 64, dtype, 11, 8, 0.1, 0.1)
+    belong = rng.integers(0, max(N - 5, 1), size=(B, H, n)).astype(np.int32)   # last groups empty
+    count = np.stack([[np.bincount(belong[b, h], minlength=N) for h in range(H)] for b in range(B)]).astype(np.int32)
+    centroid = (0.3 * rng.standard_normal((B, H, N, 64))).astype(np.float32)
+    vsum, _ = oracle_mod.aggregate(f64(V), belong, N)
+    vsum32 = vsum.astype(np.float32)
+    O = ga.attend(Q.to(dev), torch.from_numpy(centroid).to(dev), torch.from_numpy(count).to(dev),
+                  torch.from_numpy(vsum32).to(dev), N, scale)
+    torch.cuda.synchronize()
+    ref = oracle_mod.attend(f64(Q), centroid, count, vsum32, N, scale, dtype)
+    check_close(O, ref, TOL[dtype])
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_attend_all_groups_empty_gives_zeros(dev, dtype):
+    say(f"attend all-empty {dtype}")
+    Q, _, _ = inputs.make_qkv(1, 2, 100, 64, dtype, 1, 4, 0.1, 0.1)
+    N = 8
+    count = torch.zeros((1, 2, N), dtype=torch.int32)
+    count[0, 1, 3] = 100
+    cen = torch.randn(1, 2, N, 64)
+    vs = torch.randn(1, 2, N, 64)
+    O = ga.attend(Q.to(dev), cen.to(dev), count.to(dev), vs.to(dev), N, 0.125)
+    torch.cuda.synchronize()
+    O = O.float().cpu()
+    assert (O[0, 0] == 0).all()
+    want = (vs[0, 1, 3] / 100).to(Q.dtype).float()
+    assert torch.allclose(O[0, 1], want.expand(100, 64), rtol=TOL[dtype], atol=1e-6)
+
+
+FORWARD_CASES = [
+    ("bf16", 2, 2, 1200, 64, 4),
+    ("bf16", 1, 3, 555, 50, 3),
+    ("bf16", 1, 1, 96, 96, 2),      # N = n: exact attention
+    ("f32", 1, 1, 512, 32, 5),      # the fp32 workload at full size
+    ("f32", 1, 2, 100, 100, 2),     # N = n
+]
+
+
+@pytest.mark.parametrize("case", FORWARD_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_forward_end_to_end(oracle_mod, dev, case):
+    dtype, B, H, n, N, iters = case
+    say(f"forward {case}")
+    M = max(4, N // 2)
+    Q, K, V = inputs.make_qkv(B, H, n, 64, dtype, 21 + n, M, 0.05, 0.3)
+    O, bel, cnt, cen = ga.forward(Q.to(dev), K.to(dev), V.to(dev), N, iters, return_groups=True)
+    torch.cuda.synchronize()
+    ref = oracle_mod.forward(f64(Q), f64(K), f64(V), N, iters, 1 / 8, dtype)
+    assert_groups_equal((bel.cpu().numpy(), cnt.cpu().numpy(), cen.cpu().numpy()), ref)
+    check_close(O, ref["O"], TOL[dtype])
+    if N == n:  # every key its own group: Eq. 1 exactly
+        Qd, Kd, Vd = f64(Q), f64(K), f64(V)
+        P = np.einsum("bhid,bhjd->bhij", Qd, Kd) / 8
+        A = np.exp(P - P.max(-1, keepdims=True))
+        A /= A.sum(-1, keepdims=True)
+        check_close(O, np.einsum("bhij,bhjd->bhid", A, Vd), TOL[dtype])
+
+
+def test_forward_is_deterministic(dev):
+    say("determinism")
+    Q, K, V = inputs.make_qkv(2, 2, 3000, 64, "bf16", 3, 128, 0.05, 0.3)
+    Qd, Kd, Vd = Q.to(dev), K.to(dev), V.to(dev)
+    a = ga.forward(Qd, Kd, Vd, 128, 6, return_groups=True)
+    b = ga.forward(Qd, Kd, Vd, 128, 6, return_groups=True)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x.view(torch.uint8) if x.dtype == torch.bfloat16 else x,
+                           y.view(torch.uint8) if y.dtype == torch.bfloat16 else y)
+
+
+def _sampled_full_size(oracle_mod, dev, w, seed, N, slices, queries=512):
+    """Full-size forward; oracle on a few (b, h) slices (assignments) and sampled queries."""
+    Q, K, V = inputs.workload_inputs(w, seed)
+    O, bel, cnt, cen = ga.forward(Q.to(dev), K.to(dev), V.to(dev), N, w.iters, return_groups=True)
+    torch.cuda.synchronize()
+    O, bel, cnt, cen = O.cpu(), bel.cpu().numpy(), cnt.cpu().numpy(), cen.cpu().numpy()
+    rng = np.random.default_rng(seed)
+    for (b, h) in slices:
+        Ks = f64(K[b:b + 1, h:h + 1])
+        ref = oracle_mod.cluster(Ks, N, w.iters, w.dtype)
+        assert_groups_equal((bel[b:b + 1, h:h + 1], cnt[b:b + 1, h:h + 1], cen[b:b + 1, h:h + 1]), ref)
+        vsum, _ = oracle_mod.aggregate(f64(V[b:b + 1, h:h + 1]), ref["belong"], N)
+        qi = np.sort(rng.choice(w.n, size=queries, replace=False))
+        Oref = oracle_mod.attend(f64(Q[b:b + 1, h:h + 1, qi]), ref["centroid"], ref["count"], vsum, N,
+                                 1 / math.sqrt(w.d), w.dtype)
+        check_close(O[b:b + 1, h:h + 1, qi], Oref, TOL[w.dtype])
+
+
+def test_full_size_n2000_all_slices(oracle_mod, dev):
+    w = inputs.WORKLOADS["n2000_N64_bf16"]
+    say(f"full size {w.name}, every slice")
+    Q, K, V = inputs.workload_inputs(w, 0)
+    O, bel, cnt, cen = ga.forward(Q.to(dev), K.to(dev), V.to(dev), w.N, w.iters, return_groups=True)
+    torch.cuda.synchronize()
+    ref = oracle_mod.forward(f64(Q), f64(K), f64(V), w.N, w.iters, 1 / 8, w.dtype)
+    assert_groups_equal((bel.cpu().numpy(), cnt.cpu().numpy(), cen.cpu().numpy()), ref)
+    check_close(O, ref["O"], TOL[w.dtype])
+
+
+def test_full_size_n8000_sampled_slices(oracle_mod, dev):
+    w = inputs.WORKLOADS["n8000_N128_bf16"]
+    say(f"full size {w.name}, sampled slices")
+    _sampled_full_size(oracle_mod, dev, w, 0, w.N, [(0, 0), (7, 3), (15, 7)])
+
+
+def test_full_size_n20000_varying_groups(oracle_mod, dev):
+    w = inputs.WORKLOADS["n20000_Nvar_bf16"]
+    for call in range(2):
+        N = inputs.draw_group_count(w, 0, call)
+        say(f"full size {w.name}, call {call}, N={N}")
+        _sampled_full_size(oracle_mod, dev, w, call, N, [(0, 0), (3, 7)], queries=256)
