@@ -82,13 +82,44 @@ ga::Dims dims_of(const ga_shape_t& s, int32_t N) {
   } while (0)
 
 // Grouping on validated arguments.
+// bf16: the first round sums every member; later rounds apply only the keys
+// that changed group (exact fp64 sums make the order irrelevant).  fp32: every
+// round re-sums the members in ascending key order (fp32 sums need not be exact).
 int run_cluster(const ga::Dims& d, const void* K, int32_t iters, const float* init, int32_t* belong,
                 int32_t* count, float* C, const ga::Workspace& w, hipStream_t st) {
-  GA_LAUNCH(ga::launch_init(d, K, init, C, w.R, w.nrm64, w.nrm32, st), "init launch");
+  GA_LAUNCH(ga::launch_init(d, K, init, C, w.R, w.nrm64, w.nsplit, w.mcount, st), "init launch");
   for (int t = 0; t < iters; ++t) {
-    GA_LAUNCH(ga::launch_assign(d, K, w.R, w.nrm32, w.nrm64, w.knorm, belong, t == 0, st), "assign launch");
+    GA_LAUNCH(ga::launch_assign(d, K, w.R, w.nsplit, w.nrm64, w.knorm, belong, w.mcount, w.mrec, t == 0, st),
+              "assign launch");
+    if (d.dtype == GA_BF16) {
+      if (t == 0) {
+        GA_LAUNCH(ga::launch_full_bucket(d, belong, w.perm, w.grp, count, st), "bucket launch");
+        GA_LAUNCH(ga::launch_segsum_bf16(d, 0, K, w.perm, w.llist, w.grp, count, w.S64, C, w.R, w.nrm64,
+                                         w.nsplit, st), "update launch");
+      } else {
+        GA_LAUNCH(ga::launch_moved_bucket(d, w.mrec, w.mcount, w.perm, w.llist, w.grp, count, st),
+                  "bucket launch");
+        GA_LAUNCH(ga::launch_segsum_bf16(d, 1, K, w.perm, w.llist, w.grp, count, w.S64, C, w.R, w.nrm64,
+                                         w.nsplit, st), "update launch");
+      }
+    } else {
+      GA_LAUNCH(ga::launch_bucket(d, belong, w.perm, w.goff, count, st), "bucket launch");
+      GA_LAUNCH(ga::launch_update(d, K, w.perm, w.goff, count, C, w.R, w.nrm64, w.nsplit, st), "update launch");
+    }
+  }
+  return GA_OK;
+}
+
+// Value sums for the current assignment.
+int run_valuesum(const ga::Dims& d, const void* V, const int32_t* belong, int32_t* count, float* vsum,
+                 const ga::Workspace& w, hipStream_t st) {
+  if (d.dtype == GA_BF16) {
+    GA_LAUNCH(ga::launch_full_bucket(d, belong, w.perm, w.grp, count, st), "bucket launch");
+    GA_LAUNCH(ga::launch_segsum_bf16(d, 2, V, w.perm, w.llist, w.grp, count, w.S64, vsum, nullptr, nullptr,
+                                     nullptr, st), "value-sum launch");
+  } else {
     GA_LAUNCH(ga::launch_bucket(d, belong, w.perm, w.goff, count, st), "bucket launch");
-    GA_LAUNCH(ga::launch_update(d, K, w.perm, w.goff, count, C, w.R, w.nrm64, w.nrm32, st), "update launch");
+    GA_LAUNCH(ga::launch_valuesum(d, V, w.perm, w.goff, count, vsum, st), "value-sum launch");
   }
   return GA_OK;
 }
@@ -206,10 +237,7 @@ int ga_aggregate(ga_shape_t s, const void* V, const int32_t* belong, int32_t N, 
   const ga::Dims d = dims_of(s, N);
   ga::Workspace w;
   GA_TRY(check_ws(d, workspace, workspace_bytes, &w));
-  hipStream_t st = (hipStream_t)stream;
-  GA_LAUNCH(ga::launch_bucket(d, belong, w.perm, w.goff, w.count, st), "bucket launch");
-  GA_LAUNCH(ga::launch_valuesum(d, V, w.perm, w.goff, w.count, vsum, st), "value-sum launch");
-  return GA_OK;
+  return run_valuesum(d, V, belong, w.count, vsum, w, (hipStream_t)stream);
 }
 
 int ga_attend(ga_shape_t s, const void* Q, const float* centroid, const int32_t* count, const float* vsum,
@@ -266,8 +294,12 @@ int ga_forward(ga_shape_t s, const void* Q, const void* K, const void* V, int32_
   int32_t* cnt = count ? count : w.count;
   float* C = centroid ? centroid : w.C;
   GA_TRY(run_cluster(d, K, iters, nullptr, a, cnt, C, w, st));
-  // the last bucket pass sorted the keys by the final assignment: reuse it
-  GA_LAUNCH(ga::launch_valuesum(d, V, w.perm, w.goff, cnt, w.vsum, st), "value-sum launch");
+  if (d.dtype == GA_BF16) {
+    GA_TRY(run_valuesum(d, V, a, nullptr, w.vsum, w, st));
+  } else {
+    // the last stable bucket pass sorted the keys by the final assignment: reuse it
+    GA_LAUNCH(ga::launch_valuesum(d, V, w.perm, w.goff, cnt, w.vsum, st), "value-sum launch");
+  }
   if (s.dtype == GA_BF16) {
     GA_LAUNCH(ga::launch_attend_prep(d, C, cnt, w.vsum, scale, w.Rq, w.Vt, w.ginit, false, st),
               "attention prep launch");

@@ -16,7 +16,7 @@ struct Workspace {
   float* C;          // [BH][N][64] fp32 centroids (used when the caller passes none)
   void* R;           // [BH][N][64] representatives in the storage dtype
   double* nrm64;     // [BH][N] canonical fp64 |r_j|^2
-  float* nrm32;      // [BH][N] fp32 rounding of nrm64
+  uint16_t* nsplit;  // [BH][N][8] bf16 hi, mid, lo with hi + mid + lo ~ nrm64 (rest zero)
   float* knorm;      // [BH][n] upper bound of |k_i| (bf16 path)
   int32_t* belong;   // [BH][n]
   int32_t* perm;     // [BH][n] keys sorted by group, ascending key index inside a group
@@ -26,6 +26,11 @@ struct Workspace {
   uint16_t* Rq;      // [BH][N][64] bf16 representatives for the scores
   uint16_t* Vt;      // [BH][64][vt_stride] bf16 per-group value means, transposed
   float* ginit;      // [BH][Npad] score-accumulator init, log2(count)/(|scale| log2 e)
+  double* S64;       // [BH][N][64] fp64 member sums carried across rounds (bf16 path)
+  int32_t* mcount;   // [BH] moved-key records of the current round
+  unsigned long long* mrec;  // [BH][n] records (key << 32 | old << 16 | new)
+  int4* grp;         // [BH][N] {first join, joins, first leave, leaves} (or {first, members, 0, 0})
+  int32_t* llist;    // [BH][n] keys leaving each group (joins / full lists use perm)
 };
 
 struct Dims {
@@ -49,14 +54,24 @@ int vt_stride(int N);  // row stride (elements) of Vt
 size_t workspace_layout(const Dims& d, Workspace* ws, void* base);  // returns bytes
 
 hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C, void* R,
-                       double* nrm64, float* nrm32, hipStream_t st);
-hipError_t launch_assign(const Dims& d, const void* K, const void* R, const float* nrm32,
-                         const double* nrm64, float* knorm, int32_t* belong, bool first,
-                         hipStream_t st);
+                       double* nrm64, uint16_t* nsplit, int32_t* mcount, hipStream_t st);
+hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint16_t* nsplit,
+                         const double* nrm64, float* knorm, int32_t* belong, int32_t* mcount,
+                         unsigned long long* mrec, bool first, hipStream_t st);
+// bf16 path: order-free bucketing and segmented sums (see ga_kernels.hip)
+hipError_t launch_full_bucket(const Dims& d, const int32_t* belong, int32_t* list, int4* grp,
+                              int32_t* count, hipStream_t st);
+hipError_t launch_moved_bucket(const Dims& d, const unsigned long long* mrec, int32_t* mcount,
+                               int32_t* jlist, int32_t* llist, int4* grp, int32_t* count,
+                               hipStream_t st);
+hipError_t launch_segsum_bf16(const Dims& d, int mode, const void* X, const int32_t* jlist,
+                              const int32_t* llist, const int4* grp, const int32_t* count,
+                              double* S64, float* out, void* R, double* nrm64, uint16_t* nsplit,
+                              hipStream_t st);
 hipError_t launch_bucket(const Dims& d, const int32_t* belong, int32_t* perm, int32_t* goff,
                          int32_t* count, hipStream_t st);
 hipError_t launch_update(const Dims& d, const void* K, const int32_t* perm, const int32_t* goff,
-                         const int32_t* count, float* C, void* R, double* nrm64, float* nrm32,
+                         const int32_t* count, float* C, void* R, double* nrm64, uint16_t* nsplit,
                          hipStream_t st);
 hipError_t launch_valuesum(const Dims& d, const void* V, const int32_t* perm,
                            const int32_t* goff, const int32_t* count, float* vsum,

@@ -71,6 +71,19 @@ struct BF16 {
   __device__ static void store(uint16_t* p, int64_t i, float r) { p[i] = (uint16_t)(__float_as_uint(r) >> 16); }
 };
 
+// min / max of finite scores as a median of three with -FLT_MAX / FLT_MAX:
+// one v_med3_f32 each, without the NaN canonicalisation fminf / fmaxf need.
+__device__ __forceinline__ float min2(float a, float b) { return __builtin_amdgcn_fmed3f(a, b, -FLT_MAX); }
+__device__ __forceinline__ float max2(float a, float b) { return __builtin_amdgcn_fmed3f(a, b, FLT_MAX); }
+
+// v_min3_f32 without the NaN canonicalisation the compiler adds around
+// fminf-based min3 (the operands are finite scores).
+__device__ __forceinline__ float min3f(float a, float b, float c) {
+  float r;
+  asm("v_min3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 __device__ __forceinline__ float readlane_f(float x, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
 }
@@ -86,16 +99,28 @@ __device__ double canon_nrm_wave(float r) {
   return acc;
 }
 
+// |r|^2 as three bf16 terms hi + mid + lo (each the bf16 rounding of the
+// remainder; the two subtractions are exact), |sum - nrm| <= ~2^-24 nrm.  The
+// assign kernel adds them to the scores through one extra MFMA k-step.
+__device__ void write_nsplit(double nrm, uint16_t* dst) {
+  const uint32_t hi = f32_to_bf16((float)nrm);
+  const double r1 = nrm - (double)bf16_to_f32(hi);
+  const uint32_t mid = f32_to_bf16((float)r1);
+  const double r2 = r1 - (double)bf16_to_f32(mid);
+  const uint32_t lo = f32_to_bf16((float)r2);
+  *(u32x4*)dst = u32x4{hi | (mid << 16), lo, 0u, 0u};
+}
+
 // Representative of one group row from its fp32 centroid value (lane = feature).
 template <class S>
-__device__ void finalize_rep(float c, int64_t row, typename S::T* R, double* nrm64, float* nrm32) {
+__device__ void finalize_rep(float c, int64_t row, typename S::T* R, double* nrm64, uint16_t* nsplit) {
   const int lane = threadIdx.x & 63;
   const float r = S::rep(c);
   S::store(R, row * 64 + lane, r);
   const double nrm = canon_nrm_wave(r);
   if (lane == 0) {
     nrm64[row] = nrm;
-    nrm32[row] = (float)nrm;
+    write_nsplit(nrm, nsplit + row * 8);
   }
 }
 
@@ -137,7 +162,8 @@ template <class S>
 __global__ __launch_bounds__(256) void k_init(const typename S::T* __restrict__ K,
                                               const float* __restrict__ init, int n, int N,
                                               float* __restrict__ C, typename S::T* __restrict__ R,
-                                              double* __restrict__ nrm64, float* __restrict__ nrm32) {
+                                              double* __restrict__ nrm64, uint16_t* __restrict__ nsplit,
+                                              int32_t* __restrict__ mcount) {
   const int lane = threadIdx.x & 63;
   const int g = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
   const int64_t bh = blockIdx.y;
@@ -146,36 +172,90 @@ __global__ __launch_bounds__(256) void k_init(const typename S::T* __restrict__ 
   const float c = init ? init[row * 64 + lane]
                        : S::load(K, (bh * n + ((int64_t)g * n) / N) * 64 + lane);
   C[row * 64 + lane] = c;
-  finalize_rep<S>(c, row, R, nrm64, nrm32);
+  if (mcount && g == 0 && lane == 0) mcount[bh] = 0;
+  finalize_rep<S>(c, row, R, nrm64, nsplit);
 }
 
 // ------------------------------------------------------------------ assign (bf16, MFMA)
+// The assign kernel's LDS copy of -2R stores 16-byte chunk c of row r at chunk
+// c ^ ((r >> 1) & 7) of a 128-byte row: 16 consecutive rows reading the same
+// logical chunk then hit 16 distinct groups of 4 banks (no padding needed).
+__device__ __forceinline__ int swz(int r, int c) { return r * 64 + 8 * (c ^ ((r >> 1) & 7)); }
+
+// Exact assignment of one bf16 key by a whole wave, the representatives read
+// from the LDS copy of -2R (r = -0.5 * (-2r) exactly).  Same definition as
+// exact_argmin_wave: fp64 fma chain over c = 0..63, lowest index among minima.
+// The key row sits in a per-wave LDS slot and is re-read for every group
+// (volatile), which keeps the 64 widened key values out of registers.
+__device__ int exact_argmin_lds(const uint16_t* kl, const uint16_t* Rs, const double* __restrict__ nrm, int N) {
+  const int lane = threadIdx.x & 63;
+  double best = INFINITY;
+  int bj = 0x7fffffff;
+  for (int j = lane; j < N; j += 64) {
+    double dot = 0.0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const u32x4 kwi = *(const volatile u32x4*)(kl + 8 * i);
+      const u32x4 rw = *(const u32x4*)(Rs + swz(j, i));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        dot = fma((double)bf16_to_f32(kwi[e] & 0xffffu), (double)(-0.5f * bf16_to_f32(rw[e] & 0xffffu)), dot);
+        dot = fma((double)bf16_to_f32(kwi[e] >> 16), (double)(-0.5f * bf16_to_f32(rw[e] >> 16)), dot);
+      }
+    }
+    const double sc = fma(-2.0, dot, nrm[j]);
+    if (sc < best) {
+      best = sc;
+      bj = j;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const double ob = __shfl_xor(best, off);
+    const int oj = __shfl_xor(bj, off);
+    if (ob < best || (ob == best && oj < bj)) {
+      best = ob;
+      bj = oj;
+    }
+  }
+  return bj;
+}
+
 // grid (ceil(tiles / (4 * tpw)), BH), 256 threads.  Each wave owns tpw
-// consecutive 32-key tiles.  LDS: -2R as [Npad][kRs] bf16, fl32(|r|^2) [Npad].
+// consecutive 32-key tiles and scores them two at a time (two independent
+// MFMA / VALU chains sharing the A-operand reads); the next pair's key
+// fragments are loaded while the current pair is scored.  LDS: -2R as
+// [Npad][64] bf16 (swizzled), the |r|^2 split as [Npad][8] bf16, the moved-key
+// records.
 //
-// MFMA 32x32x16: rows = 32 groups (A = -2R), columns = 32 keys (B = K), the
-// accumulator initialised with fl32(|r_j|^2), so each output is the score
-// s_ij = |r_j|^2 - 2 k_i.r_j.  Lane l (h = l/32, q = l%32) supplies at k-step s
-// features 32h + 8s .. +7 of its row for both operands (the same permutation
-// of the contraction axis on both sides), and receives groups
-// 8(v/4) + 4h + v%4 of key q in accumulator register v.
+// MFMA 32x32x16: rows = 32 groups (A = -2R), columns = 32 keys (B = K).  Lane
+// l (h = l/32, q = l%32) supplies at k-step s features 32h + 8s .. +7 of its
+// row for both operands (the same permutation of the contraction axis on both
+// sides) and receives groups 8(v/4) + 4h + v%4 of key q in accumulator
+// register v.  A fifth k-step adds |r_j|^2 = hi + mid + lo (A = the split, B =
+// ones), so each output is the score s_ij = |r_j|^2 - 2 k_i.r_j.
 //
 // Each score is packed with its group index in the low `codebits` mantissa
 // bits, so one float min/med3 chain keeps the best and second-best (value and
 // index) per key.  If second - best > 2E, where E bounds |packed - exact| (the
-// MFMA fp32 accumulation, the fp32 rounding of |r|^2 and the packing), the
-// best is provably the exact fp64 argmin; otherwise the key is re-decided by
-// exact_argmin_wave.
+// MFMA fp32 accumulation, the split of |r|^2 and the packing), the best is
+// provably the exact fp64 argmin; otherwise the key is re-decided by
+// exact_argmin_lds.  Later rounds (FIRST = false) also emit the keys whose
+// group changed as records (key, old, new), one global atomic per workgroup.
 template <bool FIRST>
 __global__ __launch_bounds__(256) void k_assign_bf16(
-    const uint16_t* __restrict__ K, const uint16_t* __restrict__ R, const float* __restrict__ nrm32,
-    const double* __restrict__ nrm64, float* __restrict__ knorm, int32_t* __restrict__ belong, int n,
-    int N, int tpw, float cbound, int codebits) {
+    const uint16_t* __restrict__ K, const uint16_t* __restrict__ R, const uint16_t* __restrict__ nsplit,
+    const double* __restrict__ nrm64, float* __restrict__ knorm, int32_t* __restrict__ belong,
+    int32_t* __restrict__ mcount, unsigned long long* __restrict__ mrec, int n, int N, int tpw, float cm,
+    float cp, int codebits) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ double red[4];
+  __shared__ int nmoved, moved_base;
+  __shared__ __align__(16) uint16_t kslot[4][64];  // key row of an uncertain key, per wave
   const int Npad = (N + 31) & ~31;
   uint16_t* Rs = (uint16_t*)smem;
-  float* n32s = (float*)(smem + (size_t)Npad * kRs * 2);
+  uint16_t* Ns = Rs + Npad * 64;
+  unsigned long long* wrec = (unsigned long long*)(Ns + Npad * 8);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
   const int64_t bh = blockIdx.y;
   const uint16_t* Rbh = R + bh * (int64_t)N * 64;
@@ -192,16 +272,19 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
         v[e] = lo | (hi << 16);
       }
     }
-    *(u32x4*)(Rs + row * kRs + ch * 8) = v;
+    *(u32x4*)(Rs + swz(row, ch)) = v;
   }
   double mx = 0.0;
   for (int j = tid; j < Npad; j += 256) {
-    n32s[j] = j < N ? nrm32[bh * N + j] : FLT_MAX;
+    // padded groups get the largest bf16 as |r|^2 so they never win
+    const u32x4 sp = j < N ? *(const u32x4*)(nsplit + (bh * N + j) * 8) : u32x4{0x7f7fu, 0u, 0u, 0u};
+    *(u32x4*)(Ns + j * 8) = sp;
     if (j < N) mx = fmax(mx, nrm64[bh * N + j]);
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
   if (lane == 0) red[wave] = mx;
+  if (tid == 0) nmoved = 0;
   __syncthreads();
   const double nmax = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
   const float nmaxf = (float)nmax * (1.0f + 0x1p-20f);
@@ -210,85 +293,161 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
   const int nblk = Npad >> 5;
   const uint32_t keep = ~((1u << codebits) - 1u);
   const uint32_t codemask = (1u << codebits) - 1u;
-  uint32_t jc[16];
-#pragma unroll
-  for (int v = 0; v < 16; ++v) jc[v] = 8 * (v >> 2) + 4 * h + (v & 3);
-
   const int64_t tile0 = ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(wave)) * tpw;
-  for (int tt = 0; tt < tpw; ++tt) {
-    const int64_t tile = tile0 + tt;
-    if (tile * 32 >= n) break;
-    const int64_t key = tile * 32 + q;
-    const bool valid = key < n;
+  const int64_t ntiles = ((int64_t)n + 31) / 32;
+  const int tcount = (int)max((int64_t)0, min((int64_t)tpw, ntiles - tile0));
+  // B operand of the |r|^2 k-step: ones in the first three slots of lanes h = 0
+  const u32x4 ones = h == 0 ? u32x4{0x3f803f80u, 0x3f80u, 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
+  const f32x16 zero = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+
+  u32x4 kf[2][4];
+  float kn[2] = {0.f, 0.f};
+  int old[2] = {0, 0};
+  auto fetch = [&](int t, u32x4 (&f)[4], float& knv, int& oldv) {
+    const int64_t key = (tile0 + t) * 32 + q;
+    const bool valid = t < tcount && key < n;
     const uint16_t* krow = K + (bh * n + (valid ? key : 0)) * 64 + h * 32;
-    u32x4 kf[4];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      kf[s] = u32x4{0u, 0u, 0u, 0u};
-      if (valid) kf[s] = *(const u32x4*)(krow + s * 8);
+    for (int s2 = 0; s2 < 4; ++s2) f[s2] = valid ? *(const u32x4*)(krow + s2 * 8) : u32x4{0u, 0u, 0u, 0u};
+    if (!FIRST) {
+      knv = valid ? knorm[bh * n + key] : 0.f;
+      oldv = (valid && h == 0) ? belong[bh * n + key] : 0;
     }
-    float kn;
-    if (FIRST) {
-      float ss = 0.f;
+  };
+  if (tcount > 0) {
+    fetch(0, kf[0], kn[0], old[0]);
+    fetch(1, kf[1], kn[1], old[1]);
+  }
+
+  for (int tt = 0; tt < tcount; tt += 2) {
+    u32x4 kf_n[2][4];
+    float kn_n[2] = {0.f, 0.f};
+    int old_n[2] = {0, 0};
+    if (tt + 2 < tcount) {
+      fetch(tt + 2, kf_n[0], kn_n[0], old_n[0]);
+      fetch(tt + 3, kf_n[1], kn_n[1], old_n[1]);
+    }
+    bool valid[2];
+    int64_t key[2];
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
+    for (int u = 0; u < 2; ++u) {
+      key[u] = (tile0 + tt + u) * 32 + q;
+      valid[u] = tt + u < tcount && key[u] < n;
+      if (FIRST) {
+        float ss = 0.f;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float lo = bf16_to_f32(kf[s][e] & 0xffffu), hi = bf16_to_f32(kf[s][e] >> 16);
-          ss = fmaf(lo, lo, ss);
-          ss = fmaf(hi, hi, ss);
-        }
-      ss += __shfl_xor(ss, 32);
-      kn = sqrtf(ss) * (1.0f + 0x1p-16f);
-      if (valid && h == 0) knorm[bh * n + key] = kn;
-    } else {
-      kn = valid ? knorm[bh * n + key] : 0.f;
+        for (int s2 = 0; s2 < 4; ++s2)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float lo = bf16_to_f32(kf[u][s2][e] & 0xffffu), hi = bf16_to_f32(kf[u][s2][e] >> 16);
+            ss = fmaf(lo, lo, ss);
+            ss = fmaf(hi, hi, ss);
+          }
+        ss += __shfl_xor(ss, 32);
+        kn[u] = sqrtf(ss) * (1.0f + 0x1p-16f);
+        if (valid[u] && h == 0) knorm[bh * n + key[u]] = kn[u];
+      }
     }
 
-    float M1 = FLT_MAX, M2 = FLT_MAX;
+    float M1[2] = {FLT_MAX, FLT_MAX}, M2[2] = {FLT_MAX, FLT_MAX};
     for (int blk = 0; blk < nblk; ++blk) {
-      f32x16 acc;
-      const float* nb = n32s + blk * 32 + 4 * h;
+      // lanes h = 1 read the same split row; their B operand is zero
+      const u32x4 an = *(const u32x4*)(Ns + (blk * 32 + q) * 8);
+      u32x4 af[4];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[v] = nb[8 * (v >> 2) + (v & 3)];
-      const uint16_t* ar = Rs + (blk * 32 + q) * kRs + h * 32;
+      for (int s2 = 0; s2 < 4; ++s2) af[s2] = *(const u32x4*)(Rs + swz(blk * 32 + q, 4 * h + s2));
+      f32x16 acc[2];
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const u32x4 a = *(const u32x4*)(ar + s * 8);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                      __builtin_bit_cast(bf16x8, kf[s]), acc, 0, 0, 0);
+      for (int u = 0; u < 2; ++u)
+        acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, an),
+                                                         __builtin_bit_cast(bf16x8, ones), zero, 0, 0, 0);
+#pragma unroll
+      for (int s2 = 0; s2 < 4; ++s2)
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+          acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[s2]),
+                                                           __builtin_bit_cast(bf16x8, kf[u][s2]), acc[u], 0, 0, 0);
+      // Within the block the group is 32 blk + 8 (v/4) + 4 h + v%4: the
+      // register part 8 (v/4) + v%4 is packed per score (an inline constant),
+      // the lane-half and block bits once per block into the block's top-2
+      // (OR-ing the same bits into cleared bits preserves the order).  Top-2
+      // over pairs: with m1 <= m2 the two smallest so far, the second smallest
+      // of {m1, m2, x, y} is min(m2, med3(m1, x, y)).
+      const uint32_t bb = ((uint32_t)blk << 5) | ((uint32_t)h << 2);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        float m1 = FLT_MAX, m2 = FLT_MAX;
+#pragma unroll
+        for (int v = 0; v < 16; v += 2) {
+          const float x = __uint_as_float((__float_as_uint(acc[u][v]) & keep) | (uint32_t)(8 * (v >> 2) + (v & 3)));
+          const float y = __uint_as_float((__float_as_uint(acc[u][v + 1]) & keep) |
+                                          (uint32_t)(8 * ((v + 1) >> 2) + ((v + 1) & 3)));
+          m2 = min2(m2, __builtin_amdgcn_fmed3f(m1, x, y));
+          m1 = min3f(m1, x, y);
+        }
+        m1 = __uint_as_float(__float_as_uint(m1) | bb);
+        m2 = __uint_as_float(__float_as_uint(m2) | bb);
+        const float nm2 = min2(max2(M1[u], m1), min2(M2[u], m2));
+        M1[u] = min2(M1[u], m1);
+        M2[u] = nm2;
       }
-      float m1 = FLT_MAX, m2 = FLT_MAX;
+    }
+
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float x = __uint_as_float((__float_as_uint(acc[v]) & keep) | jc[v]);
-        m2 = __builtin_amdgcn_fmed3f(m1, m2, x);
-        m1 = fminf(m1, x);
+    for (int u = 0; u < 2; ++u) {
+      {
+        const float p1 = __shfl_xor(M1[u], 32), p2 = __shfl_xor(M2[u], 32);
+        const float nm2 = min2(max2(M1[u], p1), min2(M2[u], p2));
+        M1[u] = min2(M1[u], p1);
+        M2[u] = nm2;
       }
-      const uint32_t bb = (uint32_t)blk << 5;
-      m1 = __uint_as_float(__float_as_uint(m1) | bb);
-      m2 = __uint_as_float(__float_as_uint(m2) | bb);
-      const float nm2 = fminf(fmaxf(M1, m1), fminf(M2, m2));
-      M1 = fminf(M1, m1);
-      M2 = nm2;
+      // E bounds |packed - exact| for the best and for any group that could
+      // beat it: the MFMA part cm * M (M = max |r|^2 + 2 |k| max |r| bounds the
+      // sum of |terms|) and the packing part cp * (|M1| + 3 cm M); the last
+      // two terms cover the fp32 evaluation of E and of M1 + 2E.
+      int jstar = (int)(__float_as_uint(M1[u]) & codemask);
+      const float Mk = nmaxf + 2.0f * kn[u] * rmaxf;
+      const float aM1 = fabsf(M1[u]);
+      const float E = (cm * Mk + cp * (aM1 + 3.0f * cm * Mk)) * (1.0f + 0x1p-20f) + 0x1p-22f * aM1 + 1e-30f;
+      const bool certain = (M2[u] > M1[u] + 2.0f * E) && (jstar < N);
+      uint64_t unc = __ballot(valid[u] && !certain && h == 0);
+      while (unc) {
+        const int b = __ffsll((unsigned long long)unc) - 1;
+        unc &= unc - 1;
+        if (q == b) {
+#pragma unroll
+          for (int s2 = 0; s2 < 4; ++s2) *(u32x4*)(&kslot[wave][h * 32 + s2 * 8]) = kf[u][s2];
+        }
+        const int jb = exact_argmin_lds(kslot[wave], Rs, nrm64 + bh * N, N);
+        if (q == b) jstar = jb;
+      }
+      if (valid[u] && h == 0) belong[bh * n + key[u]] = jstar;
+      if (!FIRST) {
+        const bool moved = valid[u] && h == 0 && old[u] != jstar;
+        const uint64_t mv = __ballot(moved);
+        if (mv) {
+          int base = 0;
+          if (lane == 0) base = atomicAdd(&nmoved, __popcll(mv));
+          base = __builtin_amdgcn_readfirstlane(base);
+          if (moved)
+            wrec[base + __popcll(mv & ((1ull << lane) - 1ull))] =
+                ((unsigned long long)key[u] << 32) | ((unsigned)old[u] << 16) | (unsigned)jstar;
+        }
+      }
     }
-    {
-      const float p1 = __shfl_xor(M1, 32), p2 = __shfl_xor(M2, 32);
-      const float nm2 = fminf(fmaxf(M1, p1), fminf(M2, p2));
-      M1 = fminf(M1, p1);
-      M2 = nm2;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+#pragma unroll
+      for (int s2 = 0; s2 < 4; ++s2) kf[u][s2] = kf_n[u][s2];
+      kn[u] = kn_n[u];
+      old[u] = old_n[u];
     }
-    int jstar = (int)(__float_as_uint(M1) & codemask);
-    const float E = cbound * (nmaxf + 2.0f * kn * rmaxf) + 1e-30f;
-    const bool certain = (M2 > M1 + 2.0f * E) && (jstar < N);
-    uint64_t unc = __ballot(valid && !certain && h == 0);
-    while (unc) {
-      const int b = __ffsll((unsigned long long)unc) - 1;
-      unc &= unc - 1;
-      const int jb = exact_argmin_wave<BF16>(K + (bh * n + tile * 32 + b) * 64, Rbh, nrm64 + bh * N, N);
-      if (q == b) jstar = jb;
-    }
-    if (valid && h == 0) belong[bh * n + key] = jstar;
+  }
+  if (!FIRST) {
+    __syncthreads();
+    if (tid == 0) moved_base = nmoved ? atomicAdd(mcount + bh, nmoved) : 0;
+    __syncthreads();
+    for (int x = tid; x < nmoved; x += 256) mrec[bh * n + moved_base + x] = wrec[x];
   }
 }
 
@@ -403,7 +562,7 @@ __global__ __launch_bounds__(256) void k_segsum(const typename S::T* __restrict_
                                                 const int32_t* __restrict__ goff,
                                                 const int32_t* __restrict__ count, int n, int N,
                                                 float* __restrict__ out, typename S::T* __restrict__ R,
-                                                double* __restrict__ nrm64, float* __restrict__ nrm32) {
+                                                double* __restrict__ nrm64, uint16_t* __restrict__ nsplit) {
   const int lane = threadIdx.x & 63;
   const int g = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
   const int64_t bh = blockIdx.y;
@@ -432,9 +591,212 @@ __global__ __launch_bounds__(256) void k_segsum(const typename S::T* __restrict_
     } else {
       c = out[row * 64 + lane];
     }
-    finalize_rep<S>(c, row, R, nrm64, nrm32);
+    finalize_rep<S>(c, row, R, nrm64, nsplit);
   } else {
     out[row * 64 + lane] = (float)acc;
+  }
+}
+
+// ------------------------------------------------------------------ order-free bucketing (bf16)
+// With bf16 keys and values every fp64 member sum is exact (8-bit mantissas,
+// at most 2^30 members, magnitudes within 2^30 of each other), so the order of
+// summation cannot change a bit and the bf16 path groups keys without a stable
+// order: slots inside a group come from LDS atomic cursors.
+
+// Exclusive scan of x over threads 0..N-1 of a 1024-thread block (N <= 1024).
+__device__ int block_excl_scan(int x, int* wsum) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int incl = wave_incl_scan(x);
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  if (wave == 0) {
+    const int t = lane < 16 ? wsum[lane] : 0;
+    const int ti = wave_incl_scan(t);
+    if (lane < 16) wsum[lane] = ti - t;
+  }
+  __syncthreads();
+  const int r = incl - x + wsum[wave];
+  __syncthreads();
+  return r;
+}
+
+// Every key of a slice by group: grid BH, 1024 threads, LDS counts + cursors.
+// grp[g] = {first slot, members, 0, 0}; count[g] = members (if count != NULL).
+__global__ __launch_bounds__(1024) void k_full_bucket(const int32_t* __restrict__ belong, int n, int N,
+                                                      int32_t* __restrict__ list, int4* __restrict__ grp,
+                                                      int32_t* __restrict__ count) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int wsum[16];
+  int32_t* cnt = (int32_t*)smem;
+  int32_t* cur = cnt + N;
+  const int tid = threadIdx.x;
+  const int64_t bh = blockIdx.x;
+  const int32_t* a = belong + bh * n;
+  for (int g = tid; g < N; g += 1024) cnt[g] = 0;
+  __syncthreads();
+  for (int i = tid; i < n; i += 1024) {
+    const int g = a[i];
+    if ((unsigned)g < (unsigned)N) atomicAdd(&cnt[g], 1);
+  }
+  __syncthreads();
+  const int v = tid < N ? cnt[tid] : 0;
+  const int ex = block_excl_scan(v, wsum);
+  if (tid < N) {
+    cur[tid] = ex;
+    grp[bh * N + tid] = int4{ex, v, 0, 0};
+    if (count) count[bh * N + tid] = v;
+  }
+  __syncthreads();
+  for (int i = tid; i < n; i += 1024) {
+    const int g = a[i];
+    if ((unsigned)g < (unsigned)N) list[bh * n + atomicAdd(&cur[g], 1)] = i;
+  }
+}
+
+// Moved-key records of one round by group: joins (new group) and leaves (old
+// group).  grid BH, 1024 threads.  count[g] += joins - leaves; grp[g] =
+// {first join, joins, first leave, leaves}; the record counter is reset.
+__global__ __launch_bounds__(1024) void k_moved_bucket(const unsigned long long* __restrict__ mrec,
+                                                       int32_t* __restrict__ mcount, int n, int N,
+                                                       int32_t* __restrict__ jlist, int32_t* __restrict__ llist,
+                                                       int4* __restrict__ grp, int32_t* __restrict__ count) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int wsum[16];
+  int32_t* jc = (int32_t*)smem;
+  int32_t* lc = jc + N;
+  int32_t* jcur = lc + N;
+  int32_t* lcur = jcur + N;
+  const int tid = threadIdx.x;
+  const int64_t bh = blockIdx.x;
+  const int m = mcount[bh];
+  const unsigned long long* rec = mrec + bh * n;
+  for (int g = tid; g < N; g += 1024) {
+    jc[g] = 0;
+    lc[g] = 0;
+  }
+  __syncthreads();
+  for (int r = tid; r < m; r += 1024) {
+    const unsigned long long x = rec[r];
+    atomicAdd(&jc[(int)(x & 0xffffu)], 1);
+    atomicAdd(&lc[(int)((x >> 16) & 0xffffu)], 1);
+  }
+  __syncthreads();
+  const int vj = tid < N ? jc[tid] : 0;
+  const int vl = tid < N ? lc[tid] : 0;
+  const int ej = block_excl_scan(vj, wsum);
+  const int el = block_excl_scan(vl, wsum);
+  if (tid < N) {
+    jcur[tid] = ej;
+    lcur[tid] = el;
+    grp[bh * N + tid] = int4{ej, vj, el, vl};
+    if (vj != vl) count[bh * N + tid] += vj - vl;
+  }
+  __syncthreads();
+  for (int r = tid; r < m; r += 1024) {
+    const unsigned long long x = rec[r];
+    const int key = (int)(x >> 32);
+    jlist[bh * n + atomicAdd(&jcur[(int)(x & 0xffffu)], 1)] = key;
+    llist[bh * n + atomicAdd(&lcur[(int)((x >> 16) & 0xffffu)], 1)] = key;
+  }
+  __syncthreads();
+  if (tid == 0) mcount[bh] = 0;
+}
+
+// Sum of listed bf16 rows into a per-lane accumulator of 4 features: lane l
+// reads features 4 (l%16) .. +3 of row list[x + l/16], 4 rows per instruction
+// and 16 rows per iteration in flight.
+__device__ __forceinline__ void add_rows(const uint16_t* __restrict__ Xb, const int32_t* __restrict__ L, int cnt,
+                                         int sub, double sign, double acc[4]) {
+  for (int x = 0; x < cnt; x += 16) {
+    u32x2 w[4];
+    bool ok[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = x + 4 * u + sub;
+      ok[u] = idx < cnt;
+      const int key = L[ok[u] ? idx : 0];
+      w[u] = *(const u32x2*)(Xb + (int64_t)key * 64);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (!ok[u]) continue;
+      acc[0] = fma(sign, (double)bf16_to_f32(w[u][0] & 0xffffu), acc[0]);
+      acc[1] = fma(sign, (double)bf16_to_f32(w[u][0] >> 16), acc[1]);
+      acc[2] = fma(sign, (double)bf16_to_f32(w[u][1] & 0xffffu), acc[2]);
+      acc[3] = fma(sign, (double)bf16_to_f32(w[u][1] >> 16), acc[3]);
+    }
+  }
+}
+
+// grid (ceil(N/4), BH), 256 threads: one wave per group.
+//   MODE 0: first round: S = sum of the joins (all members)
+//   MODE 1: later rounds: S += joins - leaves (groups without either are skipped)
+//   MODE 2: value sums: vsum = (float) sum of the joins
+// MODE 0/1 then set C = (float)(S / count) (an empty group keeps C), R = bf16(C)
+// and the canonical fp64 |r|^2.
+template <int MODE>
+__global__ __launch_bounds__(256) void k_segsum_bf16(const uint16_t* __restrict__ X, const int32_t* __restrict__ jlist,
+                                                     const int32_t* __restrict__ llist, const int4* __restrict__ grp,
+                                                     const int32_t* __restrict__ count, int n, int N,
+                                                     double* __restrict__ S64, float* __restrict__ out,
+                                                     uint16_t* __restrict__ R, double* __restrict__ nrm64,
+                                                     uint16_t* __restrict__ nsplit) {
+  const int lane = threadIdx.x & 63, sub = lane >> 4, c4 = lane & 15;
+  const int g = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+  const int64_t bh = blockIdx.y;
+  if (g >= N) return;
+  const int64_t row = bh * N + g;
+  const int4 gd = grp[row];
+  if (MODE == 1 && gd.y == 0 && gd.w == 0) return;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  if (MODE == 1 && sub == 0) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = S64[row * 64 + 4 * c4 + e];
+  }
+  const uint16_t* Xb = X + bh * (int64_t)n * 64 + 4 * c4;
+  add_rows(Xb, jlist + bh * n + gd.x, gd.y, sub, 1.0, acc);
+  if (MODE == 1) add_rows(Xb, llist + bh * n + gd.z, gd.w, sub, -1.0, acc);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    acc[e] += __shfl_xor(acc[e], 16);
+    acc[e] += __shfl_xor(acc[e], 32);
+  }
+  if (MODE == 2) {
+    if (sub == 0) {
+      float4 o = {(float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]};
+      *(float4*)(out + row * 64 + 4 * c4) = o;
+    }
+    return;
+  }
+  const int cnt = MODE == 0 ? gd.y : count[row];
+  float c[4];
+  if (cnt > 0) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) c[e] = (float)(acc[e] / (double)cnt);
+  } else {
+    const float4 o = *(const float4*)(out + row * 64 + 4 * c4);
+    c[0] = o.x, c[1] = o.y, c[2] = o.z, c[3] = o.w;
+  }
+  float r[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) r[e] = BF16::rep(c[e]);
+  if (sub == 0) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) S64[row * 64 + 4 * c4 + e] = acc[e];
+    if (cnt > 0) *(float4*)(out + row * 64 + 4 * c4) = float4{c[0], c[1], c[2], c[3]};
+    const u32x2 rb = {(__float_as_uint(r[0]) >> 16) | (__float_as_uint(r[1]) & 0xffff0000u),
+                      (__float_as_uint(r[2]) >> 16) | (__float_as_uint(r[3]) & 0xffff0000u)};
+    *(u32x2*)(R + row * 64 + 4 * c4) = rb;
+  }
+  double nrm = 0.0;
+#pragma unroll
+  for (int cc = 0; cc < 64; ++cc) {
+    const double rc = (double)readlane_f(r[cc & 3], cc >> 2);
+    nrm = fma(rc, rc, nrm);
+  }
+  if (lane == 0) {
+    nrm64[row] = nrm;
+    write_nsplit(nrm, nsplit + row * 8);
   }
 }
 
@@ -549,12 +911,12 @@ __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict_
       }
       float bm = acc[0];
 #pragma unroll
-      for (int v = 1; v < 16; ++v) bm = fmaxf(bm, acc[v]);
-      bm = fmaxf(bm, __shfl_xor(bm, 32));
+      for (int v = 1; v < 16; ++v) bm = __builtin_amdgcn_fmed3f(bm, acc[v], INFINITY);
+      bm = __builtin_amdgcn_fmed3f(bm, __shfl_xor(bm, 32), INFINITY);
       if (bm == -INFINITY) continue;  // every group of this block is empty (uniform)
       const float bmt = bm * sl2e;
       if (bmt > mt + 8.0f) {
-        const float alpha = exp2f(mt - bmt);
+        const float alpha = __builtin_amdgcn_exp2f(mt - bmt);
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           o0[v] *= alpha;
@@ -566,7 +928,7 @@ __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict_
       float e[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        e[v] = exp2f(fmaf(acc[v], sl2e, -mt));
+        e[v] = __builtin_amdgcn_exp2f(fmaf(acc[v], sl2e, -mt));
         ssum += e[v];
       }
       u32x4 b0, b1;
@@ -674,9 +1036,11 @@ __global__ __launch_bounds__(256) void k_attend_f32(const float* __restrict__ Q,
   }
 }
 
-size_t assign_lds(int N) {
+constexpr size_t kAssignLdsMax = 160 * 1024 - 1024;  // dynamic LDS budget (static arrays use the rest)
+
+size_t assign_lds(int N, int tpw = 12) {
   const int Npad = (N + 31) & ~31;
-  return (size_t)Npad * kRs * 2 + (size_t)Npad * 4;
+  return (size_t)Npad * 128 + (size_t)Npad * 16 + (size_t)4 * tpw * 32 * 8;
 }
 size_t bucket_lds(int N) { return (size_t)16 * N * 8 + (size_t)2 * N * 4; }
 size_t attend_lds(int N) {
@@ -691,9 +1055,9 @@ void set_lds_limits() {
   static std::once_flag once;
   std::call_once(once, [] {
     (void)hipFuncSetAttribute((const void*)k_assign_bf16<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)assign_lds(kMaxGroups));
+                              (int)kAssignLdsMax);
     (void)hipFuncSetAttribute((const void*)k_assign_bf16<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)assign_lds(kMaxGroups));
+                              (int)kAssignLdsMax);
     (void)hipFuncSetAttribute((const void*)k_bucket, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)bucket_lds(kMaxGroups));
     (void)hipFuncSetAttribute((const void*)k_attend_bf16, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -728,7 +1092,7 @@ size_t workspace_layout(const Dims& d, Workspace* ws, void* base) {
   w.C = (float*)take(BH * N * 64 * 4);
   w.R = take(BH * N * 64 * es);
   w.nrm64 = (double*)take(BH * N * 8);
-  w.nrm32 = (float*)take(BH * N * 4);
+  w.nsplit = (uint16_t*)take(BH * N * 16);
   w.knorm = (float*)take(BH * n * 4);
   w.belong = (int32_t*)take(BH * n * 4);
   w.perm = (int32_t*)take(BH * n * 4);
@@ -738,47 +1102,56 @@ size_t workspace_layout(const Dims& d, Workspace* ws, void* base) {
   w.Rq = (uint16_t*)take(BH * N * 64 * 2);
   w.Vt = (uint16_t*)take(BH * 64 * (int64_t)vt_stride((int)N) * 2);
   w.ginit = (float*)take(BH * Npad * 4);
+  w.S64 = (double*)take(BH * N * 64 * 8);
+  w.mcount = (int32_t*)take(BH * 4);
+  w.mrec = (unsigned long long*)take(BH * n * 8);
+  w.grp = (int4*)take(BH * N * 16);
+  w.llist = (int32_t*)take(BH * n * 4);
   if (ws) *ws = w;
   return off;
 }
 
 hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C, void* R,
-                       double* nrm64, float* nrm32, hipStream_t st) {
+                       double* nrm64, uint16_t* nsplit, int32_t* mcount, hipStream_t st) {
   TimedLaunch timed("init", st);
   const dim3 grid(cdiv(d.N, 4), (unsigned)d.BH), block(256);
   if (d.dtype == 1)
     hipLaunchKernelGGL(k_init<BF16>, grid, block, 0, st, (const uint16_t*)K, init, d.n, d.N, C,
-                       (uint16_t*)R, nrm64, nrm32);
+                       (uint16_t*)R, nrm64, nsplit, mcount);
   else
     hipLaunchKernelGGL(k_init<F32>, grid, block, 0, st, (const float*)K, init, d.n, d.N, C, (float*)R,
-                       nrm64, nrm32);
+                       nrm64, nsplit, mcount);
   return hipGetLastError();
 }
 
-hipError_t launch_assign(const Dims& d, const void* K, const void* R, const float* nrm32,
-                         const double* nrm64, float* knorm, int32_t* belong, bool first,
-                         hipStream_t st) {
+hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint16_t* nsplit,
+                         const double* nrm64, float* knorm, int32_t* belong, int32_t* mcount,
+                         unsigned long long* mrec, bool first, hipStream_t st) {
   TimedLaunch timed("assign", st);
   set_lds_limits();
   if (d.dtype == 1) {
     const int64_t tiles = (d.n + 31) / 32;
-    int64_t tpw = (d.BH * tiles) / (4 * 2048);
-    tpw = tpw < 1 ? 1 : (tpw > 8 ? 8 : tpw);
+    // about 1024 workgroups (4 per CU), as many tiles each as the LDS allows
+    int64_t tpw = (d.BH * tiles + 4 * 1024 - 1) / (4 * 1024);
+    while (tpw > 1 && assign_lds(d.N, (int)tpw) > kAssignLdsMax) --tpw;
+    tpw = tpw < 1 ? 1 : (tpw > 16 ? 16 : tpw);
     const int Npad = (d.N + 31) & ~31;
     int codebits = 5;
     while ((1 << codebits) < Npad) ++codebits;
     // |MFMA fp32 accumulation error| <= (d + 4) 2^-24 * 2 * sum|terms| (each of the
-    // d products and the init rounded at most once, sequential model, 2x margin);
+    // d products and the three |r|^2 terms added with at most one rounding,
+    // sequential model, 2x margin; the split itself is within 2^-24 |r|^2);
     // packing the index moves a value by < 2^(codebits - 23) of its magnitude.
-    const float cbound = ((float)(kD + 4) * 0x1p-23f + ldexpf(1.0f, codebits - 23)) * (1.0f + 0x1p-10f);
+    const float cm = (float)(kD + 4) * 0x1p-23f * (1.0f + 0x1p-10f);
+    const float cp = ldexpf(1.0f, codebits - 23) * (1.0f + 0x1p-10f);
     const dim3 grid(cdiv(tiles, 4 * tpw), (unsigned)d.BH), block(256);
-    const size_t lds = assign_lds(d.N);
+    const size_t lds = assign_lds(d.N, (int)tpw);
     if (first)
       hipLaunchKernelGGL(k_assign_bf16<true>, grid, block, lds, st, (const uint16_t*)K, (const uint16_t*)R,
-                         nrm32, nrm64, knorm, belong, d.n, d.N, (int)tpw, cbound, codebits);
+                         nsplit, nrm64, knorm, belong, mcount, mrec, d.n, d.N, (int)tpw, cm, cp, codebits);
     else
       hipLaunchKernelGGL(k_assign_bf16<false>, grid, block, lds, st, (const uint16_t*)K, (const uint16_t*)R,
-                         nrm32, nrm64, knorm, belong, d.n, d.N, (int)tpw, cbound, codebits);
+                         nsplit, nrm64, knorm, belong, mcount, mrec, d.n, d.N, (int)tpw, cm, cp, codebits);
   } else {
     const int kpw = 4;
     const dim3 grid(cdiv(d.n, 4 * kpw), (unsigned)d.BH), block(256);
@@ -797,17 +1170,51 @@ hipError_t launch_bucket(const Dims& d, const int32_t* belong, int32_t* perm, in
   return hipGetLastError();
 }
 
+hipError_t launch_full_bucket(const Dims& d, const int32_t* belong, int32_t* list, int4* grp, int32_t* count,
+                             hipStream_t st) {
+  TimedLaunch timed("bucket", st);
+  hipLaunchKernelGGL(k_full_bucket, dim3((unsigned)d.BH), dim3(1024), (size_t)2 * d.N * 4, st, belong, d.n, d.N,
+                     list, grp, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_moved_bucket(const Dims& d, const unsigned long long* mrec, int32_t* mcount, int32_t* jlist,
+                               int32_t* llist, int4* grp, int32_t* count, hipStream_t st) {
+  TimedLaunch timed("moved_bucket", st);
+  hipLaunchKernelGGL(k_moved_bucket, dim3((unsigned)d.BH), dim3(1024), (size_t)4 * d.N * 4, st, mrec, mcount, d.n,
+                     d.N, jlist, llist, grp, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_segsum_bf16(const Dims& d, int mode, const void* X, const int32_t* jlist, const int32_t* llist,
+                              const int4* grp, const int32_t* count, double* S64, float* out, void* R,
+                              double* nrm64, uint16_t* nsplit, hipStream_t st) {
+  TimedLaunch timed(mode == 2 ? "valuesum" : "update", st);
+  const dim3 grid(cdiv(d.N, 4), (unsigned)d.BH), block(256);
+  const uint16_t* Xb = (const uint16_t*)X;
+  if (mode == 0)
+    hipLaunchKernelGGL(k_segsum_bf16<0>, grid, block, 0, st, Xb, jlist, llist, grp, count, d.n, d.N, S64, out,
+                       (uint16_t*)R, nrm64, nsplit);
+  else if (mode == 1)
+    hipLaunchKernelGGL(k_segsum_bf16<1>, grid, block, 0, st, Xb, jlist, llist, grp, count, d.n, d.N, S64, out,
+                       (uint16_t*)R, nrm64, nsplit);
+  else
+    hipLaunchKernelGGL(k_segsum_bf16<2>, grid, block, 0, st, Xb, jlist, llist, grp, count, d.n, d.N, S64, out,
+                       (uint16_t*)R, nrm64, nsplit);
+  return hipGetLastError();
+}
+
 hipError_t launch_update(const Dims& d, const void* K, const int32_t* perm, const int32_t* goff,
-                         const int32_t* count, float* C, void* R, double* nrm64, float* nrm32,
+                         const int32_t* count, float* C, void* R, double* nrm64, uint16_t* nsplit,
                          hipStream_t st) {
   TimedLaunch timed("update", st);
   const dim3 grid(cdiv(d.N, 4), (unsigned)d.BH), block(256);
   if (d.dtype == 1)
     hipLaunchKernelGGL((k_segsum<BF16, true>), grid, block, 0, st, (const uint16_t*)K, perm, goff, count,
-                       d.n, d.N, C, (uint16_t*)R, nrm64, nrm32);
+                       d.n, d.N, C, (uint16_t*)R, nrm64, nsplit);
   else
     hipLaunchKernelGGL((k_segsum<F32, true>), grid, block, 0, st, (const float*)K, perm, goff, count, d.n,
-                       d.N, C, (float*)R, nrm64, nrm32);
+                       d.N, C, (float*)R, nrm64, nsplit);
   return hipGetLastError();
 }
 
@@ -817,10 +1224,10 @@ hipError_t launch_valuesum(const Dims& d, const void* V, const int32_t* perm, co
   const dim3 grid(cdiv(d.N, 4), (unsigned)d.BH), block(256);
   if (d.dtype == 1)
     hipLaunchKernelGGL((k_segsum<BF16, false>), grid, block, 0, st, (const uint16_t*)V, perm, goff, count,
-                       d.n, d.N, vsum, (uint16_t*)nullptr, (double*)nullptr, (float*)nullptr);
+                       d.n, d.N, vsum, (uint16_t*)nullptr, (double*)nullptr, (uint16_t*)nullptr);
   else
     hipLaunchKernelGGL((k_segsum<F32, false>), grid, block, 0, st, (const float*)V, perm, goff, count, d.n,
-                       d.N, vsum, (float*)nullptr, (double*)nullptr, (float*)nullptr);
+                       d.N, vsum, (float*)nullptr, (double*)nullptr, (uint16_t*)nullptr);
   return hipGetLastError();
 }
 
