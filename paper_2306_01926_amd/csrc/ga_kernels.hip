@@ -177,6 +177,22 @@ __global__ __launch_bounds__(256) void k_init(const typename S::T* __restrict__ 
 }
 
 // ------------------------------------------------------------------ assign (bf16, MFMA)
+// Upper bound of |k| for the key whose 64 bf16 features are split over lanes
+// q and q + 32 (32 each, as MFMA fragments).
+__device__ __forceinline__ float key_norm_bound(const u32x4 (&f)[4]) {
+  float ss = 0.f;
+#pragma unroll
+  for (int s2 = 0; s2 < 4; ++s2)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = bf16_to_f32(f[s2][e] & 0xffffu), hi = bf16_to_f32(f[s2][e] >> 16);
+      ss = fmaf(lo, lo, ss);
+      ss = fmaf(hi, hi, ss);
+    }
+  ss += __shfl_xor(ss, 32);
+  return sqrtf(ss) * (1.0f + 0x1p-16f);
+}
+
 // The assign kernel's LDS copy of -2R stores 16-byte chunk c of row r at chunk
 // c ^ ((r >> 1) & 7) of a 128-byte row: 16 consecutive rows reading the same
 // logical chunk then hit 16 distinct groups of 4 banks (no padding needed).
@@ -221,45 +237,132 @@ __device__ int exact_argmin_lds(const uint16_t* kl, const uint16_t* Rs, const do
   return bj;
 }
 
-// grid (ceil(tiles / (4 * tpw)), BH), 256 threads.  Each wave owns tpw
-// consecutive 32-key tiles and scores them two at a time (two independent
-// MFMA / VALU chains sharing the A-operand reads); the next pair's key
-// fragments are loaded while the current pair is scored.  LDS: -2R as
-// [Npad][64] bf16 (swizzled), the |r|^2 split as [Npad][8] bf16, the moved-key
-// records.
-//
-// MFMA 32x32x16: rows = 32 groups (A = -2R), columns = 32 keys (B = K).  Lane
-// l (h = l/32, q = l%32) supplies at k-step s features 32h + 8s .. +7 of its
-// row for both operands (the same permutation of the contraction axis on both
-// sides) and receives groups 8(v/4) + 4h + v%4 of key q in accumulator
-// register v.  A fifth k-step adds |r_j|^2 = hi + mid + lo (A = the split, B =
-// ones), so each output is the score s_ij = |r_j|^2 - 2 k_i.r_j.
-//
-// Each score is packed with its group index in the low `codebits` mantissa
-// bits, so one float min/med3 chain keeps the best and second-best (value and
-// index) per key.  If second - best > 2E, where E bounds |packed - exact| (the
-// MFMA fp32 accumulation, the split of |r|^2 and the packing), the best is
-// provably the exact fp64 argmin; otherwise the key is re-decided by
-// exact_argmin_lds.  Later rounds (FIRST = false) also emit the keys whose
-// group changed as records (key, old, new), one global atomic per workgroup.
-template <bool FIRST>
-__global__ __launch_bounds__(256) void k_assign_bf16(
-    const uint16_t* __restrict__ K, const uint16_t* __restrict__ R, const uint16_t* __restrict__ nsplit,
-    const double* __restrict__ nrm64, float* __restrict__ knorm, int32_t* __restrict__ belong,
-    int32_t* __restrict__ mcount, unsigned long long* __restrict__ mrec, int n, int N, int tpw, float cm,
-    float cp, int codebits) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ double red[4];
-  __shared__ int nmoved, moved_base;
-  __shared__ __align__(16) uint16_t kslot[4][64];  // key row of an uncertain key, per wave
-  const int Npad = (N + 31) & ~31;
-  uint16_t* Rs = (uint16_t*)smem;
-  uint16_t* Ns = Rs + Npad * 64;
-  unsigned long long* wrec = (unsigned long long*)(Ns + Npad * 8);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
-  const int64_t bh = blockIdx.y;
-  const uint16_t* Rbh = R + bh * (int64_t)N * 64;
+// Scores are ranked as packed floats: the low 4 mantissa bits of a score are
+// replaced by its accumulator register index v (0..15), so one min/med3 chain
+// keeps value and register of the best two.  The block of the best is tracked
+// beside it and the lane half is resolved when the halves merge, so the
+// group of a packed best (v, block b, half h) is 32 b + 8 (v/4) + 4 h + v%4.
+constexpr uint32_t kPackMask = 15u;
 
+// Top-2 of one block's 16 scores merged into the running (M1, M2, B1 = block
+// of M1).  Over pairs: with m1 <= m2 the two smallest so far, the second
+// smallest of {m1, m2, x, y} is min(m2, med3(m1, x, y)).  Equal packed values
+// in two blocks keep the earlier block; such a key is never certified (its
+// gap is 0), so the choice does not matter.
+__device__ __forceinline__ void reduce_block(const f32x16& acc, int blk, float& M1, float& M2, int& B1) {
+  float m1 = FLT_MAX, m2 = FLT_MAX;
+#pragma unroll
+  for (int v = 0; v < 16; v += 2) {
+    const float x = __uint_as_float((__float_as_uint(acc[v]) & ~kPackMask) | (uint32_t)v);
+    const float y = __uint_as_float((__float_as_uint(acc[v + 1]) & ~kPackMask) | (uint32_t)(v + 1));
+    m2 = min2(m2, __builtin_amdgcn_fmed3f(m1, x, y));
+    m1 = min3f(m1, x, y);
+  }
+  B1 = m1 < M1 ? blk : B1;
+  const float nm2 = min2(max2(M1, m1), min2(M2, m2));
+  M1 = min2(M1, m1);
+  M2 = nm2;
+}
+
+// Bounds shared by every tile of a slice: the largest |r|^2 and |r| (with
+// margins for their fp32 evaluation) and the error constants of the launch.
+struct Certify {
+  float nmaxf, rmaxf, cm, cp;
+};
+
+// Per-workgroup lists of the assign kernels (in LDS): moved-key records and
+// the queue of keys whose packed top-2 was not certified, with their counts.
+struct AssignCounts {
+  int nmoved, nunc, moved_base;
+};
+struct AssignLists {
+  AssignCounts* c;
+  unsigned long long* wrec;  // (key << 32) | (old << 16) | new
+  unsigned long long* uq;    // (key << 32) | old
+};
+
+// Append the keys of `mask` (one bit per lane) to an LDS list with one
+// atomic per wave; `rec` is this lane's record.
+__device__ __forceinline__ void wave_append(uint64_t mask, bool mine, unsigned long long rec, int* count,
+                                            unsigned long long* list) {
+  if (!mask) return;
+  const int lane = threadIdx.x & 63;
+  int base = 0;
+  if (lane == 0) base = atomicAdd(count, __popcll(mask));
+  base = __builtin_amdgcn_readfirstlane(base);
+  if (mine) list[base + __popcll(mask & ((1ull << lane) - 1ull))] = rec;
+}
+
+// Decision for the 32 keys of one tile, given each lane's top-2 over its half
+// of the groups: merge the halves, certify the packed best against the error
+// bound E, store the group and (later rounds) record keys whose group changed.
+// Keys that fail the test are queued for exact_decide_queue.
+//
+// E bounds |packed - exact| for the best and for any group that could beat
+// it: the MFMA part cm * M (M = max |r|^2 + 2 |k| max |r| bounds the sum of
+// |terms|) and the packing part cp * (|M1| + 3 cm M); the last two terms cover
+// the fp32 evaluation of E and of M1 + 2E.
+template <bool FIRST>
+__device__ __forceinline__ void decide_tile(float M1, float M2, int B1, float knv, int oldv, int64_t key, bool valid,
+                                            int N, const Certify& cf, int32_t* __restrict__ belong_bh,
+                                            const AssignLists& sh) {
+  const int h = (threadIdx.x >> 5) & 1;
+  const float p1 = __shfl_xor(M1, 32), p2 = __shfl_xor(M2, 32);
+  const int pB = __shfl_xor(B1, 32);
+  // lanes h = 0 decide; the other half wins only with a strictly smaller best
+  const bool other = p1 < M1;
+  const uint32_t vw = __float_as_uint(other ? p1 : M1) & kPackMask;
+  const int jstar = 32 * (other ? pB : B1) + 8 * (int)(vw >> 2) + (other ? 4 : 0) + (int)(vw & 3);
+  const float nm2 = min2(max2(M1, p1), min2(M2, p2));
+  M1 = min2(M1, p1);
+  M2 = nm2;
+  const float Mk = cf.nmaxf + 2.0f * knv * cf.rmaxf;
+  const float aM1 = fabsf(M1);
+  const float E = (cf.cm * Mk + cf.cp * (aM1 + 3.0f * cf.cm * Mk)) * (1.0f + 0x1p-20f) + 0x1p-22f * aM1 + 1e-30f;
+  const bool certain = (M2 > M1 + 2.0f * E) && (jstar < N);
+  const bool mine = valid && h == 0;
+  const bool unc = mine && !certain;
+  wave_append(__ballot(unc), unc, ((unsigned long long)key << 32) | (unsigned)oldv, &sh.c->nunc, sh.uq);
+  if (mine && certain) belong_bh[key] = jstar;
+  if (!FIRST) {
+    const bool moved = mine && certain && oldv != jstar;
+    wave_append(__ballot(moved), moved, ((unsigned long long)key << 32) | ((unsigned)oldv << 16) | (unsigned)jstar,
+                &sh.c->nmoved, sh.wrec);
+  }
+}
+
+// After every tile of the workgroup is scored: the four waves take the queued
+// keys in turn and decide each with exact_argmin_lds (the key row staged in
+// the wave's LDS slot), then store and record it like decide_tile.
+template <bool FIRST>
+__device__ __forceinline__ void exact_decide_queue(const uint16_t* __restrict__ Kbh, const uint16_t* Rs,
+                                                   const double* __restrict__ nrm_bh, int N,
+                                                   int32_t* __restrict__ belong_bh, uint16_t* kslot_w,
+                                                   const AssignLists& sh) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nunc = sh.c->nunc;
+  for (int u = wave; u < nunc; u += 4) {
+    const unsigned long long rec = sh.uq[u];
+    const int64_t key = (int64_t)(rec >> 32);
+    const int oldv = (int)(rec & 0xffffffffu);
+    if (lane < 8) *(u32x4*)(kslot_w + lane * 8) = *(const u32x4*)(Kbh + key * 64 + lane * 8);
+    const int jb = exact_argmin_lds(kslot_w, Rs, nrm_bh, N);
+    if (lane == 0) {
+      belong_bh[key] = jb;
+      if (!FIRST && oldv != jb)
+        sh.wrec[atomicAdd(&sh.c->nmoved, 1)] = ((unsigned long long)key << 32) | ((unsigned)oldv << 16) | (unsigned)jb;
+    }
+  }
+}
+
+// Stage -2R (swizzled, see swz) and the |r|^2 split of one slice into LDS and
+// return the slice's largest canonical |r|^2.  Padded groups (j >= N) get
+// zero rows and the largest bf16 as |r|^2, so they never win.  Ends with a
+// barrier.
+__device__ __forceinline__ double stage_reps(const uint16_t* __restrict__ Rbh, const uint16_t* __restrict__ nsplit_bh,
+                                             const double* __restrict__ nrm_bh, int N, int Npad, uint16_t* Rs,
+                                             uint16_t* Ns, double* red) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   for (int idx = tid; idx < Npad * 8; idx += 256) {
     const int row = idx >> 3, ch = idx & 7;
     u32x4 v = {0u, 0u, 0u, 0u};
@@ -276,26 +379,108 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
   }
   double mx = 0.0;
   for (int j = tid; j < Npad; j += 256) {
-    // padded groups get the largest bf16 as |r|^2 so they never win
-    const u32x4 sp = j < N ? *(const u32x4*)(nsplit + (bh * N + j) * 8) : u32x4{0x7f7fu, 0u, 0u, 0u};
+    const u32x4 sp = j < N ? *(const u32x4*)(nsplit_bh + j * 8) : u32x4{0x7f7fu, 0u, 0u, 0u};
     *(u32x4*)(Ns + j * 8) = sp;
-    if (j < N) mx = fmax(mx, nrm64[bh * N + j]);
+    if (j < N) mx = fmax(mx, nrm_bh[j]);
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
   if (lane == 0) red[wave] = mx;
-  if (tid == 0) nmoved = 0;
   __syncthreads();
-  const double nmax = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+  return fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+}
+
+// Dynamic LDS of the assign kernels: -2R as [Npad][64] bf16 (swizzled), the
+// |r|^2 split as [Npad][8] bf16, then the moved-key records and the
+// uncertain-key queue, 4 tpw 32 entries each.
+struct AssignLds {
+  uint16_t* Rs;
+  uint16_t* Ns;
+  AssignLists lists;
+};
+
+__device__ __forceinline__ AssignLds assign_lds_layout(unsigned char* smem, int Npad, int tpw, AssignCounts* c) {
+  AssignLds l;
+  l.Rs = (uint16_t*)smem;
+  l.Ns = l.Rs + Npad * 64;
+  l.lists.c = c;
+  l.lists.wrec = (unsigned long long*)(l.Ns + Npad * 8);
+  l.lists.uq = l.lists.wrec + 4 * tpw * 32;
+  return l;
+}
+
+template <bool FIRST>
+__device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh, const uint16_t* Rs,
+                                                const double* __restrict__ nrm_bh, int n, int N,
+                                                int32_t* __restrict__ belong_bh, int32_t* __restrict__ mcount_bh,
+                                                unsigned long long* __restrict__ mrec_bh, uint16_t* kslot_w,
+                                                const AssignLists& sh) {
+  const int tid = threadIdx.x;
+  __syncthreads();
+  if (sh.c->nunc) {  // uniform: read after the barrier
+    exact_decide_queue<FIRST>(Kbh, Rs, nrm_bh, N, belong_bh, kslot_w, sh);
+    __syncthreads();
+  }
+  if (!FIRST) {
+    if (tid == 0) sh.c->moved_base = sh.c->nmoved ? atomicAdd(mcount_bh, sh.c->nmoved) : 0;
+    __syncthreads();
+    const int nm = sh.c->nmoved, base = sh.c->moved_base;
+    for (int x = tid; x < nm; x += 256) mrec_bh[base + x] = sh.wrec[x];
+  }
+}
+
+// MFMA 32x32x16 scoring shared by both assign kernels: rows = 32 groups
+// (A = -2R), columns = 32 keys (B = K).  Lane l (h = l/32, q = l%32) supplies
+// at k-step s features 32h + 8s .. +7 of its row for both operands (the same
+// permutation of the contraction axis on both sides) and receives groups
+// 8(v/4) + 4h + v%4 of key q in accumulator register v.  A fifth k-step adds
+// |r_j|^2 = hi + mid + lo (A = the split, B = ones in the first three slots
+// of lanes h = 0), so each output is the score s_ij = |r_j|^2 - 2 k_i.r_j.
+//
+// If second - best > 2E, where E bounds |packed - exact| (the MFMA fp32
+// accumulation, the split of |r|^2 and the packing), the packed best is
+// provably the exact fp64 argmin; otherwise the key is queued and re-decided
+// by exact_argmin_lds once the workgroup's tiles are done.  Later rounds
+// (FIRST = false) also emit the keys whose group changed as records
+// (key, old, new), one global atomic per workgroup.
+//
+// k_assign_bf16: grid (ceil(tiles / (4 * tpw)), BH), 256 threads, any N up to
+// 1024 (k_assign_reg covers N <= 128).  Each wave owns tpw consecutive 32-key
+// tiles and scores them two at a time (two independent MFMA / VALU chains
+// sharing the A-operand reads, which come from LDS); the next pair's key
+// fragments are loaded while the current pair is scored.
+template <bool FIRST>
+__global__ __launch_bounds__(256) void k_assign_bf16(
+    const uint16_t* __restrict__ K, const uint16_t* __restrict__ R, const uint16_t* __restrict__ nsplit,
+    const double* __restrict__ nrm64, float* __restrict__ knorm, int32_t* __restrict__ belong,
+    int32_t* __restrict__ mcount, unsigned long long* __restrict__ mrec, int n, int N, int tpw, float cm,
+    float cp) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ double red[4];
+  __shared__ AssignCounts cnt;
+  __shared__ __align__(16) uint16_t kslot[4][64];  // key row of a queued key, per wave
+  const int Npad = (N + 31) & ~31;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
+  const int64_t bh = blockIdx.y;
+  if (tid == 0) {
+    cnt.nmoved = 0;
+    cnt.nunc = 0;
+  }
+  const AssignLds L = assign_lds_layout(smem, Npad, tpw, &cnt);
+  const uint16_t* Rs = L.Rs;
+  const uint16_t* Ns = L.Ns;
+  const double nmax = stage_reps(R + bh * (int64_t)N * 64, nsplit + bh * N * 8, nrm64 + bh * N, N, Npad, L.Rs, L.Ns,
+                                 red);
   const float nmaxf = (float)nmax * (1.0f + 0x1p-20f);
   const float rmaxf = sqrtf(nmaxf) * (1.0f + 0x1p-20f);
+  const Certify cf = {nmaxf, rmaxf, cm, cp};
 
   const int nblk = Npad >> 5;
-  const uint32_t keep = ~((1u << codebits) - 1u);
-  const uint32_t codemask = (1u << codebits) - 1u;
   const int64_t tile0 = ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(wave)) * tpw;
   const int64_t ntiles = ((int64_t)n + 31) / 32;
   const int tcount = (int)max((int64_t)0, min((int64_t)tpw, ntiles - tile0));
+  const uint16_t* Kbh = K + bh * (int64_t)n * 64;
+  int32_t* belong_bh = belong + bh * n;
   // B operand of the |r|^2 k-step: ones in the first three slots of lanes h = 0
   const u32x4 ones = h == 0 ? u32x4{0x3f803f80u, 0x3f80u, 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
   const f32x16 zero = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -306,12 +491,12 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
   auto fetch = [&](int t, u32x4 (&f)[4], float& knv, int& oldv) {
     const int64_t key = (tile0 + t) * 32 + q;
     const bool valid = t < tcount && key < n;
-    const uint16_t* krow = K + (bh * n + (valid ? key : 0)) * 64 + h * 32;
+    const uint16_t* krow = Kbh + (valid ? key : 0) * 64 + h * 32;
 #pragma unroll
     for (int s2 = 0; s2 < 4; ++s2) f[s2] = valid ? *(const u32x4*)(krow + s2 * 8) : u32x4{0u, 0u, 0u, 0u};
     if (!FIRST) {
       knv = valid ? knorm[bh * n + key] : 0.f;
-      oldv = (valid && h == 0) ? belong[bh * n + key] : 0;
+      oldv = valid ? belong_bh[key] : 0;
     }
   };
   if (tcount > 0) {
@@ -334,22 +519,13 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
       key[u] = (tile0 + tt + u) * 32 + q;
       valid[u] = tt + u < tcount && key[u] < n;
       if (FIRST) {
-        float ss = 0.f;
-#pragma unroll
-        for (int s2 = 0; s2 < 4; ++s2)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float lo = bf16_to_f32(kf[u][s2][e] & 0xffffu), hi = bf16_to_f32(kf[u][s2][e] >> 16);
-            ss = fmaf(lo, lo, ss);
-            ss = fmaf(hi, hi, ss);
-          }
-        ss += __shfl_xor(ss, 32);
-        kn[u] = sqrtf(ss) * (1.0f + 0x1p-16f);
+        kn[u] = key_norm_bound(kf[u]);
         if (valid[u] && h == 0) knorm[bh * n + key[u]] = kn[u];
       }
     }
 
     float M1[2] = {FLT_MAX, FLT_MAX}, M2[2] = {FLT_MAX, FLT_MAX};
+    int B1[2] = {0, 0};
     for (int blk = 0; blk < nblk; ++blk) {
       // lanes h = 1 read the same split row; their B operand is zero
       const u32x4 an = *(const u32x4*)(Ns + (blk * 32 + q) * 8);
@@ -367,74 +543,12 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
         for (int u = 0; u < 2; ++u)
           acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[s2]),
                                                            __builtin_bit_cast(bf16x8, kf[u][s2]), acc[u], 0, 0, 0);
-      // Within the block the group is 32 blk + 8 (v/4) + 4 h + v%4: the
-      // register part 8 (v/4) + v%4 is packed per score (an inline constant),
-      // the lane-half and block bits once per block into the block's top-2
-      // (OR-ing the same bits into cleared bits preserves the order).  Top-2
-      // over pairs: with m1 <= m2 the two smallest so far, the second smallest
-      // of {m1, m2, x, y} is min(m2, med3(m1, x, y)).
-      const uint32_t bb = ((uint32_t)blk << 5) | ((uint32_t)h << 2);
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        float m1 = FLT_MAX, m2 = FLT_MAX;
-#pragma unroll
-        for (int v = 0; v < 16; v += 2) {
-          const float x = __uint_as_float((__float_as_uint(acc[u][v]) & keep) | (uint32_t)(8 * (v >> 2) + (v & 3)));
-          const float y = __uint_as_float((__float_as_uint(acc[u][v + 1]) & keep) |
-                                          (uint32_t)(8 * ((v + 1) >> 2) + ((v + 1) & 3)));
-          m2 = min2(m2, __builtin_amdgcn_fmed3f(m1, x, y));
-          m1 = min3f(m1, x, y);
-        }
-        m1 = __uint_as_float(__float_as_uint(m1) | bb);
-        m2 = __uint_as_float(__float_as_uint(m2) | bb);
-        const float nm2 = min2(max2(M1[u], m1), min2(M2[u], m2));
-        M1[u] = min2(M1[u], m1);
-        M2[u] = nm2;
-      }
+      for (int u = 0; u < 2; ++u) reduce_block(acc[u], blk, M1[u], M2[u], B1[u]);
     }
-
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      {
-        const float p1 = __shfl_xor(M1[u], 32), p2 = __shfl_xor(M2[u], 32);
-        const float nm2 = min2(max2(M1[u], p1), min2(M2[u], p2));
-        M1[u] = min2(M1[u], p1);
-        M2[u] = nm2;
-      }
-      // E bounds |packed - exact| for the best and for any group that could
-      // beat it: the MFMA part cm * M (M = max |r|^2 + 2 |k| max |r| bounds the
-      // sum of |terms|) and the packing part cp * (|M1| + 3 cm M); the last
-      // two terms cover the fp32 evaluation of E and of M1 + 2E.
-      int jstar = (int)(__float_as_uint(M1[u]) & codemask);
-      const float Mk = nmaxf + 2.0f * kn[u] * rmaxf;
-      const float aM1 = fabsf(M1[u]);
-      const float E = (cm * Mk + cp * (aM1 + 3.0f * cm * Mk)) * (1.0f + 0x1p-20f) + 0x1p-22f * aM1 + 1e-30f;
-      const bool certain = (M2[u] > M1[u] + 2.0f * E) && (jstar < N);
-      uint64_t unc = __ballot(valid[u] && !certain && h == 0);
-      while (unc) {
-        const int b = __ffsll((unsigned long long)unc) - 1;
-        unc &= unc - 1;
-        if (q == b) {
-#pragma unroll
-          for (int s2 = 0; s2 < 4; ++s2) *(u32x4*)(&kslot[wave][h * 32 + s2 * 8]) = kf[u][s2];
-        }
-        const int jb = exact_argmin_lds(kslot[wave], Rs, nrm64 + bh * N, N);
-        if (q == b) jstar = jb;
-      }
-      if (valid[u] && h == 0) belong[bh * n + key[u]] = jstar;
-      if (!FIRST) {
-        const bool moved = valid[u] && h == 0 && old[u] != jstar;
-        const uint64_t mv = __ballot(moved);
-        if (mv) {
-          int base = 0;
-          if (lane == 0) base = atomicAdd(&nmoved, __popcll(mv));
-          base = __builtin_amdgcn_readfirstlane(base);
-          if (moved)
-            wrec[base + __popcll(mv & ((1ull << lane) - 1ull))] =
-                ((unsigned long long)key[u] << 32) | ((unsigned)old[u] << 16) | (unsigned)jstar;
-        }
-      }
-    }
+    for (int u = 0; u < 2; ++u)
+      decide_tile<FIRST>(M1[u], M2[u], B1[u], kn[u], old[u], key[u], valid[u], N, cf, belong_bh, L.lists);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
 #pragma unroll
@@ -443,12 +557,129 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
       old[u] = old_n[u];
     }
   }
+  assign_epilogue<FIRST>(Kbh, Rs, nrm64 + bh * N, n, N, belong_bh, mcount + bh, mrec + bh * n, kslot[wave], L.lists);
+}
+
+// Key fragments of tile `tile` of a slice, and in later rounds the keys' |k|
+// bound and previous group.  Keys past n read the slice's last key instead
+// (their results are never stored), so every lane loads unconditionally.
+template <bool FIRST>
+__device__ __forceinline__ void load_keys(const uint16_t* __restrict__ Kbh, const float* __restrict__ knorm_bh,
+                                          const int32_t* __restrict__ belong_bh, int64_t tile, int n, int q, int h,
+                                          u32x4 (&f)[4], float& knv, int& oldv) {
+  const int64_t key = min(tile * 32 + q, (int64_t)n - 1);
+  const uint16_t* krow = Kbh + key * 64 + h * 32;
+#pragma unroll
+  for (int s2 = 0; s2 < 4; ++s2) f[s2] = *(const u32x4*)(krow + s2 * 8);
   if (!FIRST) {
-    __syncthreads();
-    if (tid == 0) moved_base = nmoved ? atomicAdd(mcount + bh, nmoved) : 0;
-    __syncthreads();
-    for (int x = tid; x < nmoved; x += 256) mrec[bh * n + moved_base + x] = wrec[x];
+    knv = knorm_bh[key];
+    oldv = belong_bh[key];
   }
+}
+
+// Scores of one tile against all NB blocks of groups and the lane's top-2.
+// Block b + 1's five MFMAs are interleaved with block b's reduction (all in
+// one straight-line region), so the matrix cores and the VALU work together.
+template <int NB>
+__device__ __forceinline__ void score_tile(const u32x4 (&af)[NB][4], const u32x4 (&an)[NB], const u32x4& ones,
+                                           const u32x4 (&kf)[4], float& M1, float& M2, int& B1) {
+  const f32x16 zero = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  f32x16 acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, an[b]),
+                                                     __builtin_bit_cast(bf16x8, ones), zero, 0, 0, 0);
+#pragma unroll
+    for (int s2 = 0; s2 < 4; ++s2)
+      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[b][s2]),
+                                                       __builtin_bit_cast(bf16x8, kf[s2]), acc[b], 0, 0, 0);
+  }
+  M1 = FLT_MAX;
+  M2 = FLT_MAX;
+  B1 = 0;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) reduce_block(acc[b], b, M1, M2, B1);
+  __builtin_amdgcn_sched_group_barrier(0x008, 5, 0);  // block 0's MFMAs
+#pragma unroll
+  for (int b = 1; b < NB; ++b)
+#pragma unroll
+    for (int g = 0; g < 5; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA of block b
+      __builtin_amdgcn_sched_group_barrier(0x002, 9, 0);  // VALU of block b - 1
+    }
+}
+
+// k_assign_reg: the variant for N <= 32 NB (NB = 1..4).  Each lane keeps its
+// A fragments of -2R and of the |r|^2 split for all NB blocks in VGPRs (read
+// once from LDS), so the scoring loop issues no LDS reads; only the exact
+// re-decisions read the LDS copy.  The key fragments of the next tile are
+// loaded while the current one is scored (two register sets used in turn, no
+// copies).  Same grid, LDS layout, scores, certification and outputs as
+// k_assign_bf16.
+template <bool FIRST, int NB>
+__global__ __launch_bounds__(256) void k_assign_reg(
+    const uint16_t* __restrict__ K, const uint16_t* __restrict__ R, const uint16_t* __restrict__ nsplit,
+    const double* __restrict__ nrm64, float* __restrict__ knorm, int32_t* __restrict__ belong,
+    int32_t* __restrict__ mcount, unsigned long long* __restrict__ mrec, int n, int N, int tpw, float cm,
+    float cp) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ double red[4];
+  __shared__ AssignCounts cnt;
+  __shared__ __align__(16) uint16_t kslot[4][64];  // key row of a queued key, per wave
+  constexpr int Npad = NB * 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
+  const int64_t bh = blockIdx.y;
+  if (tid == 0) {
+    cnt.nmoved = 0;
+    cnt.nunc = 0;
+  }
+  const AssignLds L = assign_lds_layout(smem, Npad, tpw, &cnt);
+  const double nmax = stage_reps(R + bh * (int64_t)N * 64, nsplit + bh * N * 8, nrm64 + bh * N, N, Npad, L.Rs, L.Ns,
+                                 red);
+  const float nmaxf = (float)nmax * (1.0f + 0x1p-20f);
+  const float rmaxf = sqrtf(nmaxf) * (1.0f + 0x1p-20f);
+  const Certify cf = {nmaxf, rmaxf, cm, cp};
+
+  u32x4 af[NB][4], an[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    an[b] = *(const u32x4*)(L.Ns + (b * 32 + q) * 8);  // lanes h = 1 read it too; their B is zero
+#pragma unroll
+    for (int s2 = 0; s2 < 4; ++s2) af[b][s2] = *(const u32x4*)(L.Rs + swz(b * 32 + q, 4 * h + s2));
+  }
+  const u32x4 ones = h == 0 ? u32x4{0x3f803f80u, 0x3f80u, 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
+
+  const int64_t tile0 = ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(wave)) * tpw;
+  const int64_t ntiles = ((int64_t)n + 31) / 32;
+  const int tcount = (int)max((int64_t)0, min((int64_t)tpw, ntiles - tile0));
+  const uint16_t* Kbh = K + bh * (int64_t)n * 64;
+  float* knorm_bh = knorm + bh * n;
+  int32_t* belong_bh = belong + bh * n;
+
+  u32x4 kA[4], kB[4];
+  float knA = 0.f, knB = 0.f;
+  int oldA = 0, oldB = 0;
+  auto run = [&](const u32x4 (&kf)[4], float knv, int oldv, int t) __attribute__((always_inline)) {
+    const int64_t key = (tile0 + t) * 32 + q;
+    const bool valid = key < n;
+    if (FIRST) {
+      knv = key_norm_bound(kf);
+      if (valid && h == 0) knorm_bh[key] = knv;
+    }
+    float M1, M2;
+    int B1;
+    score_tile<NB>(af, an, ones, kf, M1, M2, B1);
+    decide_tile<FIRST>(M1, M2, B1, knv, oldv, key, valid, N, cf, belong_bh, L.lists);
+  };
+  if (tcount > 0) load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0, n, q, h, kA, knA, oldA);
+  for (int t = 0; t < tcount; t += 2) {
+    if (t + 1 < tcount) load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + t + 1, n, q, h, kB, knB, oldB);
+    run(kA, knA, oldA, t);
+    if (t + 1 >= tcount) break;
+    if (t + 2 < tcount) load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + t + 2, n, q, h, kA, knA, oldA);
+    run(kB, knB, oldB, t + 1);
+  }
+  assign_epilogue<FIRST>(Kbh, L.Rs, nrm64 + bh * N, n, N, belong_bh, mcount + bh, mrec + bh * n, kslot[wave], L.lists);
 }
 
 // ------------------------------------------------------------------ assign (exact)
@@ -1040,7 +1271,7 @@ constexpr size_t kAssignLdsMax = 160 * 1024 - 1024;  // dynamic LDS budget (stat
 
 size_t assign_lds(int N, int tpw = 12) {
   const int Npad = (N + 31) & ~31;
-  return (size_t)Npad * 128 + (size_t)Npad * 16 + (size_t)4 * tpw * 32 * 8;
+  return (size_t)Npad * 128 + (size_t)Npad * 16 + (size_t)4 * tpw * 32 * 16;
 }
 size_t bucket_lds(int N) { return (size_t)16 * N * 8 + (size_t)2 * N * 4; }
 size_t attend_lds(int N) {
@@ -1131,27 +1362,35 @@ hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint
   set_lds_limits();
   if (d.dtype == 1) {
     const int64_t tiles = (d.n + 31) / 32;
-    // about 1024 workgroups (4 per CU), as many tiles each as the LDS allows
-    int64_t tpw = (d.BH * tiles + 4 * 1024 - 1) / (4 * 1024);
-    while (tpw > 1 && assign_lds(d.N, (int)tpw) > kAssignLdsMax) --tpw;
+    // about 512 workgroups (two per CU, all resident at once), the same number
+    // for every slice, as many tiles each as the LDS allows (at most 16 per wave)
+    const int64_t wg_per_slice = d.BH >= 512 ? 1 : 512 / d.BH;
+    int64_t tpw = (tiles + 4 * wg_per_slice - 1) / (4 * wg_per_slice);
     tpw = tpw < 1 ? 1 : (tpw > 16 ? 16 : tpw);
+    while (tpw > 1 && assign_lds(d.N, (int)tpw) > kAssignLdsMax) --tpw;
     const int Npad = (d.N + 31) & ~31;
-    int codebits = 5;
-    while ((1 << codebits) < Npad) ++codebits;
     // |MFMA fp32 accumulation error| <= (d + 4) 2^-24 * 2 * sum|terms| (each of the
     // d products and the three |r|^2 terms added with at most one rounding,
     // sequential model, 2x margin; the split itself is within 2^-24 |r|^2);
-    // packing the index moves a value by < 2^(codebits - 23) of its magnitude.
+    // packing the register index into the low 4 mantissa bits moves a value by
+    // < 2^(4 - 23) of its magnitude.
     const float cm = (float)(kD + 4) * 0x1p-23f * (1.0f + 0x1p-10f);
-    const float cp = ldexpf(1.0f, codebits - 23) * (1.0f + 0x1p-10f);
+    const float cp = 0x1p-19f * (1.0f + 0x1p-10f);
     const dim3 grid(cdiv(tiles, 4 * tpw), (unsigned)d.BH), block(256);
     const size_t lds = assign_lds(d.N, (int)tpw);
-    if (first)
-      hipLaunchKernelGGL(k_assign_bf16<true>, grid, block, lds, st, (const uint16_t*)K, (const uint16_t*)R,
-                         nsplit, nrm64, knorm, belong, mcount, mrec, d.n, d.N, (int)tpw, cm, cp, codebits);
-    else
-      hipLaunchKernelGGL(k_assign_bf16<false>, grid, block, lds, st, (const uint16_t*)K, (const uint16_t*)R,
-                         nsplit, nrm64, knorm, belong, mcount, mrec, d.n, d.N, (int)tpw, cm, cp, codebits);
+    // Npad <= 128: the register-resident kernel, one instantiation per block count
+    using AssignFn = void (*)(const uint16_t*, const uint16_t*, const uint16_t*, const double*, float*, int32_t*,
+                              int32_t*, unsigned long long*, int, int, int, float, float);
+    AssignFn kern = first ? k_assign_bf16<true> : k_assign_bf16<false>;
+    switch (Npad >> 5) {
+      case 1: kern = first ? k_assign_reg<true, 1> : k_assign_reg<false, 1>; break;
+      case 2: kern = first ? k_assign_reg<true, 2> : k_assign_reg<false, 2>; break;
+      case 3: kern = first ? k_assign_reg<true, 3> : k_assign_reg<false, 3>; break;
+      case 4: kern = first ? k_assign_reg<true, 4> : k_assign_reg<false, 4>; break;
+      default: break;
+    }
+    hipLaunchKernelGGL(kern, grid, block, lds, st, (const uint16_t*)K, (const uint16_t*)R, nsplit, nrm64, knorm,
+                       belong, mcount, mrec, d.n, d.N, (int)tpw, cm, cp);
   } else {
     const int kpw = 4;
     const dim3 grid(cdiv(d.n, 4 * kpw), (unsigned)d.BH), block(256);
