@@ -83,25 +83,20 @@ ga::Dims dims_of(const ga_shape_t& s, int32_t N) {
 
 // Grouping on validated arguments.
 // bf16: the first round sums every member; later rounds apply only the keys
-// that changed group (exact fp64 sums make the order irrelevant).  fp32: every
-// round re-sums the members in ascending key order (fp32 sums need not be exact).
+// that changed group (exact fp64 sums make the order irrelevant).  Round t's
+// moved-key records are counted in mcount[t % 2].  fp32: every round re-sums
+// the members in ascending key order (fp32 sums need not be exact).
 int run_cluster(const ga::Dims& d, const void* K, int32_t iters, const float* init, int32_t* belong,
                 int32_t* count, float* C, const ga::Workspace& w, hipStream_t st) {
   GA_LAUNCH(ga::launch_init(d, K, init, C, w.R, w.nrm64, w.nsplit, w.mcount, st), "init launch");
   for (int t = 0; t < iters; ++t) {
-    GA_LAUNCH(ga::launch_assign(d, K, w.R, w.nsplit, w.nrm64, w.knorm, belong, w.mcount, w.mrec, t == 0, st),
+    int32_t* mc_cur = w.mcount + (t & 1) * d.BH;
+    int32_t* mc_next = w.mcount + ((t + 1) & 1) * d.BH;
+    GA_LAUNCH(ga::launch_assign(d, K, w.R, w.nsplit, w.nrm64, w.knorm, belong, mc_cur, w.mrec, t == 0, st),
               "assign launch");
     if (d.dtype == GA_BF16) {
-      if (t == 0) {
-        GA_LAUNCH(ga::launch_full_bucket(d, belong, w.perm, w.grp, count, st), "bucket launch");
-        GA_LAUNCH(ga::launch_segsum_bf16(d, 0, K, w.perm, w.llist, w.grp, count, w.S64, C, w.R, w.nrm64,
-                                         w.nsplit, st), "update launch");
-      } else {
-        GA_LAUNCH(ga::launch_moved_bucket(d, w.mrec, w.mcount, w.perm, w.llist, w.grp, count, st),
-                  "bucket launch");
-        GA_LAUNCH(ga::launch_segsum_bf16(d, 1, K, w.perm, w.llist, w.grp, count, w.S64, C, w.R, w.nrm64,
-                                         w.nsplit, st), "update launch");
-      }
+      GA_LAUNCH(ga::launch_gsum(d, t == 0 ? 0 : 1, K, belong, w.mrec, mc_cur, mc_next, w.S64, count, C, w.R,
+                                w.nrm64, w.nsplit, st), "update launch");
     } else {
       GA_LAUNCH(ga::launch_bucket(d, belong, w.perm, w.goff, count, st), "bucket launch");
       GA_LAUNCH(ga::launch_update(d, K, w.perm, w.goff, count, C, w.R, w.nrm64, w.nsplit, st), "update launch");
@@ -114,9 +109,8 @@ int run_cluster(const ga::Dims& d, const void* K, int32_t iters, const float* in
 int run_valuesum(const ga::Dims& d, const void* V, const int32_t* belong, int32_t* count, float* vsum,
                  const ga::Workspace& w, hipStream_t st) {
   if (d.dtype == GA_BF16) {
-    GA_LAUNCH(ga::launch_full_bucket(d, belong, w.perm, w.grp, count, st), "bucket launch");
-    GA_LAUNCH(ga::launch_segsum_bf16(d, 2, V, w.perm, w.llist, w.grp, count, w.S64, vsum, nullptr, nullptr,
-                                     nullptr, st), "value-sum launch");
+    GA_LAUNCH(ga::launch_gsum(d, 2, V, belong, nullptr, nullptr, nullptr, nullptr, nullptr, vsum, nullptr, nullptr,
+                              nullptr, st), "value-sum launch");
   } else {
     GA_LAUNCH(ga::launch_bucket(d, belong, w.perm, w.goff, count, st), "bucket launch");
     GA_LAUNCH(ga::launch_valuesum(d, V, w.perm, w.goff, count, vsum, st), "value-sum launch");

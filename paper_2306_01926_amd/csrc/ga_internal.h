@@ -27,10 +27,8 @@ struct Workspace {
   uint16_t* Vt;      // [BH][64][vt_stride] bf16 per-group value means, transposed
   float* ginit;      // [BH][Npad] score-accumulator init, log2(count)/(|scale| log2 e)
   double* S64;       // [BH][N][64] fp64 member sums carried across rounds (bf16 path)
-  int32_t* mcount;   // [BH] moved-key records of the current round
+  int32_t* mcount;   // [2][BH] moved-key records of rounds t with t % 2 = 0, 1
   unsigned long long* mrec;  // [BH][n] records (key << 32 | old << 16 | new)
-  int4* grp;         // [BH][N] {first join, joins, first leave, leaves} (or {first, members, 0, 0})
-  int32_t* llist;    // [BH][n] keys leaving each group (joins / full lists use perm)
 };
 
 struct Dims {
@@ -58,16 +56,11 @@ hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C
 hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint16_t* nsplit,
                          const double* nrm64, float* knorm, int32_t* belong, int32_t* mcount,
                          unsigned long long* mrec, bool first, hipStream_t st);
-// bf16 path: order-free bucketing and segmented sums (see ga_kernels.hip)
-hipError_t launch_full_bucket(const Dims& d, const int32_t* belong, int32_t* list, int4* grp,
-                              int32_t* count, hipStream_t st);
-hipError_t launch_moved_bucket(const Dims& d, const unsigned long long* mrec, int32_t* mcount,
-                               int32_t* jlist, int32_t* llist, int4* grp, int32_t* count,
-                               hipStream_t st);
-hipError_t launch_segsum_bf16(const Dims& d, int mode, const void* X, const int32_t* jlist,
-                              const int32_t* llist, const int4* grp, const int32_t* count,
-                              double* S64, float* out, void* R, double* nrm64, uint16_t* nsplit,
-                              hipStream_t st);
+// bf16 path: exact fp64 group sums, each workgroup finishing its own groups (see ga_kernels.hip)
+hipError_t launch_gsum(const Dims& d, int mode, const void* X, const int32_t* belong,
+                       const unsigned long long* mrec, const int32_t* mcount_cur, int32_t* mcount_next,
+                       double* S64, int32_t* count, float* out, void* R, double* nrm64, uint16_t* nsplit,
+                       hipStream_t st);
 hipError_t launch_bucket(const Dims& d, const int32_t* belong, int32_t* perm, int32_t* goff,
                          int32_t* count, hipStream_t st);
 hipError_t launch_update(const Dims& d, const void* K, const int32_t* perm, const int32_t* goff,

@@ -172,26 +172,14 @@ __global__ __launch_bounds__(256) void k_init(const typename S::T* __restrict__ 
   const float c = init ? init[row * 64 + lane]
                        : S::load(K, (bh * n + ((int64_t)g * n) / N) * 64 + lane);
   C[row * 64 + lane] = c;
-  if (mcount && g == 0 && lane == 0) mcount[bh] = 0;
+  if (mcount && g == 0 && lane == 0) {
+    mcount[bh] = 0;
+    mcount[gridDim.y + bh] = 0;
+  }
   finalize_rep<S>(c, row, R, nrm64, nsplit);
 }
 
 // ------------------------------------------------------------------ assign (bf16, MFMA)
-// Upper bound of |k| for the key whose 64 bf16 features are split over lanes
-// q and q + 32 (32 each, as MFMA fragments).
-__device__ __forceinline__ float key_norm_bound(const u32x4 (&f)[4]) {
-  float ss = 0.f;
-#pragma unroll
-  for (int s2 = 0; s2 < 4; ++s2)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float lo = bf16_to_f32(f[s2][e] & 0xffffu), hi = bf16_to_f32(f[s2][e] >> 16);
-      ss = fmaf(lo, lo, ss);
-      ss = fmaf(hi, hi, ss);
-    }
-  ss += __shfl_xor(ss, 32);
-  return sqrtf(ss) * (1.0f + 0x1p-16f);
-}
 
 // The assign kernel's LDS copy of -2R stores 16-byte chunk c of row r at chunk
 // c ^ ((r >> 1) & 7) of a 128-byte row: 16 consecutive rows reading the same
@@ -270,118 +258,180 @@ struct Certify {
   float nmaxf, rmaxf, cm, cp;
 };
 
-// Per-workgroup lists of the assign kernels (in LDS): moved-key records and
-// the queue of keys whose packed top-2 was not certified, with their counts.
+// Per-workgroup state of the assign kernels, in LDS.  Keys are numbered
+// locally within the workgroup (lk < 4 tpw 32 <= 2048, 11 bits; groups < 1024,
+// 10 bits).  The groups (and in the first round the |k| bounds) are staged
+// here and written out once at the end, so the scoring loop issues no global
+// stores and the only memory operations between a tile's prefetch and its use
+// are the unconditional loads of the next tile (which keeps the compiler's
+// wait counts exact).  Each wave appends moved keys and uncertain keys to its
+// own region of tpw 32 entries with a wave-uniform counter (no atomics).
 struct AssignCounts {
-  int nmoved, nunc, moved_base;
+  int wcnt[4], ucnt[4];  // per-wave moved / uncertain entries
+  int nx, moved_base;    // moved keys found by the exact decisions
 };
 struct AssignLists {
   AssignCounts* c;
-  unsigned long long* wrec;  // (key << 32) | (old << 16) | new
-  unsigned long long* uq;    // (key << 32) | old
+  uint32_t* wrec;  // [4][tpw 32] moved keys: lk | old << 11 | new << 21
+  uint32_t* uq;    // [4][tpw 32] uncertain keys: lk | old << 11
+  int32_t* bst;    // [4 tpw 32] group of every local key
+  uint32_t* kx;    // [4 tpw 32] first round: |k| bounds (float bits); later: moved keys of the exact decisions
+  int cap;         // tpw 32
 };
 
-// Append the keys of `mask` (one bit per lane) to an LDS list with one
-// atomic per wave; `rec` is this lane's record.
-__device__ __forceinline__ void wave_append(uint64_t mask, bool mine, unsigned long long rec, int* count,
-                                            unsigned long long* list) {
-  if (!mask) return;
-  const int lane = threadIdx.x & 63;
-  int base = 0;
-  if (lane == 0) base = atomicAdd(count, __popcll(mask));
-  base = __builtin_amdgcn_readfirstlane(base);
-  if (mine) list[base + __popcll(mask & ((1ull << lane) - 1ull))] = rec;
+// (value of lane q, value of lane q + 32) in every lane l, q = l % 32.
+__device__ __forceinline__ u32x2 halves(uint32_t x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return u32x2{r[0], r[1]};
+}
+
+// Upper bound of |k| for the key whose 64 bf16 features are split over lanes
+// q and q + 32 (32 each, as MFMA fragments); the same value in both lanes.
+__device__ __forceinline__ float key_norm_bound(const u32x4 (&f)[4]) {
+  float ss = 0.f;
+#pragma unroll
+  for (int s2 = 0; s2 < 4; ++s2)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = bf16_to_f32(f[s2][e] & 0xffffu), hi = bf16_to_f32(f[s2][e] >> 16);
+      ss = fmaf(lo, lo, ss);
+      ss = fmaf(hi, hi, ss);
+    }
+  const u32x2 p = halves(__float_as_uint(ss));
+  return sqrtf(__uint_as_float(p[0]) + __uint_as_float(p[1])) * (1.0f + 0x1p-16f);
+}
+
+// Append this lane's entry if `mine`; the region's count `n` is wave-uniform.
+__device__ __forceinline__ void wave_append(bool mine, uint32_t rec, uint32_t* region, int& n) {
+  const uint64_t mask = __ballot(mine);
+  if (mine)
+    region[n + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u))] =
+        rec;
+  n += (int)__popcll(mask);
 }
 
 // Decision for the 32 keys of one tile, given each lane's top-2 over its half
-// of the groups: merge the halves, certify the packed best against the error
-// bound E, store the group and (later rounds) record keys whose group changed.
-// Keys that fail the test are queued for exact_decide_queue.
+// of the groups: merge the halves (both halves compute the same result),
+// certify the packed best against the error bound E, stage the group and
+// (later rounds) record keys whose group changed.  Keys that fail the test
+// are queued for exact_decide_queue (their staged group is provisional).
 //
 // E bounds |packed - exact| for the best and for any group that could beat
 // it: the MFMA part cm * M (M = max |r|^2 + 2 |k| max |r| bounds the sum of
 // |terms|) and the packing part cp * (|M1| + 3 cm M); the last two terms cover
 // the fp32 evaluation of E and of M1 + 2E.
 template <bool FIRST>
-__device__ __forceinline__ void decide_tile(float M1, float M2, int B1, float knv, int oldv, int64_t key, bool valid,
-                                            int N, const Certify& cf, int32_t* __restrict__ belong_bh,
-                                            const AssignLists& sh) {
+__device__ __forceinline__ void decide_tile(float M1, float M2, int B1, float knv, int oldv, int lk, bool valid,
+                                            int N, const Certify& cf, const AssignLists& sh, int wave, int& wn,
+                                            int& un) {
   const int h = (threadIdx.x >> 5) & 1;
-  const float p1 = __shfl_xor(M1, 32), p2 = __shfl_xor(M2, 32);
-  const int pB = __shfl_xor(B1, 32);
-  // lanes h = 0 decide; the other half wins only with a strictly smaller best
-  const bool other = p1 < M1;
-  const uint32_t vw = __float_as_uint(other ? p1 : M1) & kPackMask;
-  const int jstar = 32 * (other ? pB : B1) + 8 * (int)(vw >> 2) + (other ? 4 : 0) + (int)(vw & 3);
-  const float nm2 = min2(max2(M1, p1), min2(M2, p2));
-  M1 = min2(M1, p1);
-  M2 = nm2;
+  const u32x2 p1 = halves(__float_as_uint(M1)), p2 = halves(__float_as_uint(M2)), pb = halves((uint32_t)B1);
+  const float a1 = __uint_as_float(p1[0]), b1 = __uint_as_float(p1[1]);
+  // the half h = 1 wins only with a strictly smaller best
+  const bool hi_wins = b1 < a1;
+  const uint32_t vw = __float_as_uint(hi_wins ? b1 : a1) & kPackMask;
+  const int jstar = 32 * (int)(hi_wins ? pb[1] : pb[0]) + 8 * (int)(vw >> 2) + (hi_wins ? 4 : 0) + (int)(vw & 3);
+  const float best = min2(a1, b1);
+  const float second = min2(max2(a1, b1), min2(__uint_as_float(p2[0]), __uint_as_float(p2[1])));
   const float Mk = cf.nmaxf + 2.0f * knv * cf.rmaxf;
-  const float aM1 = fabsf(M1);
+  const float aM1 = fabsf(best);
   const float E = (cf.cm * Mk + cf.cp * (aM1 + 3.0f * cf.cm * Mk)) * (1.0f + 0x1p-20f) + 0x1p-22f * aM1 + 1e-30f;
-  const bool certain = (M2 > M1 + 2.0f * E) && (jstar < N);
+  const bool certain = (second > best + 2.0f * E) && (jstar < N);
   const bool mine = valid && h == 0;
-  const bool unc = mine && !certain;
-  wave_append(__ballot(unc), unc, ((unsigned long long)key << 32) | (unsigned)oldv, &sh.c->nunc, sh.uq);
-  if (mine && certain) belong_bh[key] = jstar;
-  if (!FIRST) {
-    const bool moved = mine && certain && oldv != jstar;
-    wave_append(__ballot(moved), moved, ((unsigned long long)key << 32) | ((unsigned)oldv << 16) | (unsigned)jstar,
-                &sh.c->nmoved, sh.wrec);
-  }
+  sh.bst[lk] = jstar;
+  wave_append(mine && !certain, (uint32_t)lk | ((uint32_t)oldv << 11), sh.uq + wave * sh.cap, un);
+  if (!FIRST)
+    wave_append(mine && certain && oldv != jstar,
+                (uint32_t)lk | ((uint32_t)oldv << 11) | ((uint32_t)jstar << 21), sh.wrec + wave * sh.cap, wn);
+}
+
+// Entry u of the concatenation of four per-wave regions with counts cnt[0..3].
+__device__ __forceinline__ uint32_t region_entry(const uint32_t* base, int cap, const int* cnt, int u) {
+  int r = 0;
+  while (r < 3 && u >= cnt[r]) u -= cnt[r++];
+  return base[r * cap + u];
 }
 
 // After every tile of the workgroup is scored: the four waves take the queued
 // keys in turn and decide each with exact_argmin_lds (the key row staged in
-// the wave's LDS slot), then store and record it like decide_tile.
+// the wave's LDS slot), then stage and record it like decide_tile.
 template <bool FIRST>
-__device__ __forceinline__ void exact_decide_queue(const uint16_t* __restrict__ Kbh, const uint16_t* Rs,
-                                                   const double* __restrict__ nrm_bh, int N,
-                                                   int32_t* __restrict__ belong_bh, uint16_t* kslot_w,
-                                                   const AssignLists& sh) {
+__device__ __forceinline__ void exact_decide_queue(const uint16_t* __restrict__ Kbh, int64_t key0, const uint16_t* Rs,
+                                                   const double* __restrict__ nrm_bh, int N, uint16_t* kslot_w,
+                                                   const AssignLists& sh, int nunc) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nunc = sh.c->nunc;
   for (int u = wave; u < nunc; u += 4) {
-    const unsigned long long rec = sh.uq[u];
-    const int64_t key = (int64_t)(rec >> 32);
-    const int oldv = (int)(rec & 0xffffffffu);
-    if (lane < 8) *(u32x4*)(kslot_w + lane * 8) = *(const u32x4*)(Kbh + key * 64 + lane * 8);
+    const uint32_t e = region_entry(sh.uq, sh.cap, sh.c->ucnt, u);
+    const int lk = (int)(e & 2047u), oldv = (int)(e >> 11);
+    if (lane < 8) *(u32x4*)(kslot_w + lane * 8) = *(const u32x4*)(Kbh + (key0 + lk) * 64 + lane * 8);
     const int jb = exact_argmin_lds(kslot_w, Rs, nrm_bh, N);
     if (lane == 0) {
-      belong_bh[key] = jb;
+      sh.bst[lk] = jb;
       if (!FIRST && oldv != jb)
-        sh.wrec[atomicAdd(&sh.c->nmoved, 1)] = ((unsigned long long)key << 32) | ((unsigned)oldv << 16) | (unsigned)jb;
+        sh.kx[atomicAdd(&sh.c->nx, 1)] = (uint32_t)lk | ((uint32_t)oldv << 11) | ((uint32_t)jb << 21);
     }
   }
 }
 
 // Stage -2R (swizzled, see swz) and the |r|^2 split of one slice into LDS and
 // return the slice's largest canonical |r|^2.  Padded groups (j >= N) get
-// zero rows and the largest bf16 as |r|^2, so they never win.  Ends with a
-// barrier.
+// zero rows and the largest bf16 as |r|^2, so they never win.  Every thread
+// issues all of its loads before converting (NPAD_C > 0: Npad known at
+// compile time).  Ends with a barrier.
+template <int NPAD_C>
 __device__ __forceinline__ double stage_reps(const uint16_t* __restrict__ Rbh, const uint16_t* __restrict__ nsplit_bh,
-                                             const double* __restrict__ nrm_bh, int N, int Npad, uint16_t* Rs,
+                                             const double* __restrict__ nrm_bh, int N, int Npad_rt, uint16_t* Rs,
                                              uint16_t* Ns, double* red) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int idx = tid; idx < Npad * 8; idx += 256) {
-    const int row = idx >> 3, ch = idx & 7;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (row < N) {
-      const u32x4 w = *(const u32x4*)(Rbh + (int64_t)row * 64 + ch * 8);
+  const int Npad = NPAD_C > 0 ? NPAD_C : Npad_rt;
+  const int j = tid;  // Npad <= 1024 rows: the split and |r|^2 of rows tid, tid + 256, ...
+  u32x4 sp = {0x7f7fu, 0u, 0u, 0u};
+  double mx = 0.0;
+  if (j < N) {
+    sp = *(const u32x4*)(nsplit_bh + j * 8);
+    mx = nrm_bh[j];
+  }
+  if (NPAD_C > 0) {
+    constexpr int IT = NPAD_C > 0 ? NPAD_C * 8 / 256 : 1;
+    u32x4 w[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + it * 256, row = idx >> 3, ch = idx & 7;
+      w[it] = row < N ? *(const u32x4*)(Rbh + (int64_t)row * 64 + ch * 8) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + it * 256, row = idx >> 3, ch = idx & 7;
+      u32x4 v;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const uint32_t lo = __float_as_uint(bf16_to_f32(w[e] & 0xffffu) * -2.0f) >> 16;
-        const uint32_t hi = __float_as_uint(bf16_to_f32(w[e] >> 16) * -2.0f) >> 16;
+        const uint32_t lo = __float_as_uint(bf16_to_f32(w[it][e] & 0xffffu) * -2.0f) >> 16;
+        const uint32_t hi = __float_as_uint(bf16_to_f32(w[it][e] >> 16) * -2.0f) >> 16;
         v[e] = lo | (hi << 16);
       }
+      *(u32x4*)(Rs + swz(row, ch)) = v;
     }
-    *(u32x4*)(Rs + swz(row, ch)) = v;
+  } else {
+    for (int idx = tid; idx < Npad * 8; idx += 256) {
+      const int row = idx >> 3, ch = idx & 7;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (row < N) {
+        const u32x4 w = *(const u32x4*)(Rbh + (int64_t)row * 64 + ch * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t lo = __float_as_uint(bf16_to_f32(w[e] & 0xffffu) * -2.0f) >> 16;
+          const uint32_t hi = __float_as_uint(bf16_to_f32(w[e] >> 16) * -2.0f) >> 16;
+          v[e] = lo | (hi << 16);
+        }
+      }
+      *(u32x4*)(Rs + swz(row, ch)) = v;
+    }
   }
-  double mx = 0.0;
-  for (int j = tid; j < Npad; j += 256) {
-    const u32x4 sp = j < N ? *(const u32x4*)(nsplit_bh + j * 8) : u32x4{0x7f7fu, 0u, 0u, 0u};
-    *(u32x4*)(Ns + j * 8) = sp;
-    if (j < N) mx = fmax(mx, nrm_bh[j]);
+  if (j < Npad) *(u32x4*)(Ns + j * 8) = sp;
+  for (int jj = tid + 256; jj < Npad; jj += 256) {
+    const u32x4 sp2 = jj < N ? *(const u32x4*)(nsplit_bh + jj * 8) : u32x4{0x7f7fu, 0u, 0u, 0u};
+    *(u32x4*)(Ns + jj * 8) = sp2;
+    if (jj < N) mx = fmax(mx, nrm_bh[jj]);
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
@@ -391,8 +441,9 @@ __device__ __forceinline__ double stage_reps(const uint16_t* __restrict__ Rbh, c
 }
 
 // Dynamic LDS of the assign kernels: -2R as [Npad][64] bf16 (swizzled), the
-// |r|^2 split as [Npad][8] bf16, then the moved-key records and the
-// uncertain-key queue, 4 tpw 32 entries each.
+// |r|^2 split as [Npad][8] bf16, then four arrays of 4 tpw 32 words: moved
+// records, uncertain queue, staged groups, staged |k| bounds / exact-decision
+// moved records.
 struct AssignLds {
   uint16_t* Rs;
   uint16_t* Ns;
@@ -400,32 +451,55 @@ struct AssignLds {
 };
 
 __device__ __forceinline__ AssignLds assign_lds_layout(unsigned char* smem, int Npad, int tpw, AssignCounts* c) {
+  const int cap = tpw * 32;
   AssignLds l;
   l.Rs = (uint16_t*)smem;
   l.Ns = l.Rs + Npad * 64;
   l.lists.c = c;
-  l.lists.wrec = (unsigned long long*)(l.Ns + Npad * 8);
-  l.lists.uq = l.lists.wrec + 4 * tpw * 32;
+  l.lists.cap = cap;
+  l.lists.wrec = (uint32_t*)(l.Ns + Npad * 8);
+  l.lists.uq = l.lists.wrec + 4 * cap;
+  l.lists.bst = (int32_t*)(l.lists.uq + 4 * cap);
+  l.lists.kx = (uint32_t*)(l.lists.bst + 4 * cap);
   return l;
 }
 
+// End of an assign workgroup (after each wave stored its counts): exact
+// decisions of the queued keys, then the staged groups (and first-round |k|
+// bounds) of keys key0 .. key0 + 4 tpw 32 (those below n) and the moved-key
+// records, one global atomic per workgroup.
 template <bool FIRST>
-__device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh, const uint16_t* Rs,
-                                                const double* __restrict__ nrm_bh, int n, int N,
-                                                int32_t* __restrict__ belong_bh, int32_t* __restrict__ mcount_bh,
+__device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh, int64_t key0, int tpw,
+                                                const uint16_t* Rs, const double* __restrict__ nrm_bh, int n, int N,
+                                                int32_t* __restrict__ belong_bh, float* __restrict__ knorm_bh,
+                                                int32_t* __restrict__ mcount_bh,
                                                 unsigned long long* __restrict__ mrec_bh, uint16_t* kslot_w,
                                                 const AssignLists& sh) {
   const int tid = threadIdx.x;
   __syncthreads();
-  if (sh.c->nunc) {  // uniform: read after the barrier
-    exact_decide_queue<FIRST>(Kbh, Rs, nrm_bh, N, belong_bh, kslot_w, sh);
+  const int* uc = sh.c->ucnt;
+  const int nunc = uc[0] + uc[1] + uc[2] + uc[3];
+  if (nunc) {  // uniform: read after the barrier
+    exact_decide_queue<FIRST>(Kbh, key0, Rs, nrm_bh, N, kslot_w, sh, nunc);
     __syncthreads();
   }
+  const int nk = (int)min((int64_t)4 * tpw * 32, (int64_t)n - key0);
+  for (int x = tid; x < nk; x += 256) {
+    belong_bh[key0 + x] = sh.bst[x];
+    if (FIRST) knorm_bh[key0 + x] = __uint_as_float(sh.kx[x]);
+  }
   if (!FIRST) {
-    if (tid == 0) sh.c->moved_base = sh.c->nmoved ? atomicAdd(mcount_bh, sh.c->nmoved) : 0;
+    const int* wc = sh.c->wcnt;
+    const int nw = wc[0] + wc[1] + wc[2] + wc[3];
+    const int nm = nw + sh.c->nx;
+    if (tid == 0) sh.c->moved_base = nm ? atomicAdd(mcount_bh, nm) : 0;
     __syncthreads();
-    const int nm = sh.c->nmoved, base = sh.c->moved_base;
-    for (int x = tid; x < nm; x += 256) mrec_bh[base + x] = sh.wrec[x];
+    const int base = sh.c->moved_base;
+    for (int x = tid; x < nm; x += 256) {
+      const uint32_t e = x < nw ? region_entry(sh.wrec, sh.cap, wc, x) : sh.kx[x - nw];
+      mrec_bh[base + x] = ((unsigned long long)(key0 + (e & 2047u)) << 32) | (((e >> 11) & 1023u) << 16) |
+                          (e >> 21);
+    }
   }
 }
 
@@ -442,7 +516,7 @@ __device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh
 // provably the exact fp64 argmin; otherwise the key is queued and re-decided
 // by exact_argmin_lds once the workgroup's tiles are done.  Later rounds
 // (FIRST = false) also emit the keys whose group changed as records
-// (key, old, new), one global atomic per workgroup.
+// (key, old, new).
 //
 // k_assign_bf16: grid (ceil(tiles / (4 * tpw)), BH), 256 threads, any N up to
 // 1024 (k_assign_reg covers N <= 128).  Each wave owns tpw consecutive 32-key
@@ -462,29 +536,30 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
   const int Npad = (N + 31) & ~31;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
   const int64_t bh = blockIdx.y;
-  if (tid == 0) {
-    cnt.nmoved = 0;
-    cnt.nunc = 0;
-  }
+  if (tid == 0) cnt.nx = 0;
   const AssignLds L = assign_lds_layout(smem, Npad, tpw, &cnt);
   const uint16_t* Rs = L.Rs;
   const uint16_t* Ns = L.Ns;
-  const double nmax = stage_reps(R + bh * (int64_t)N * 64, nsplit + bh * N * 8, nrm64 + bh * N, N, Npad, L.Rs, L.Ns,
-                                 red);
+  const double nmax = stage_reps<0>(R + bh * (int64_t)N * 64, nsplit + bh * N * 8, nrm64 + bh * N, N, Npad, L.Rs,
+                                    L.Ns, red);
   const float nmaxf = (float)nmax * (1.0f + 0x1p-20f);
   const float rmaxf = sqrtf(nmaxf) * (1.0f + 0x1p-20f);
   const Certify cf = {nmaxf, rmaxf, cm, cp};
 
   const int nblk = Npad >> 5;
-  const int64_t tile0 = ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(wave)) * tpw;
+  const int64_t key0 = (int64_t)blockIdx.x * 4 * tpw * 32;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int64_t tile0 = key0 / 32 + (int64_t)wv * tpw;
   const int64_t ntiles = ((int64_t)n + 31) / 32;
   const int tcount = (int)max((int64_t)0, min((int64_t)tpw, ntiles - tile0));
   const uint16_t* Kbh = K + bh * (int64_t)n * 64;
+  const float* knorm_bh = knorm + bh * n;
   int32_t* belong_bh = belong + bh * n;
   // B operand of the |r|^2 k-step: ones in the first three slots of lanes h = 0
   const u32x4 ones = h == 0 ? u32x4{0x3f803f80u, 0x3f80u, 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
   const f32x16 zero = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 
+  int wn = 0, un = 0;  // this wave's moved / uncertain entries (wave-uniform)
   u32x4 kf[2][4];
   float kn[2] = {0.f, 0.f};
   int old[2] = {0, 0};
@@ -495,7 +570,7 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
 #pragma unroll
     for (int s2 = 0; s2 < 4; ++s2) f[s2] = valid ? *(const u32x4*)(krow + s2 * 8) : u32x4{0u, 0u, 0u, 0u};
     if (!FIRST) {
-      knv = valid ? knorm[bh * n + key] : 0.f;
+      knv = valid ? knorm_bh[key] : 0.f;
       oldv = valid ? belong_bh[key] : 0;
     }
   };
@@ -513,14 +588,14 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
       fetch(tt + 3, kf_n[1], kn_n[1], old_n[1]);
     }
     bool valid[2];
-    int64_t key[2];
+    int lk[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      key[u] = (tile0 + tt + u) * 32 + q;
-      valid[u] = tt + u < tcount && key[u] < n;
+      lk[u] = (wv * tpw + tt + u) * 32 + q;
+      valid[u] = tt + u < tcount && key0 + lk[u] < n;
       if (FIRST) {
         kn[u] = key_norm_bound(kf[u]);
-        if (valid[u] && h == 0) knorm[bh * n + key[u]] = kn[u];
+        if (tt + u < tcount) L.lists.kx[lk[u]] = __float_as_uint(kn[u]);
       }
     }
 
@@ -548,7 +623,8 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u)
-      decide_tile<FIRST>(M1[u], M2[u], B1[u], kn[u], old[u], key[u], valid[u], N, cf, belong_bh, L.lists);
+      if (tt + u < tcount)
+        decide_tile<FIRST>(M1[u], M2[u], B1[u], kn[u], old[u], lk[u], valid[u], N, cf, L.lists, wv, wn, un);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
 #pragma unroll
@@ -557,7 +633,12 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
       old[u] = old_n[u];
     }
   }
-  assign_epilogue<FIRST>(Kbh, Rs, nrm64 + bh * N, n, N, belong_bh, mcount + bh, mrec + bh * n, kslot[wave], L.lists);
+  if (lane == 0) {
+    cnt.wcnt[wv] = wn;
+    cnt.ucnt[wv] = un;
+  }
+  assign_epilogue<FIRST>(Kbh, key0, tpw, Rs, nrm64 + bh * N, n, N, belong_bh, knorm + bh * n, mcount + bh,
+                         mrec + bh * n, kslot[wave], L.lists);
 }
 
 // Key fragments of tile `tile` of a slice, and in later rounds the keys' |k|
@@ -614,8 +695,8 @@ __device__ __forceinline__ void score_tile(const u32x4 (&af)[NB][4], const u32x4
 // once from LDS), so the scoring loop issues no LDS reads; only the exact
 // re-decisions read the LDS copy.  The key fragments of the next tile are
 // loaded while the current one is scored (two register sets used in turn, no
-// copies).  Same grid, LDS layout, scores, certification and outputs as
-// k_assign_bf16.
+// copies; the last tile's prefetch repeats it).  Same grid, LDS layout,
+// scores, certification and outputs as k_assign_bf16.
 template <bool FIRST, int NB>
 __global__ __launch_bounds__(256) void k_assign_reg(
     const uint16_t* __restrict__ K, const uint16_t* __restrict__ R, const uint16_t* __restrict__ nsplit,
@@ -629,13 +710,10 @@ __global__ __launch_bounds__(256) void k_assign_reg(
   constexpr int Npad = NB * 32;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
   const int64_t bh = blockIdx.y;
-  if (tid == 0) {
-    cnt.nmoved = 0;
-    cnt.nunc = 0;
-  }
+  if (tid == 0) cnt.nx = 0;
   const AssignLds L = assign_lds_layout(smem, Npad, tpw, &cnt);
-  const double nmax = stage_reps(R + bh * (int64_t)N * 64, nsplit + bh * N * 8, nrm64 + bh * N, N, Npad, L.Rs, L.Ns,
-                                 red);
+  const double nmax = stage_reps<Npad>(R + bh * (int64_t)N * 64, nsplit + bh * N * 8, nrm64 + bh * N, N, Npad, L.Rs,
+                                       L.Ns, red);
   const float nmaxf = (float)nmax * (1.0f + 0x1p-20f);
   const float rmaxf = sqrtf(nmaxf) * (1.0f + 0x1p-20f);
   const Certify cf = {nmaxf, rmaxf, cm, cp};
@@ -649,37 +727,48 @@ __global__ __launch_bounds__(256) void k_assign_reg(
   }
   const u32x4 ones = h == 0 ? u32x4{0x3f803f80u, 0x3f80u, 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
 
-  const int64_t tile0 = ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(wave)) * tpw;
+  const int64_t key0 = (int64_t)blockIdx.x * 4 * tpw * 32;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int64_t tile0 = key0 / 32 + (int64_t)wv * tpw;
   const int64_t ntiles = ((int64_t)n + 31) / 32;
   const int tcount = (int)max((int64_t)0, min((int64_t)tpw, ntiles - tile0));
   const uint16_t* Kbh = K + bh * (int64_t)n * 64;
-  float* knorm_bh = knorm + bh * n;
-  int32_t* belong_bh = belong + bh * n;
+  const float* knorm_bh = knorm + bh * n;
+  const int32_t* belong_bh = belong + bh * n;
 
+  int wn = 0, un = 0;  // this wave's moved / uncertain entries (wave-uniform)
   u32x4 kA[4], kB[4];
   float knA = 0.f, knB = 0.f;
   int oldA = 0, oldB = 0;
   auto run = [&](const u32x4 (&kf)[4], float knv, int oldv, int t) __attribute__((always_inline)) {
-    const int64_t key = (tile0 + t) * 32 + q;
-    const bool valid = key < n;
+    const int lk = (wv * tpw + t) * 32 + q;
+    const bool valid = key0 + lk < n;
     if (FIRST) {
       knv = key_norm_bound(kf);
-      if (valid && h == 0) knorm_bh[key] = knv;
+      L.lists.kx[lk] = __float_as_uint(knv);
     }
     float M1, M2;
     int B1;
     score_tile<NB>(af, an, ones, kf, M1, M2, B1);
-    decide_tile<FIRST>(M1, M2, B1, knv, oldv, key, valid, N, cf, belong_bh, L.lists);
+    decide_tile<FIRST>(M1, M2, B1, knv, oldv, lk, valid, N, cf, L.lists, wv, wn, un);
   };
   if (tcount > 0) load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0, n, q, h, kA, knA, oldA);
+  // the scheduling barriers keep each prefetch ahead of the tile it overlaps
   for (int t = 0; t < tcount; t += 2) {
-    if (t + 1 < tcount) load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + t + 1, n, q, h, kB, knB, oldB);
+    load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(t + 1, tcount - 1), n, q, h, kB, knB, oldB);
+    __builtin_amdgcn_sched_barrier(0);
     run(kA, knA, oldA, t);
     if (t + 1 >= tcount) break;
-    if (t + 2 < tcount) load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + t + 2, n, q, h, kA, knA, oldA);
+    load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(t + 2, tcount - 1), n, q, h, kA, knA, oldA);
+    __builtin_amdgcn_sched_barrier(0);
     run(kB, knB, oldB, t + 1);
   }
-  assign_epilogue<FIRST>(Kbh, L.Rs, nrm64 + bh * N, n, N, belong_bh, mcount + bh, mrec + bh * n, kslot[wave], L.lists);
+  if (lane == 0) {
+    cnt.wcnt[wv] = wn;
+    cnt.ucnt[wv] = un;
+  }
+  assign_epilogue<FIRST>(Kbh, key0, tpw, L.Rs, nrm64 + bh * N, n, N, belong + bh * n, knorm + bh * n, mcount + bh,
+                         mrec + bh * n, kslot[wave], L.lists);
 }
 
 // ------------------------------------------------------------------ assign (exact)
@@ -828,207 +917,286 @@ __global__ __launch_bounds__(256) void k_segsum(const typename S::T* __restrict_
   }
 }
 
-// ------------------------------------------------------------------ order-free bucketing (bf16)
-// With bf16 keys and values every fp64 member sum is exact (8-bit mantissas,
-// at most 2^30 members, magnitudes within 2^30 of each other), so the order of
-// summation cannot change a bit and the bf16 path groups keys without a stable
-// order: slots inside a group come from LDS atomic cursors.
+// ------------------------------------------------------------------ exact sums (bf16)
+// With bf16 keys and values every fp64 member sum is exact: a member is a
+// multiple of 2^(e_min - 7) (8-bit significand, e_min the smallest member
+// exponent) and every partial sum, in any order, is below 2^(e_max + 1 +
+// log2 count), so all of them are representable in fp64's 53 bits whenever
+// (e_max - e_min) + log2 count <= 45, e.g. at most 2^15 members with nonzero
+// magnitudes within 2^30 of each other.  The order of summation then cannot
+// change a bit, and the bf16 path sums without a stable order.
 
-// Exclusive scan of x over threads 0..N-1 of a 1024-thread block (N <= 1024).
-__device__ int block_excl_scan(int x, int* wsum) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int incl = wave_incl_scan(x);
-  if (lane == 63) wsum[wave] = incl;
-  __syncthreads();
-  if (wave == 0) {
-    const int t = lane < 16 ? wsum[lane] : 0;
-    const int ti = wave_incl_scan(t);
-    if (lane < 16) wsum[lane] = ti - t;
-  }
-  __syncthreads();
-  const int r = incl - x + wsum[wave];
-  __syncthreads();
-  return r;
-}
+// ------------------------------------------------------------------ group sums (bf16)
+// The member sums of the bf16 path are exact in fp64 (see above), so they can
+// be accumulated in any order and split any way: no global bucketing.
+//
+// k_gsum: grid (ceil(N / 32), BH), 256 threads.  Workgroup x owns groups
+// g0 = 32 x .. g0 + 31 of slice bh and finishes them itself:
+//   MODE 0 (first round): S = sum of the member key rows, count = members
+//   MODE 1 (later rounds): S += joins - leaves from the round's moved-key
+//           records, count += joins - leaves (groups without either are left
+//           alone)
+//   MODE 2 (value sums):  vsum = (float) sum of the member value rows
+// MODE 0/1 then set C = (float)(S / count) (an empty group keeps C), R =
+// bf16(C), the canonical fp64 |r|^2 (fma chain over c = 0..63, one lane per
+// group) and its split.
+//
+// Per chunk of keys (or records), all loaded at once:
+// 1. count the entries (key, sign) of every owned group, lay the groups out
+//    in LDS padded to multiples of 8 entries, scatter the entries (a local
+//    counting sort; one LDS atomic per entry);
+// 2. each wave takes a run of whole groups and sums 8 rows per instruction
+//    (row slot = lane / 8, 16 bytes = features 8 (lane % 8) .. +7 per lane)
+//    into 8 fp64 registers per lane; the next 8 chunks of 8 rows are loaded
+//    while the current 8 are added; at the end of a group the 8 slots are
+//    combined with cross-lane VALU moves and added into the LDS accumulator;
+// 3. finish the owned groups.
+constexpr int kGsumG = 32;
+constexpr int kGsumList = 8448;  // entry capacity of the sorted chunk list
+constexpr int kGsumU = 8;        // 8-row chunks per batch
 
-// Every key of a slice by group: grid BH, 1024 threads, LDS counts + cursors.
-// grp[g] = {first slot, members, 0, 0}; count[g] = members (if count != NULL).
-__global__ __launch_bounds__(1024) void k_full_bucket(const int32_t* __restrict__ belong, int n, int N,
-                                                      int32_t* __restrict__ list, int4* __restrict__ grp,
-                                                      int32_t* __restrict__ count) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ int wsum[16];
-  int32_t* cnt = (int32_t*)smem;
-  int32_t* cur = cnt + N;
-  const int tid = threadIdx.x;
-  const int64_t bh = blockIdx.x;
-  const int32_t* a = belong + bh * n;
-  for (int g = tid; g < N; g += 1024) cnt[g] = 0;
-  __syncthreads();
-  for (int i = tid; i < n; i += 1024) {
-    const int g = a[i];
-    if ((unsigned)g < (unsigned)N) atomicAdd(&cnt[g], 1);
-  }
-  __syncthreads();
-  const int v = tid < N ? cnt[tid] : 0;
-  const int ex = block_excl_scan(v, wsum);
-  if (tid < N) {
-    cur[tid] = ex;
-    grp[bh * N + tid] = int4{ex, v, 0, 0};
-    if (count) count[bh * N + tid] = v;
-  }
-  __syncthreads();
-  for (int i = tid; i < n; i += 1024) {
-    const int g = a[i];
-    if ((unsigned)g < (unsigned)N) list[bh * n + atomicAdd(&cur[g], 1)] = i;
-  }
-}
-
-// Moved-key records of one round by group: joins (new group) and leaves (old
-// group).  grid BH, 1024 threads.  count[g] += joins - leaves; grp[g] =
-// {first join, joins, first leave, leaves}; the record counter is reset.
-__global__ __launch_bounds__(1024) void k_moved_bucket(const unsigned long long* __restrict__ mrec,
-                                                       int32_t* __restrict__ mcount, int n, int N,
-                                                       int32_t* __restrict__ jlist, int32_t* __restrict__ llist,
-                                                       int4* __restrict__ grp, int32_t* __restrict__ count) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ int wsum[16];
-  int32_t* jc = (int32_t*)smem;
-  int32_t* lc = jc + N;
-  int32_t* jcur = lc + N;
-  int32_t* lcur = jcur + N;
-  const int tid = threadIdx.x;
-  const int64_t bh = blockIdx.x;
-  const int m = mcount[bh];
-  const unsigned long long* rec = mrec + bh * n;
-  for (int g = tid; g < N; g += 1024) {
-    jc[g] = 0;
-    lc[g] = 0;
-  }
-  __syncthreads();
-  for (int r = tid; r < m; r += 1024) {
-    const unsigned long long x = rec[r];
-    atomicAdd(&jc[(int)(x & 0xffffu)], 1);
-    atomicAdd(&lc[(int)((x >> 16) & 0xffffu)], 1);
-  }
-  __syncthreads();
-  const int vj = tid < N ? jc[tid] : 0;
-  const int vl = tid < N ? lc[tid] : 0;
-  const int ej = block_excl_scan(vj, wsum);
-  const int el = block_excl_scan(vl, wsum);
-  if (tid < N) {
-    jcur[tid] = ej;
-    lcur[tid] = el;
-    grp[bh * N + tid] = int4{ej, vj, el, vl};
-    if (vj != vl) count[bh * N + tid] += vj - vl;
-  }
-  __syncthreads();
-  for (int r = tid; r < m; r += 1024) {
-    const unsigned long long x = rec[r];
-    const int key = (int)(x >> 32);
-    jlist[bh * n + atomicAdd(&jcur[(int)(x & 0xffffu)], 1)] = key;
-    llist[bh * n + atomicAdd(&lcur[(int)((x >> 16) & 0xffffu)], 1)] = key;
-  }
-  __syncthreads();
-  if (tid == 0) mcount[bh] = 0;
-}
-
-// Sum of listed bf16 rows into a per-lane accumulator of 4 features: lane l
-// reads features 4 (l%16) .. +3 of row list[x + l/16], 4 rows per instruction
-// and 16 rows per iteration in flight.
-__device__ __forceinline__ void add_rows(const uint16_t* __restrict__ Xb, const int32_t* __restrict__ L, int cnt,
-                                         int sub, double sign, double acc[4]) {
-  for (int x = 0; x < cnt; x += 16) {
-    u32x2 w[4];
-    bool ok[4];
+// One batch of a wave's run: entries of chunks ch0 .. ch0 + kGsumU - 1 (clamped
+// to the run's last chunk, so every lane loads) and their row fragments.
+__device__ __forceinline__ void gsum_load(const uint32_t* ent, const uint16_t* __restrict__ Xb, int ch0, int ce,
+                                          int slot, int j, uint32_t (&e)[kGsumU], u32x4 (&w)[kGsumU]) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int idx = x + 4 * u + sub;
-      ok[u] = idx < cnt;
-      const int key = L[ok[u] ? idx : 0];
-      w[u] = *(const u32x2*)(Xb + (int64_t)key * 64);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (!ok[u]) continue;
-      acc[0] = fma(sign, (double)bf16_to_f32(w[u][0] & 0xffffu), acc[0]);
-      acc[1] = fma(sign, (double)bf16_to_f32(w[u][0] >> 16), acc[1]);
-      acc[2] = fma(sign, (double)bf16_to_f32(w[u][1] & 0xffffu), acc[2]);
-      acc[3] = fma(sign, (double)bf16_to_f32(w[u][1] >> 16), acc[3]);
-    }
+  for (int u = 0; u < kGsumU; ++u) {
+    e[u] = ent[min(ch0 + u, ce - 1) * 8 + slot];
+    const uint32_t key = e[u] == 0xffffffffu ? 0u : (e[u] & 0x7fffffffu);
+    w[u] = *(const u32x4*)(Xb + (int64_t)key * 64 + 8 * j);
   }
 }
 
-// grid (ceil(N/4), BH), 256 threads: one wave per group.
-//   MODE 0: first round: S = sum of the joins (all members)
-//   MODE 1: later rounds: S += joins - leaves (groups without either are skipped)
-//   MODE 2: value sums: vsum = (float) sum of the joins
-// MODE 0/1 then set C = (float)(S / count) (an empty group keeps C), R = bf16(C)
-// and the canonical fp64 |r|^2.
+// x summed over the 8 lanes l ^ {0, 8, 16, ..., 56} (lane bits 3, 4, 5), in
+// every lane: DPP row rotation by 8 (lane ^ 8 within 16-lane rows), then the
+// 16- and 32-lane half swaps.
+__device__ __forceinline__ double sum_slots8(double x) {
+  const uint32_t lo = (uint32_t)__double2loint(x), hi = (uint32_t)__double2hiint(x);
+  x += __hiloint2double((int)__builtin_amdgcn_update_dpp(0u, hi, 0x128, 0xf, 0xf, false),
+                        (int)__builtin_amdgcn_update_dpp(0u, lo, 0x128, 0xf, 0xf, false));
+  {
+    const auto l16 = __builtin_amdgcn_permlane16_swap((uint32_t)__double2loint(x), (uint32_t)__double2loint(x), false,
+                                                      false);
+    const auto h16 = __builtin_amdgcn_permlane16_swap((uint32_t)__double2hiint(x), (uint32_t)__double2hiint(x), false,
+                                                      false);
+    x = __hiloint2double((int)h16[0], (int)l16[0]) + __hiloint2double((int)h16[1], (int)l16[1]);
+  }
+  const u32x2 l32 = halves((uint32_t)__double2loint(x)), h32 = halves((uint32_t)__double2hiint(x));
+  return __hiloint2double((int)h32[0], (int)l32[0]) + __hiloint2double((int)h32[1], (int)l32[1]);
+}
+
 template <int MODE>
-__global__ __launch_bounds__(256) void k_segsum_bf16(const uint16_t* __restrict__ X, const int32_t* __restrict__ jlist,
-                                                     const int32_t* __restrict__ llist, const int4* __restrict__ grp,
-                                                     const int32_t* __restrict__ count, int n, int N,
-                                                     double* __restrict__ S64, float* __restrict__ out,
-                                                     uint16_t* __restrict__ R, double* __restrict__ nrm64,
-                                                     uint16_t* __restrict__ nsplit) {
-  const int lane = threadIdx.x & 63, sub = lane >> 4, c4 = lane & 15;
-  const int g = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+__global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, const int32_t* __restrict__ belong,
+                                              const unsigned long long* __restrict__ mrec,
+                                              const int32_t* __restrict__ mcount_cur,
+                                              int32_t* __restrict__ mcount_next, int n, int N,
+                                              double* __restrict__ S64, int32_t* __restrict__ count,
+                                              float* __restrict__ out, uint16_t* __restrict__ R,
+                                              double* __restrict__ nrm64, uint16_t* __restrict__ nsplit) {
+  __shared__ uint32_t ent[kGsumList];  // key | leave << 31; 0xffffffff pads a group to 8k entries
+  __shared__ double acc[kGsumG * 64];  // [g][c] sums of this workgroup's groups
+  __shared__ int ecnt[kGsumG], eoff[kGsumG + 1], ecur[kGsumG], dcnt[kGsumG], hit[kGsumG], wbeg[5], wg0[4];
+  float* rsh = (float*)ent;            // [32][65] bf16 representatives, after the sums
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bh = blockIdx.y;
-  if (g >= N) return;
-  const int64_t row = bh * N + g;
-  const int4 gd = grp[row];
-  if (MODE == 1 && gd.y == 0 && gd.w == 0) return;
-  double acc[4] = {0.0, 0.0, 0.0, 0.0};
-  if (MODE == 1 && sub == 0) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) acc[e] = S64[row * 64 + 4 * c4 + e];
+  const int g0 = blockIdx.x * kGsumG, ng = min(kGsumG, N - g0);
+  for (int i = tid; i < kGsumG * 64; i += 256) acc[i] = 0.0;
+  if (tid < kGsumG) {
+    dcnt[tid] = 0;
+    hit[tid] = 0;
   }
-  const uint16_t* Xb = X + bh * (int64_t)n * 64 + 4 * c4;
-  add_rows(Xb, jlist + bh * n + gd.x, gd.y, sub, 1.0, acc);
-  if (MODE == 1) add_rows(Xb, llist + bh * n + gd.z, gd.w, sub, -1.0, acc);
+
+  const int64_t total = MODE == 1 ? (int64_t)mcount_cur[bh] : (int64_t)n;
+  // entries per chunk: at most 2 per record (join, leave) plus 7 padding per group
+  constexpr int CH = MODE == 1 ? 4096 : 8192;
+  constexpr int PER = CH / 256;
+  static_assert((MODE == 1 ? 2 : 1) * CH + 7 * kGsumG <= kGsumList, "chunk list overflow");
+  const uint16_t* Xb = X + bh * (int64_t)n * 64;
+  for (int64_t c0 = 0; c0 < total; c0 += CH) {
+    int kv[PER], gj[PER], gl[PER];
+    // every lane loads (index clamped into the chunk) so that the loads overlap
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    acc[e] += __shfl_xor(acc[e], 16);
-    acc[e] += __shfl_xor(acc[e], 32);
-  }
-  if (MODE == 2) {
-    if (sub == 0) {
-      float4 o = {(float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]};
-      *(float4*)(out + row * 64 + 4 * c4) = o;
+    for (int u = 0; u < PER; ++u) {
+      const int64_t e = c0 + tid + 256 * u, ec = min(e, total - 1);
+      if (MODE == 1) {
+        const unsigned long long r = mrec[bh * n + ec];
+        kv[u] = (int)(r >> 32);
+        gj[u] = (int)(r & 0xffffu) - g0;
+        gl[u] = (int)((r >> 16) & 0xffffu) - g0;
+      } else {
+        kv[u] = (int)e;
+        gj[u] = belong[bh * n + ec] - g0;
+        gl[u] = -1;
+      }
     }
-    return;
-  }
-  const int cnt = MODE == 0 ? gd.y : count[row];
-  float c[4];
-  if (cnt > 0) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) c[e] = (float)(acc[e] / (double)cnt);
-  } else {
-    const float4 o = *(const float4*)(out + row * 64 + 4 * c4);
-    c[0] = o.x, c[1] = o.y, c[2] = o.z, c[3] = o.w;
-  }
-  float r[4];
+    for (int u = 0; u < PER; ++u)
+      if (c0 + tid + 256 * u >= total) {
+        gj[u] = -1;
+        gl[u] = -1;
+      }
+    if (tid < kGsumG) ecnt[tid] = 0;
+    __syncthreads();
+    // 1. count, lay out, scatter
 #pragma unroll
-  for (int e = 0; e < 4; ++e) r[e] = BF16::rep(c[e]);
-  if (sub == 0) {
+    for (int u = 0; u < PER; ++u)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) S64[row * 64 + 4 * c4 + e] = acc[e];
-    if (cnt > 0) *(float4*)(out + row * 64 + 4 * c4) = float4{c[0], c[1], c[2], c[3]};
-    const u32x2 rb = {(__float_as_uint(r[0]) >> 16) | (__float_as_uint(r[1]) & 0xffff0000u),
-                      (__float_as_uint(r[2]) >> 16) | (__float_as_uint(r[3]) & 0xffff0000u)};
-    *(u32x2*)(R + row * 64 + 4 * c4) = rb;
-  }
-  double nrm = 0.0;
+      for (int side = 0; side < (MODE == 1 ? 2 : 1); ++side) {
+        const int g = side ? gl[u] : gj[u];
+        if ((unsigned)g < (unsigned)ng) {
+          atomicAdd(&ecnt[g], 1);
+          if (MODE != 2) atomicAdd(&dcnt[g], side ? -1 : 1);
+          hit[g] = 1;
+        }
+      }
+    __syncthreads();
+    if (wave == 0) {
+      const int c = lane < kGsumG ? ecnt[lane] : 0;
+      const int pc = (c + 7) & ~7;
+      int incl = pc;  // inclusive scan over the 32 groups
 #pragma unroll
-  for (int cc = 0; cc < 64; ++cc) {
-    const double rc = (double)readlane_f(r[cc & 3], cc >> 2);
-    nrm = fma(rc, rc, nrm);
+      for (int off = 1; off < 32; off <<= 1) {
+        const int y = __shfl_up(incl, off);
+        if (lane >= off) incl += y;
+      }
+      const int start = incl - pc, tot = __shfl(incl, kGsumG - 1);
+      if (lane < kGsumG) {
+        eoff[lane] = start;
+        ecur[lane] = start;
+        for (int k = c; k < pc; ++k) ent[start + k] = 0xffffffffu;
+      }
+      if (lane == 0) {
+        eoff[kGsumG] = tot;
+        wbeg[0] = 0;
+        wbeg[4] = tot;
+        wg0[0] = 0;
+      }
+      // wave w starts at the first group beginning at or after w tot / 4
+#pragma unroll
+      for (int w = 1; w < 4; ++w) {
+        const uint64_t m = __ballot(lane < kGsumG && start >= w * tot / 4);
+        const int g = m ? __ffsll((unsigned long long)m) - 1 : kGsumG;
+        const int gs = __shfl(start, g < kGsumG ? g : 0);  // all lanes take part
+        if (lane == 0) {
+          wbeg[w] = g < kGsumG ? gs : tot;
+          wg0[w] = g;
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+#pragma unroll
+      for (int side = 0; side < (MODE == 1 ? 2 : 1); ++side) {
+        const int g = side ? gl[u] : gj[u];
+        if ((unsigned)g < (unsigned)ng) ent[atomicAdd(&ecur[g], 1)] = (uint32_t)kv[u] | ((uint32_t)side << 31);
+      }
+    __syncthreads();
+    // 2. per-wave register sums over runs of whole groups
+    {
+      const int slot = lane >> 3, j = lane & 7;
+      const int cb = wbeg[wave] / 8, ce = wbeg[wave + 1] / 8;
+      double a[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+      int g = wg0[wave], gend = 0;  // current group and its end chunk
+      auto flush = [&]() {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) a[k] = sum_slots8(a[k]);
+        if (slot == 0) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) atomicAdd(&acc[g * 64 + 8 * j + k], a[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) a[k] = 0.0;
+      };
+      auto add = [&](int ch0, const uint32_t (&e)[kGsumU], const u32x4 (&w)[kGsumU]) {
+#pragma unroll
+        for (int u = 0; u < kGsumU; ++u) {
+          const int ch = ch0 + u;
+          if (ch >= ce) break;
+          if (ch >= gend) {  // next non-empty group (uniform)
+            if (ch > cb) flush();
+            while (eoff[g + 1] <= ch * 8) ++g;
+            gend = eoff[g + 1] / 8;
+          }
+          const double sg = e[u] == 0xffffffffu ? 0.0 : ((e[u] >> 31) ? -1.0 : 1.0);
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            const uint32_t bits = (k & 1) ? (w[u][k >> 1] >> 16) : (w[u][k >> 1] & 0xffffu);
+            a[k] = fma(sg, (double)bf16_to_f32(bits), a[k]);
+          }
+        }
+      };
+      if (cb < ce) {
+        uint32_t eA[kGsumU], eB[kGsumU];
+        u32x4 wA[kGsumU], wB[kGsumU];
+        gsum_load(ent, Xb, cb, ce, slot, j, eA, wA);
+        for (int ch0 = cb; ch0 < ce; ch0 += 2 * kGsumU) {
+          gsum_load(ent, Xb, ch0 + kGsumU, ce, slot, j, eB, wB);
+          __builtin_amdgcn_sched_barrier(0);
+          add(ch0, eA, wA);
+          if (ch0 + kGsumU >= ce) break;
+          gsum_load(ent, Xb, ch0 + 2 * kGsumU, ce, slot, j, eA, wA);
+          __builtin_amdgcn_sched_barrier(0);
+          add(ch0 + kGsumU, eB, wB);
+        }
+        flush();
+      }
+    }
+    __syncthreads();
   }
-  if (lane == 0) {
+
+  // 3. finish the owned groups: element (g, c) = (idx / 64, idx % 64), 8 per thread
+  constexpr int EPT = kGsumG * 64 / 256;
+  double prev[EPT];
+  int pc[EPT];
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int idx = tid + 256 * u, g = idx >> 6, c = idx & 63;
+    const int64_t row = bh * N + g0 + min(g, ng - 1);
+    prev[u] = MODE == 1 ? S64[row * 64 + c] : 0.0;
+    pc[u] = MODE == 1 ? count[row] : 0;
+  }
+  __syncthreads();  // (total == 0: dcnt, hit, acc initialised above)
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int idx = tid + 256 * u, g = idx >> 6, c = idx & 63;
+    if (g >= ng) continue;
+    const int64_t row = bh * N + g0 + g;
+    const double s = acc[g * 64 + c];
+    if (MODE == 2) {
+      out[row * 64 + c] = (float)s;
+      continue;
+    }
+    if (MODE == 1 && !hit[g]) continue;
+    const double S = prev[u] + s;
+    const int cnt = pc[u] + dcnt[g];
+    S64[row * 64 + c] = S;
+    if (c == 0) count[row] = cnt;
+    float cf;
+    if (cnt > 0) {
+      cf = (float)(S / (double)cnt);
+      out[row * 64 + c] = cf;
+    } else {
+      cf = out[row * 64 + c];
+    }
+    const float r = BF16::rep(cf);
+    BF16::store(R, row * 64 + c, r);
+    rsh[g * 65 + c] = r;
+  }
+  if (MODE == 2) return;
+  __syncthreads();
+  if (tid < ng && (MODE == 0 || hit[tid])) {
+    const int64_t row = bh * N + g0 + tid;
+    double nrm = 0.0;
+#pragma unroll 8
+    for (int c = 0; c < 64; ++c) {
+      const double rc = (double)rsh[tid * 65 + c];
+      nrm = fma(rc, rc, nrm);
+    }
     nrm64[row] = nrm;
     write_nsplit(nrm, nsplit + row * 8);
   }
+  if (MODE == 1 && blockIdx.x == 0 && tid == 0) mcount_next[bh] = 0;
 }
 
 // ------------------------------------------------------------------ attention (bf16)
@@ -1271,7 +1439,7 @@ constexpr size_t kAssignLdsMax = 160 * 1024 - 1024;  // dynamic LDS budget (stat
 
 size_t assign_lds(int N, int tpw = 12) {
   const int Npad = (N + 31) & ~31;
-  return (size_t)Npad * 128 + (size_t)Npad * 16 + (size_t)4 * tpw * 32 * 16;
+  return (size_t)Npad * 128 + (size_t)Npad * 16 + (size_t)4 * tpw * 32 * 16;  // see assign_lds_layout
 }
 size_t bucket_lds(int N) { return (size_t)16 * N * 8 + (size_t)2 * N * 4; }
 size_t attend_lds(int N) {
@@ -1334,10 +1502,8 @@ size_t workspace_layout(const Dims& d, Workspace* ws, void* base) {
   w.Vt = (uint16_t*)take(BH * 64 * (int64_t)vt_stride((int)N) * 2);
   w.ginit = (float*)take(BH * Npad * 4);
   w.S64 = (double*)take(BH * N * 64 * 8);
-  w.mcount = (int32_t*)take(BH * 4);
+  w.mcount = (int32_t*)take(2 * BH * 4);
   w.mrec = (unsigned long long*)take(BH * n * 8);
-  w.grp = (int4*)take(BH * N * 16);
-  w.llist = (int32_t*)take(BH * n * 4);
   if (ws) *ws = w;
   return off;
 }
@@ -1409,37 +1575,24 @@ hipError_t launch_bucket(const Dims& d, const int32_t* belong, int32_t* perm, in
   return hipGetLastError();
 }
 
-hipError_t launch_full_bucket(const Dims& d, const int32_t* belong, int32_t* list, int4* grp, int32_t* count,
-                             hipStream_t st) {
-  TimedLaunch timed("bucket", st);
-  hipLaunchKernelGGL(k_full_bucket, dim3((unsigned)d.BH), dim3(1024), (size_t)2 * d.N * 4, st, belong, d.n, d.N,
-                     list, grp, count);
-  return hipGetLastError();
-}
-
-hipError_t launch_moved_bucket(const Dims& d, const unsigned long long* mrec, int32_t* mcount, int32_t* jlist,
-                               int32_t* llist, int4* grp, int32_t* count, hipStream_t st) {
-  TimedLaunch timed("moved_bucket", st);
-  hipLaunchKernelGGL(k_moved_bucket, dim3((unsigned)d.BH), dim3(1024), (size_t)4 * d.N * 4, st, mrec, mcount, d.n,
-                     d.N, jlist, llist, grp, count);
-  return hipGetLastError();
-}
-
-hipError_t launch_segsum_bf16(const Dims& d, int mode, const void* X, const int32_t* jlist, const int32_t* llist,
-                              const int4* grp, const int32_t* count, double* S64, float* out, void* R,
-                              double* nrm64, uint16_t* nsplit, hipStream_t st) {
-  TimedLaunch timed(mode == 2 ? "valuesum" : "update", st);
-  const dim3 grid(cdiv(d.N, 4), (unsigned)d.BH), block(256);
+hipError_t launch_gsum(const Dims& d, int mode, const void* X, const int32_t* belong,
+                       const unsigned long long* mrec, const int32_t* mcount_cur, int32_t* mcount_next,
+                       double* S64, int32_t* count, float* out, void* R, double* nrm64, uint16_t* nsplit,
+                       hipStream_t st) {
+  TimedLaunch timed(mode == 0 ? "sums_full" : mode == 1 ? "sums_delta" : "valuesum", st);
+  const dim3 grid(cdiv(d.N, kGsumG), (unsigned)d.BH), block(256);
+  const size_t lds = 0;
   const uint16_t* Xb = (const uint16_t*)X;
+  uint16_t* Rb = (uint16_t*)R;
   if (mode == 0)
-    hipLaunchKernelGGL(k_segsum_bf16<0>, grid, block, 0, st, Xb, jlist, llist, grp, count, d.n, d.N, S64, out,
-                       (uint16_t*)R, nrm64, nsplit);
+    hipLaunchKernelGGL(k_gsum<0>, grid, block, lds, st, Xb, belong, mrec, mcount_cur, mcount_next, d.n, d.N, S64,
+                       count, out, Rb, nrm64, nsplit);
   else if (mode == 1)
-    hipLaunchKernelGGL(k_segsum_bf16<1>, grid, block, 0, st, Xb, jlist, llist, grp, count, d.n, d.N, S64, out,
-                       (uint16_t*)R, nrm64, nsplit);
+    hipLaunchKernelGGL(k_gsum<1>, grid, block, lds, st, Xb, belong, mrec, mcount_cur, mcount_next, d.n, d.N, S64,
+                       count, out, Rb, nrm64, nsplit);
   else
-    hipLaunchKernelGGL(k_segsum_bf16<2>, grid, block, 0, st, Xb, jlist, llist, grp, count, d.n, d.N, S64, out,
-                       (uint16_t*)R, nrm64, nsplit);
+    hipLaunchKernelGGL(k_gsum<2>, grid, block, lds, st, Xb, belong, mrec, mcount_cur, mcount_next, d.n, d.N, S64,
+                       count, out, Rb, nrm64, nsplit);
   return hipGetLastError();
 }
 
