@@ -23,25 +23,28 @@ METRIC = "group-attention queries/sec (B·H·n) at n=8000,N=128; % HBM roofline"
 
 
 def kernel_work(name, w, N, BH):
-    """(bound, algorithmic work per launch, unit, peak) of each kernel.
+    """(bound, algorithmic work per launch, unit, peak) of each kernel, or None.
 
-    assign:  the n x N x d score contraction, 2 n N d flop per slice.
-    attend:  Q read + O write, 2 n d storage elements per slice (HBM-bound:
-             4 N d = 32768 flop per 256 B query is below the MFMA ridge).
-    update / valuesum: one read of K (or V), n d elements per slice.
-    bucket:  belong read twice + perm write, 12 B per key.
+    assign:    per key its row of K, |k| bound and previous group (read) and
+               its group (written): d*es + 12 bytes (the first round writes the
+               bound instead of reading bound and group: d*es + 8).  Its
+               arithmetic intensity, 2 N d flop per d*es + 12 bytes (~117
+               flop/B at N = 128), is below MI355X's ridge (2.5 PF / 8 TB/s =
+               312 flop/B), so the roofline that bounds it is HBM.
+    attend:    Q read + O write, 2 n d storage elements per slice (4 N d flop
+               per query is below the ridge too).
+    sums_full, valuesum: one pass over K (or V) and the groups, n (d*es + 4).
     """
     es = 2 if w.dtype == "bf16" else 4
     n, d = w.n, w.d
     if name == "assign":
-        return "mfma", 2.0 * n * N * d * BH / 1e12, "TFLOP/s", MFMA_BF16_PEAK_TFS
+        per_key = (d * es + 8 + 9 * (d * es + 12)) / 10.0  # mean over the first and the later rounds
+        return "hbm", per_key * n * BH / 1e9, "GB/s", HBM_PEAK_GBS
     if name == "attend":
         return "hbm", 2.0 * n * d * es * BH / 1e9, "GB/s", HBM_PEAK_GBS
-    if name in ("update", "valuesum"):
-        return "hbm", 1.0 * n * d * es * BH / 1e9, "GB/s", HBM_PEAK_GBS
-    if name == "bucket":
-        return "hbm", 12.0 * n * BH / 1e9, "GB/s", HBM_PEAK_GBS
-    return "hbm", 1.0 * N * d * 4 * BH / 1e9, "GB/s", HBM_PEAK_GBS
+    if name in ("sums_full", "valuesum", "update"):
+        return "hbm", 1.0 * n * (d * es + 4) * BH / 1e9, "GB/s", HBM_PEAK_GBS
+    return None
 
 
 def traffic_for(kernel, workload):
@@ -68,6 +71,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-slices", type=int, default=16, help="(b,h) slices the oracle times")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run an elementwise copy of this many MiB (a known-size kernel for HBM counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -129,17 +134,30 @@ def main():
 
     kernels = {}
     for name, (launches, tot) in per_kernel.items():
-        bound, work, unit, peak = kernel_work(name, w, N, BH)
         avg = tot / launches
-        ach = work / (avg / 1e3)
-        kernels[name] = dict(launches_per_step=launches / args.steps, avg_ms=avg, bound=bound,
-                             achieved=ach, unit=unit, frac=ach / peak)
-    dom = max(per_kernel, key=lambda k: per_kernel[k][1])
+        kernels[name] = dict(launches_per_step=launches / args.steps, avg_ms=avg)
+        kw = kernel_work(name, w, N, BH)
+        if kw:
+            bound, work, unit, peak = kw
+            ach = work / (avg / 1e3)
+            kernels[name].update(bound=bound, achieved=ach, unit=unit, frac=ach / peak)
+    # the dominant kernel: most time per step among those with a defined roofline
+    dom = max((k for k in per_kernel if "frac" in kernels[k]), key=lambda k: per_kernel[k][1])
     kd = kernels[dom]
     _, work, _, peak = kernel_work(dom, w, N, BH)
     roofline = dict(kernel=dom, bound=kd["bound"], achieved=round(kd["achieved"], 3), peak=peak, unit=kd["unit"],
                     frac=round(kd["frac"], 4), traffic=traffic_for(dom, w.name),
                     avg_launch_ms=round(kd["avg_ms"], 5))
+
+    if args.copy_calibration_mib:
+        # int32 x + 0: one elementwise kernel that reads and writes exactly this many bytes
+        nel = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.arange(nel, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.add(src, 0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     # parity spot-check and CPU baseline on a bounded sample of slices (oracle)
     cpu = None

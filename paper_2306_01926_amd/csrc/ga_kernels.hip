@@ -27,7 +27,9 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <map>
 #include <mutex>
+#include <tuple>
 
 #include "ga_internal.h"
 
@@ -42,7 +44,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRs = 72;       // LDS row stride (bf16 elements) of the 32x16 MFMA A tiles
-constexpr int kAttTpw = 4;    // 32-query tiles per wave in the bf16 attention kernel
+constexpr int kAssignDepth = 1;  // key tiles loaded ahead per wave in k_assign_reg
 constexpr int kAttMaxN = 256; // groups held in LDS by the bf16 attention kernel
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
@@ -642,13 +644,14 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
 }
 
 // Key fragments of tile `tile` of a slice, and in later rounds the keys' |k|
-// bound and previous group.  Keys past n read the slice's last key instead
-// (their results are never stored), so every lane loads unconditionally.
+// bound and previous group.  Keys outside 0 .. n - 1 read the nearest key
+// instead (their results are never stored), so every lane loads
+// unconditionally.
 template <bool FIRST>
 __device__ __forceinline__ void load_keys(const uint16_t* __restrict__ Kbh, const float* __restrict__ knorm_bh,
                                           const int32_t* __restrict__ belong_bh, int64_t tile, int n, int q, int h,
                                           u32x4 (&f)[4], float& knv, int& oldv) {
-  const int64_t key = min(tile * 32 + q, (int64_t)n - 1);
+  const int64_t key = max((int64_t)0, min(tile * 32 + q, (int64_t)n - 1));
   const uint16_t* krow = Kbh + key * 64 + h * 32;
 #pragma unroll
   for (int s2 = 0; s2 < 4; ++s2) f[s2] = *(const u32x4*)(krow + s2 * 8);
@@ -737,9 +740,6 @@ __global__ __launch_bounds__(256) void k_assign_reg(
   const int32_t* belong_bh = belong + bh * n;
 
   int wn = 0, un = 0;  // this wave's moved / uncertain entries (wave-uniform)
-  u32x4 kA[4], kB[4];
-  float knA = 0.f, knB = 0.f;
-  int oldA = 0, oldB = 0;
   auto run = [&](const u32x4 (&kf)[4], float knv, int oldv, int t) __attribute__((always_inline)) {
     const int lk = (wv * tpw + t) * 32 + q;
     const bool valid = key0 + lk < n;
@@ -752,16 +752,33 @@ __global__ __launch_bounds__(256) void k_assign_reg(
     score_tile<NB>(af, an, ones, kf, M1, M2, B1);
     decide_tile<FIRST>(M1, M2, B1, knv, oldv, lk, valid, N, cf, L.lists, wv, wn, un);
   };
-  if (tcount > 0) load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0, n, q, h, kA, knA, oldA);
-  // the scheduling barriers keep each prefetch ahead of the tile it overlaps
-  for (int t = 0; t < tcount; t += 2) {
-    load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(t + 1, tcount - 1), n, q, h, kB, knB, oldB);
-    __builtin_amdgcn_sched_barrier(0);
-    run(kA, knA, oldA, t);
-    if (t + 1 >= tcount) break;
-    load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(t + 2, tcount - 1), n, q, h, kA, knA, oldA);
-    __builtin_amdgcn_sched_barrier(0);
-    run(kB, knB, oldB, t + 1);
+  // Ring of kAssignDepth + 1 register sets: tile t + kAssignDepth is loaded
+  // while tile t is scored (deeper rings measured no faster: the loop is
+  // bound by the scoring, not by the loads).  Loads past the last tile repeat
+  // it.  The scheduling barriers keep each prefetch ahead of the tile it
+  // overlaps.
+  constexpr int D = kAssignDepth;
+  u32x4 kb[D + 1][4];
+  float knb[D + 1];
+  int oldb[D + 1];
+#pragma unroll
+  for (int r = 0; r <= D; ++r) {
+    knb[r] = 0.f;
+    oldb[r] = 0;
+  }
+#pragma unroll
+  for (int r = 0; r < D; ++r)
+    load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(r, tcount - 1), n, q, h, kb[r], knb[r], oldb[r]);
+  for (int t0 = 0; t0 < tcount; t0 += D + 1) {
+#pragma unroll
+    for (int r = 0; r <= D; ++r) {
+      const int t = t0 + r;
+      if (t >= tcount) break;
+      const int w = (r + D) % (D + 1);
+      load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(t + D, tcount - 1), n, q, h, kb[w], knb[w], oldb[w]);
+      __builtin_amdgcn_sched_barrier(0);
+      run(kb[r], knb[r], oldb[r], t);
+    }
   }
   if (lane == 0) {
     cnt.wcnt[wv] = wn;
@@ -1224,22 +1241,30 @@ __global__ __launch_bounds__(256) void k_attend_prep(const float* __restrict__ c
   if (lane == 0) ginit[bh * Npad + g] = cnt > 0 ? log2f((float)cnt) * inv_sl2e : -INFINITY;
 }
 
-// grid (ceil(tiles / (4 * kAttTpw)), BH), 256 threads, N <= kAttMaxN.
+// grid (ceil(tiles / (4 * tpw)), BH), 256 threads, N <= 32 NB (NB <= 8).
 // LDS: sign(scale) R as [Npad][kRs] bf16, Vt as [64][vts] bf16, ginit [Npad].
-// Scores: MFMA with A = R rows (32 groups), B = Q tile (32 queries); accumulator
-// init ginit.  t = acc * sl2e; online max per 32-group block, rescaled only when
-// the block max exceeds the running max by more than 8 (log2 units).  Combine:
-// MFMA with A = Vt rows (32 features x 16 groups), B = bf16(exp2(t - m)) taken
-// straight from the score registers (the group order of the contraction axis
-// is the score layout's, applied identically to A).
+// Each wave owns tpw consecutive 32-query tiles; the next tile's queries are
+// loaded while the current one is processed (two register sets in turn).
+// Scores: MFMA with A = R rows (32 groups), B = Q tile (32 queries);
+// accumulator init ginit.  t = acc * sl2e; online max per 32-group block,
+// rescaled only when the block max exceeds the running max by more than 8
+// (log2 units).  Combine: MFMA with A = Vt rows (32 features x 16 groups), B =
+// bf16(exp2(t - m)) taken straight from the score registers (the group order
+// of the contraction axis is the score layout's, applied identically to A).
+// The denominator sum_j c_j e_ij comes from the matrix core too: a third
+// combine tile whose A operand is a constant row of ones (row 0) adds the same
+// bf16 weights the numerator uses.
+// Queries past n are computed as the slice's last query and store that
+// query's (identical) output, so every lane loads and stores unconditionally.
+template <int NB>
 __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict__ Q,
                                                      const uint16_t* __restrict__ R,
                                                      const uint16_t* __restrict__ Vt,
                                                      const float* __restrict__ ginit, int n, int N,
-                                                     int vts, float sl2e, uint32_t rsign,
+                                                     int vts, float sl2e, uint32_t rsign, int tpw,
                                                      uint16_t* __restrict__ O) {
   extern __shared__ __align__(16) unsigned char smem[];
-  const int Npad = (N + 31) & ~31;
+  constexpr int Npad = NB * 32;
   uint16_t* Rs = (uint16_t*)smem;
   uint16_t* Vs = Rs + Npad * kRs;
   float* gi = (float*)(Vs + 64 * vts);
@@ -1268,107 +1293,122 @@ __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict_
     nonempty |= (x != -INFINITY);
   }
   const int any = __syncthreads_or(nonempty);
-  const int nblk = Npad >> 5;
 
-  const int64_t tile0 = ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(wave)) * kAttTpw;
-  for (int tt = 0; tt < kAttTpw; ++tt) {
-    const int64_t tile = tile0 + tt;
-    if (tile * 32 >= n) break;
-    const int64_t qi = tile * 32 + q;
-    const bool valid = qi < n;
-    uint16_t* orow = O + (bh * n + (valid ? qi : 0)) * 64;
-    if (!any) {
-      if (valid)
-        for (int c = h * 32; c < h * 32 + 32; c += 8) *(u32x4*)(orow + c) = u32x4{0u, 0u, 0u, 0u};
-      continue;
-    }
-    const uint16_t* qrow = Q + (bh * n + (valid ? qi : 0)) * 64 + h * 32;
-    u32x4 qf[4];
+  const int64_t tile0 = ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(wave)) * tpw;
+  const int64_t ntiles = ((int64_t)n + 31) / 32;
+  const int tcount = (int)max((int64_t)0, min((int64_t)tpw, ntiles - tile0));
+  const uint16_t* Qbh = Q + bh * (int64_t)n * 64 + h * 32;
+  uint16_t* Obh = O + bh * (int64_t)n * 64;
+  // A operand of the denominator tile: row 0 (lane 0 and its h = 1 partner) all ones
+  const u32x4 ones_row = q == 0 ? u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u} : u32x4{0u, 0u, 0u, 0u};
+
+  auto qload = [&](int t, u32x4 (&qf)[4]) __attribute__((always_inline)) {
+    const int64_t qi = min((tile0 + t) * 32 + q, (int64_t)n - 1);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      qf[s] = u32x4{0u, 0u, 0u, 0u};
-      if (valid) qf[s] = *(const u32x4*)(qrow + s * 8);
-    }
-    f32x16 o0, o1;
+    for (int s = 0; s < 4; ++s) qf[s] = *(const u32x4*)(Qbh + qi * 64 + s * 8);
+  };
+  auto run = [&](int t, const u32x4 (&qf)[4]) __attribute__((always_inline)) {
+    f32x16 o0, o1, o2;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       o0[v] = 0.f;
       o1[v] = 0.f;
+      o2[v] = 0.f;
     }
-    float mt = -INFINITY, ssum = 0.f;
-    for (int blk = 0; blk < nblk; ++blk) {
-      f32x16 acc;
-      const float* gb = gi + blk * 32 + 4 * h;
+    float mt = -INFINITY;
+    if (any) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[v] = gb[8 * (v >> 2) + (v & 3)];
-      const uint16_t* ar = Rs + (blk * 32 + q) * kRs + h * 32;
+      for (int blk = 0; blk < NB; ++blk) {
+        f32x16 acc;
+        const float* gb = gi + blk * 32 + 4 * h;
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const u32x4 a = *(const u32x4*)(ar + s * 8);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                      __builtin_bit_cast(bf16x8, qf[s]), acc, 0, 0, 0);
-      }
-      float bm = acc[0];
+        for (int v = 0; v < 16; ++v) acc[v] = gb[8 * (v >> 2) + (v & 3)];
+        const uint16_t* ar = Rs + (blk * 32 + q) * kRs + h * 32;
 #pragma unroll
-      for (int v = 1; v < 16; ++v) bm = __builtin_amdgcn_fmed3f(bm, acc[v], INFINITY);
-      bm = __builtin_amdgcn_fmed3f(bm, __shfl_xor(bm, 32), INFINITY);
-      if (bm == -INFINITY) continue;  // every group of this block is empty (uniform)
-      const float bmt = bm * sl2e;
-      if (bmt > mt + 8.0f) {
-        const float alpha = __builtin_amdgcn_exp2f(mt - bmt);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          o0[v] *= alpha;
-          o1[v] *= alpha;
+        for (int s = 0; s < 4; ++s) {
+          const u32x4 a = *(const u32x4*)(ar + s * 8);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                        __builtin_bit_cast(bf16x8, qf[s]), acc, 0, 0, 0);
         }
-        ssum *= alpha;
-        mt = bmt;
-      }
-      float e[16];
+        float bm = acc[0];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        e[v] = __builtin_amdgcn_exp2f(fmaf(acc[v], sl2e, -mt));
-        ssum += e[v];
-      }
-      u32x4 b0, b1;
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        b0[w] = pack_bf16x2(e[2 * w], e[2 * w + 1]);
-        b1[w] = pack_bf16x2(e[8 + 2 * w], e[8 + 2 * w + 1]);
-      }
-#pragma unroll
-      for (int sp = 0; sp < 2; ++sp) {
-        const int gcol = blk * 32 + 16 * sp + 4 * h;
-        const u32x4 bsp = sp == 0 ? b0 : b1;
+        for (int v = 1; v < 16; ++v) bm = __builtin_amdgcn_fmed3f(bm, acc[v], INFINITY);
         {
-          const uint16_t* vr = Vs + q * vts + gcol;
-          const u32x2 lo = *(const u32x2*)vr, hi = *(const u32x2*)(vr + 8);
-          const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
-          o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                       __builtin_bit_cast(bf16x8, bsp), o0, 0, 0, 0);
+          const u32x2 p = halves(__float_as_uint(bm));
+          bm = __builtin_amdgcn_fmed3f(__uint_as_float(p[0]), __uint_as_float(p[1]), INFINITY);
         }
-        {
-          const uint16_t* vr = Vs + (32 + q) * vts + gcol;
-          const u32x2 lo = *(const u32x2*)vr, hi = *(const u32x2*)(vr + 8);
-          const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
-          o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                       __builtin_bit_cast(bf16x8, bsp), o1, 0, 0, 0);
-        }
-      }
-    }
-    const float stot = ssum + __shfl_xor(ssum, 32);
-    const float inv = 1.0f / stot;
-    if (valid) {
+        if (bm == -INFINITY) continue;  // every group of this block is empty (uniform)
+        const float bmt = bm * sl2e;
+        if (mt == -INFINITY) {  // first non-empty block: nothing to rescale
+          mt = bmt;
+        } else if (bmt > mt + 8.0f) {
+          const float alpha = __builtin_amdgcn_exp2f(mt - bmt);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        u32x2 w0 = {pack_bf16x2(o0[4 * r] * inv, o0[4 * r + 1] * inv),
-                    pack_bf16x2(o0[4 * r + 2] * inv, o0[4 * r + 3] * inv)};
-        u32x2 w1 = {pack_bf16x2(o1[4 * r] * inv, o1[4 * r + 1] * inv),
-                    pack_bf16x2(o1[4 * r + 2] * inv, o1[4 * r + 3] * inv)};
-        *(u32x2*)(orow + 8 * r + 4 * h) = w0;
-        *(u32x2*)(orow + 32 + 8 * r + 4 * h) = w1;
+          for (int v = 0; v < 16; ++v) {
+            o0[v] *= alpha;
+            o1[v] *= alpha;
+          }
+          o2[0] *= alpha;
+          mt = bmt;
+        }
+        float e[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) e[v] = __builtin_amdgcn_exp2f(fmaf(acc[v], sl2e, -mt));
+        u32x4 b0, b1;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          b0[w] = pack_bf16x2(e[2 * w], e[2 * w + 1]);
+          b1[w] = pack_bf16x2(e[8 + 2 * w], e[8 + 2 * w + 1]);
+        }
+#pragma unroll
+        for (int sp = 0; sp < 2; ++sp) {
+          const int gcol = blk * 32 + 16 * sp + 4 * h;
+          const u32x4 bsp = sp == 0 ? b0 : b1;
+          {
+            const uint16_t* vr = Vs + q * vts + gcol;
+            const u32x2 lo = *(const u32x2*)vr, hi = *(const u32x2*)(vr + 8);
+            const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
+            o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                         __builtin_bit_cast(bf16x8, bsp), o0, 0, 0, 0);
+          }
+          {
+            const uint16_t* vr = Vs + (32 + q) * vts + gcol;
+            const u32x2 lo = *(const u32x2*)vr, hi = *(const u32x2*)(vr + 8);
+            const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
+            o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                         __builtin_bit_cast(bf16x8, bsp), o1, 0, 0, 0);
+          }
+          o2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ones_row),
+                                                       __builtin_bit_cast(bf16x8, bsp), o2, 0, 0, 0);
+        }
       }
     }
+    // row 0 of the third tile (register 0 of lanes h = 0) is the denominator of query q
+    const float stot = __uint_as_float(halves(__float_as_uint(o2[0]))[0]);
+    const float inv = any ? 1.0f / stot : 0.f;  // no group at all: zero output
+    uint16_t* orow = Obh + min((tile0 + t) * 32 + q, (int64_t)n - 1) * 64;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const u32x2 w0 = {pack_bf16x2(o0[4 * r] * inv, o0[4 * r + 1] * inv),
+                        pack_bf16x2(o0[4 * r + 2] * inv, o0[4 * r + 3] * inv)};
+      const u32x2 w1 = {pack_bf16x2(o1[4 * r] * inv, o1[4 * r + 1] * inv),
+                        pack_bf16x2(o1[4 * r + 2] * inv, o1[4 * r + 3] * inv)};
+      *(u32x2*)(orow + 8 * r + 4 * h) = w0;
+      *(u32x2*)(orow + 32 + 8 * r + 4 * h) = w1;
+    }
+  };
+  if (tcount <= 0) return;
+  u32x4 qA[4], qB[4];
+  qload(0, qA);
+  // the scheduling barriers keep each prefetch ahead of the tile it overlaps
+  for (int t = 0; t < tcount; t += 2) {
+    qload(min(t + 1, tcount - 1), qB);
+    __builtin_amdgcn_sched_barrier(0);
+    run(t, qA);
+    if (t + 1 >= tcount) break;
+    qload(min(t + 2, tcount - 1), qA);
+    __builtin_amdgcn_sched_barrier(0);
+    run(t + 1, qB);
   }
 }
 
@@ -1459,13 +1499,41 @@ void set_lds_limits() {
                               (int)kAssignLdsMax);
     (void)hipFuncSetAttribute((const void*)k_bucket, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)bucket_lds(kMaxGroups));
-    (void)hipFuncSetAttribute((const void*)k_attend_bf16, hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)attend_lds(kAttMaxN));
+    for (const void* f : {(const void*)k_attend_bf16<1>, (const void*)k_attend_bf16<2>, (const void*)k_attend_bf16<3>,
+                          (const void*)k_attend_bf16<4>, (const void*)k_attend_bf16<5>, (const void*)k_attend_bf16<6>,
+                          (const void*)k_attend_bf16<7>, (const void*)k_attend_bf16<8>})
+      (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)attend_lds(kAttMaxN));
     (void)hipGetLastError();
   });
 }
 
 inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
+
+// Workgroups of 256 threads that the current device holds at once for `fn`
+// with `lds` bytes of dynamic LDS (runtime occupancy query, cached).
+int64_t resident_wgs(const void* fn, size_t lds) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, const void*, size_t>, int64_t> cache;
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  std::lock_guard<std::mutex> lock(mu);
+  const auto key = std::make_tuple(dev, fn, lds);
+  const auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, lds) != hipSuccess || per_cu < 1) per_cu = 1;
+  (void)hipGetLastError();
+  return cache[key] = (int64_t)cus * per_cu;
+}
+
+// Tiles per wave so that a grid of (ceil(tiles / (4 tpw)), BH) workgroups of
+// 4 waves fits in one round of `resident` workgroups (at least 1, at most cap).
+int64_t tiles_per_wave(int64_t tiles, int64_t BH, int64_t resident, int64_t cap) {
+  const int64_t per_slice = max((int64_t)1, resident / max((int64_t)1, BH));
+  const int64_t tpw = (tiles + 4 * per_slice - 1) / (4 * per_slice);
+  return tpw < 1 ? 1 : (tpw > cap ? cap : tpw);
+}
 
 }  // namespace
 
@@ -1528,12 +1596,6 @@ hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint
   set_lds_limits();
   if (d.dtype == 1) {
     const int64_t tiles = (d.n + 31) / 32;
-    // about 512 workgroups (two per CU, all resident at once), the same number
-    // for every slice, as many tiles each as the LDS allows (at most 16 per wave)
-    const int64_t wg_per_slice = d.BH >= 512 ? 1 : 512 / d.BH;
-    int64_t tpw = (tiles + 4 * wg_per_slice - 1) / (4 * wg_per_slice);
-    tpw = tpw < 1 ? 1 : (tpw > 16 ? 16 : tpw);
-    while (tpw > 1 && assign_lds(d.N, (int)tpw) > kAssignLdsMax) --tpw;
     const int Npad = (d.N + 31) & ~31;
     // |MFMA fp32 accumulation error| <= (d + 4) 2^-24 * 2 * sum|terms| (each of the
     // d products and the three |r|^2 terms added with at most one rounding,
@@ -1542,8 +1604,6 @@ hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint
     // < 2^(4 - 23) of its magnitude.
     const float cm = (float)(kD + 4) * 0x1p-23f * (1.0f + 0x1p-10f);
     const float cp = 0x1p-19f * (1.0f + 0x1p-10f);
-    const dim3 grid(cdiv(tiles, 4 * tpw), (unsigned)d.BH), block(256);
-    const size_t lds = assign_lds(d.N, (int)tpw);
     // Npad <= 128: the register-resident kernel, one instantiation per block count
     using AssignFn = void (*)(const uint16_t*, const uint16_t*, const uint16_t*, const double*, float*, int32_t*,
                               int32_t*, unsigned long long*, int, int, int, float, float);
@@ -1555,6 +1615,13 @@ hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint
       case 4: kern = first ? k_assign_reg<true, 4> : k_assign_reg<false, 4>; break;
       default: break;
     }
+    // one round of resident workgroups, the same number per slice, at most 16
+    // tiles per wave (the LDS lists grow with tpw; the occupancy is taken at 16)
+    int64_t tpw = 16;
+    while (tpw > 1 && assign_lds(d.N, (int)tpw) > kAssignLdsMax) --tpw;
+    tpw = tiles_per_wave(tiles, d.BH, resident_wgs((const void*)kern, assign_lds(d.N, (int)tpw)), tpw);
+    const dim3 grid(cdiv(tiles, 4 * tpw), (unsigned)d.BH), block(256);
+    const size_t lds = assign_lds(d.N, (int)tpw);
     hipLaunchKernelGGL(kern, grid, block, lds, st, (const uint16_t*)K, (const uint16_t*)R, nsplit, nrm64, knorm,
                        belong, mcount, mrec, d.n, d.N, (int)tpw, cm, cp);
   } else {
@@ -1647,11 +1714,17 @@ hipError_t launch_attend(const Dims& d, const void* Q, const void* R, const uint
   if (d.dtype == 1) {
     if (d.N > kAttMaxN) return hipErrorInvalidValue;
     const int64_t tiles = (d.n + 31) / 32;
-    const dim3 grid(cdiv(tiles, 4 * kAttTpw), (unsigned)d.BH), block(256);
     const uint32_t rsign = scale < 0.f ? 0x80008000u : 0u;
-    hipLaunchKernelGGL(k_attend_bf16, grid, block, attend_lds(d.N), st, (const uint16_t*)Q,
-                       (const uint16_t*)R, Vt, ginit, d.n, d.N, vt_stride(d.N), clamp_sl2e(scale), rsign,
-                       (uint16_t*)O);
+    using AttendFn = void (*)(const uint16_t*, const uint16_t*, const uint16_t*, const float*, int, int, int, float,
+                              uint32_t, int, uint16_t*);
+    static const AttendFn fns[8] = {k_attend_bf16<1>, k_attend_bf16<2>, k_attend_bf16<3>, k_attend_bf16<4>,
+                                    k_attend_bf16<5>, k_attend_bf16<6>, k_attend_bf16<7>, k_attend_bf16<8>};
+    const AttendFn fn = fns[((d.N + 31) >> 5) - 1];
+    // one round of resident workgroups, the same number per slice
+    const int64_t tpw = tiles_per_wave(tiles, d.BH, resident_wgs((const void*)fn, attend_lds(d.N)), 64);
+    const dim3 grid(cdiv(tiles, 4 * tpw), (unsigned)d.BH), block(256);
+    hipLaunchKernelGGL(fn, grid, block, attend_lds(d.N), st, (const uint16_t*)Q, (const uint16_t*)R, Vt, ginit, d.n,
+                       d.N, vt_stride(d.N), clamp_sl2e(scale), rsign, (int)tpw, (uint16_t*)O);
   } else {
     const dim3 grid(cdiv(d.n, 256), (unsigned)d.BH), block(256);
     hipLaunchKernelGGL(k_attend_f32, grid, block, 0, st, (const float*)Q, centroid, count, vsum, d.n, d.N,
