@@ -45,6 +45,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRs = 72;       // LDS row stride (bf16 elements) of the 32x16 MFMA A tiles
 constexpr int kAssignDepth = 1;  // key tiles loaded ahead per wave in k_assign_reg
+constexpr int kAttDepth = 1;     // query tiles loaded ahead per wave in k_attend_bf16
+constexpr int kOs = 72;          // LDS row stride (bf16) of the attention output tiles
 constexpr int kAttMaxN = 256; // groups held in LDS by the bf16 attention kernel
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
@@ -1242,13 +1244,16 @@ __global__ __launch_bounds__(256) void k_attend_prep(const float* __restrict__ c
 }
 
 // grid (ceil(tiles / (4 * tpw)), BH), 256 threads, N <= 32 NB (NB <= 8).
-// LDS: sign(scale) R as [Npad][kRs] bf16, Vt as [64][vts] bf16, ginit [Npad].
-// Each wave owns tpw consecutive 32-query tiles; the next tile's queries are
+// LDS: sign(scale) R as [Npad][kRs] bf16, Vt as [64][vts] bf16, ginit [Npad],
+// one [32][kOs] bf16 tile per wave (the wave's query tile, then its output
+// tile, both moved between HBM and LDS as whole rows).  Each wave owns tpw
+// consecutive 32-query tiles; the next tile's queries are
 // loaded while the current one is processed (two register sets in turn).
 // Scores: MFMA with A = R rows (32 groups), B = Q tile (32 queries);
-// accumulator init ginit.  t = acc * sl2e; online max per 32-group block,
-// rescaled only when the block max exceeds the running max by more than 8
-// (log2 units).  Combine: MFMA with A = Vt rows (32 features x 16 groups), B =
+// accumulator init ginit; t = acc * sl2e.  N <= 128: all scores of the tile,
+// then the exact max over its groups.  N > 128: online max per 32-group
+// block, rescaled only when the block max exceeds the running max by more than
+// 8 (log2 units).  Combine: MFMA with A = Vt rows (32 features x 16 groups), B =
 // bf16(exp2(t - m)) taken straight from the score registers (the group order
 // of the contraction axis is the score layout's, applied identically to A).
 // The denominator sum_j c_j e_ij comes from the matrix core too: a third
@@ -1269,6 +1274,7 @@ __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict_
   uint16_t* Vs = Rs + Npad * kRs;
   float* gi = (float*)(Vs + 64 * vts);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
+  uint16_t* Ow = (uint16_t*)(gi + Npad) + wave * 32 * kOs;  // this wave's output tile
   const int64_t bh = blockIdx.y;
   const uint16_t* Rbh = R + bh * (int64_t)N * 64;
   for (int idx = tid; idx < Npad * 8; idx += 256) {
@@ -1297,17 +1303,28 @@ __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict_
   const int64_t tile0 = ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(wave)) * tpw;
   const int64_t ntiles = ((int64_t)n + 31) / 32;
   const int tcount = (int)max((int64_t)0, min((int64_t)tpw, ntiles - tile0));
-  const uint16_t* Qbh = Q + bh * (int64_t)n * 64 + h * 32;
+  const uint16_t* Qbh = Q + bh * (int64_t)n * 64;
   uint16_t* Obh = O + bh * (int64_t)n * 64;
   // A operand of the denominator tile: row 0 (lane 0 and its h = 1 partner) all ones
   const u32x4 ones_row = q == 0 ? u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u} : u32x4{0u, 0u, 0u, 0u};
 
-  auto qload = [&](int t, u32x4 (&qf)[4]) __attribute__((always_inline)) {
-    const int64_t qi = min((tile0 + t) * 32 + q, (int64_t)n - 1);
+  // Query tile t in row-major order: lane l holds 16 bytes (chunk l % 8) of
+  // rows l / 8 + 8 k, so each load instruction reads 8 whole 128-byte rows.
+  auto qload = [&](int t, u32x4 (&qc)[4]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) qf[s] = *(const u32x4*)(Qbh + qi * 64 + s * 8);
+    for (int k = 0; k < 4; ++k) {
+      const int64_t qi = min((tile0 + t) * 32 + 8 * k + (lane >> 3), (int64_t)n - 1);
+      qc[k] = *(const u32x4*)(Qbh + qi * 64 + (lane & 7) * 8);
+    }
   };
-  auto run = [&](int t, const u32x4 (&qf)[4]) __attribute__((always_inline)) {
+  auto run = [&](int t, const u32x4 (&qc)[4]) __attribute__((always_inline)) {
+    // to MFMA B fragments through the wave's LDS tile: lane (h, q) takes
+    // features 32 h + 8 s .. +7 of query q at k-step s
+#pragma unroll
+    for (int k = 0; k < 4; ++k) *(u32x4*)(Ow + (8 * k + (lane >> 3)) * kOs + (lane & 7) * 8) = qc[k];
+    u32x4 qf[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qf[s] = *(const u32x4*)(Ow + q * kOs + h * 32 + s * 8);
     f32x16 o0, o1, o2;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
@@ -1316,7 +1333,68 @@ __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict_
       o2[v] = 0.f;
     }
     float mt = -INFINITY;
-    if (any) {
+    if (NB <= 4 && any) {
+      // All scores first (NB accumulators), then one exact max over every
+      // group of the tile, then exp2 / pack / combine per block: no branch
+      // inside the tile, so one block's MFMAs overlap another's VALU work.
+      f32x16 acc[NB];
+#pragma unroll
+      for (int blk = 0; blk < NB; ++blk) {
+        const float* gb = gi + blk * 32 + 4 * h;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[blk][v] = gb[8 * (v >> 2) + (v & 3)];
+        const uint16_t* ar = Rs + (blk * 32 + q) * kRs + h * 32;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const u32x4 a = *(const u32x4*)(ar + s * 8);
+          acc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                             __builtin_bit_cast(bf16x8, qf[s]), acc[blk], 0, 0, 0);
+        }
+      }
+      float bm = -INFINITY;
+#pragma unroll
+      for (int blk = 0; blk < NB; ++blk)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) bm = __builtin_amdgcn_fmed3f(bm, acc[blk][v], INFINITY);
+      {
+        const u32x2 p = halves(__float_as_uint(bm));
+        bm = __builtin_amdgcn_fmed3f(__uint_as_float(p[0]), __uint_as_float(p[1]), INFINITY);
+      }
+      // some group is non-empty (any), so bm is finite; empty groups give exp2(-inf) = 0
+      const float nm = -bm * sl2e;
+#pragma unroll
+      for (int blk = 0; blk < NB; ++blk) {
+        u32x4 b0, b1;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          b0[w] = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(acc[blk][2 * w], sl2e, nm)),
+                              __builtin_amdgcn_exp2f(fmaf(acc[blk][2 * w + 1], sl2e, nm)));
+          b1[w] = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(acc[blk][8 + 2 * w], sl2e, nm)),
+                              __builtin_amdgcn_exp2f(fmaf(acc[blk][8 + 2 * w + 1], sl2e, nm)));
+        }
+#pragma unroll
+        for (int sp = 0; sp < 2; ++sp) {
+          const int gcol = blk * 32 + 16 * sp + 4 * h;
+          const u32x4 bsp = sp == 0 ? b0 : b1;
+          {
+            const uint16_t* vr = Vs + q * vts + gcol;
+            const u32x2 lo = *(const u32x2*)vr, hi = *(const u32x2*)(vr + 8);
+            const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
+            o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                         __builtin_bit_cast(bf16x8, bsp), o0, 0, 0, 0);
+          }
+          {
+            const uint16_t* vr = Vs + (32 + q) * vts + gcol;
+            const u32x2 lo = *(const u32x2*)vr, hi = *(const u32x2*)(vr + 8);
+            const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
+            o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                         __builtin_bit_cast(bf16x8, bsp), o1, 0, 0, 0);
+          }
+          o2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ones_row),
+                                                       __builtin_bit_cast(bf16x8, bsp), o2, 0, 0, 0);
+        }
+      }
+    } else if (any) {
 #pragma unroll
       for (int blk = 0; blk < NB; ++blk) {
         f32x16 acc;
@@ -1386,29 +1464,41 @@ __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict_
     // row 0 of the third tile (register 0 of lanes h = 0) is the denominator of query q
     const float stot = __uint_as_float(halves(__float_as_uint(o2[0]))[0]);
     const float inv = any ? 1.0f / stot : 0.f;  // no group at all: zero output
-    uint16_t* orow = Obh + min((tile0 + t) * 32 + q, (int64_t)n - 1) * 64;
+    // The output tile goes through the wave's LDS tile (rows of kOs bf16) so
+    // that each store instruction writes 8 whole 128-byte rows.
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const u32x2 w0 = {pack_bf16x2(o0[4 * r] * inv, o0[4 * r + 1] * inv),
                         pack_bf16x2(o0[4 * r + 2] * inv, o0[4 * r + 3] * inv)};
       const u32x2 w1 = {pack_bf16x2(o1[4 * r] * inv, o1[4 * r + 1] * inv),
                         pack_bf16x2(o1[4 * r + 2] * inv, o1[4 * r + 3] * inv)};
-      *(u32x2*)(orow + 8 * r + 4 * h) = w0;
-      *(u32x2*)(orow + 32 + 8 * r + 4 * h) = w1;
+      *(u32x2*)(Ow + q * kOs + 8 * r + 4 * h) = w0;
+      *(u32x2*)(Ow + q * kOs + 32 + 8 * r + 4 * h) = w1;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = 8 * k + (lane >> 3), ch = lane & 7;
+      const u32x4 v = *(const u32x4*)(Ow + row * kOs + ch * 8);
+      *(u32x4*)(Obh + min((tile0 + t) * 32 + row, (int64_t)n - 1) * 64 + ch * 8) = v;
     }
   };
   if (tcount <= 0) return;
-  u32x4 qA[4], qB[4];
-  qload(0, qA);
-  // the scheduling barriers keep each prefetch ahead of the tile it overlaps
-  for (int t = 0; t < tcount; t += 2) {
-    qload(min(t + 1, tcount - 1), qB);
-    __builtin_amdgcn_sched_barrier(0);
-    run(t, qA);
-    if (t + 1 >= tcount) break;
-    qload(min(t + 2, tcount - 1), qA);
-    __builtin_amdgcn_sched_barrier(0);
-    run(t + 1, qB);
+  // Ring of kAttDepth + 1 register sets: tile t + kAttDepth is loaded while
+  // tile t is processed.  Loads past the last tile repeat it.  The scheduling
+  // barriers keep each prefetch ahead of the tile it overlaps.
+  constexpr int D = kAttDepth;
+  u32x4 qb[D + 1][4];
+#pragma unroll
+  for (int r = 0; r < D; ++r) qload(min(r, tcount - 1), qb[r]);
+  for (int t0 = 0; t0 < tcount; t0 += D + 1) {
+#pragma unroll
+    for (int r = 0; r <= D; ++r) {
+      const int t = t0 + r;
+      if (t >= tcount) break;
+      qload(min(t + D, tcount - 1), qb[(r + D) % (D + 1)]);
+      __builtin_amdgcn_sched_barrier(0);
+      run(t, qb[r]);
+    }
   }
 }
 
@@ -1484,7 +1574,7 @@ size_t assign_lds(int N, int tpw = 12) {
 size_t bucket_lds(int N) { return (size_t)16 * N * 8 + (size_t)2 * N * 4; }
 size_t attend_lds(int N) {
   const int Npad = (N + 31) & ~31;
-  return (size_t)Npad * kRs * 2 + (size_t)64 * vt_stride(N) * 2 + (size_t)Npad * 4;
+  return (size_t)Npad * kRs * 2 + (size_t)64 * vt_stride(N) * 2 + (size_t)Npad * 4 + (size_t)4 * 32 * kOs * 2;
 }
 
 // Raise the dynamic-LDS limit of the kernels that can exceed 64 KB to the
