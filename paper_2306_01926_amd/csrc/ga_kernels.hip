@@ -161,26 +161,52 @@ __device__ int exact_argmin_wave(const typename S::T* __restrict__ krow,
 }
 
 // ------------------------------------------------------------------ init
-// grid (ceil(N/4), BH), 256 threads: one wave per group, lane = feature.
+// grid (ceil(N/64), BH), 256 threads; groups g0 = 64 x .. g0 + 63.  Each wave
+// reads 16 groups' initial rows at once (lane = feature) and writes C and R;
+// then one lane per group forms the canonical |r|^2 from the LDS copy of R.
 template <class S>
 __global__ __launch_bounds__(256) void k_init(const typename S::T* __restrict__ K,
                                               const float* __restrict__ init, int n, int N,
                                               float* __restrict__ C, typename S::T* __restrict__ R,
                                               double* __restrict__ nrm64, uint16_t* __restrict__ nsplit,
                                               int32_t* __restrict__ mcount) {
-  const int lane = threadIdx.x & 63;
-  const int g = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+  __shared__ float rsh[64][65];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bh = blockIdx.y;
-  if (g >= N) return;
-  const int64_t row = bh * N + g;
-  const float c = init ? init[row * 64 + lane]
-                       : S::load(K, (bh * n + ((int64_t)g * n) / N) * 64 + lane);
-  C[row * 64 + lane] = c;
-  if (mcount && g == 0 && lane == 0) {
+  const int g0 = blockIdx.x * 64, ng = min(64, N - g0);
+  float c[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int g = min(g0 + wave * 16 + i, N - 1);
+    const int64_t row = bh * N + g;
+    c[i] = init ? init[row * 64 + lane] : S::load(K, (bh * n + ((int64_t)g * n) / N) * 64 + lane);
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int gl = wave * 16 + i;
+    if (gl >= ng) break;
+    const int64_t row = bh * N + g0 + gl;
+    C[row * 64 + lane] = c[i];
+    const float r = S::rep(c[i]);
+    S::store(R, row * 64 + lane, r);
+    rsh[gl][lane] = r;
+  }
+  if (mcount && blockIdx.x == 0 && tid == 0) {
     mcount[bh] = 0;
     mcount[gridDim.y + bh] = 0;
   }
-  finalize_rep<S>(c, row, R, nrm64, nsplit);
+  __syncthreads();
+  if (tid < ng) {
+    const int64_t row = bh * N + g0 + tid;
+    double nrm = 0.0;
+#pragma unroll 8
+    for (int cc = 0; cc < 64; ++cc) {
+      const double rc = (double)rsh[tid][cc];
+      nrm = fma(rc, rc, nrm);
+    }
+    nrm64[row] = nrm;
+    write_nsplit(nrm, nsplit + row * 8);
+  }
 }
 
 // ------------------------------------------------------------------ assign (bf16, MFMA)
@@ -717,6 +743,27 @@ __global__ __launch_bounds__(256) void k_assign_reg(
   const int64_t bh = blockIdx.y;
   if (tid == 0) cnt.nx = 0;
   const AssignLds L = assign_lds_layout(smem, Npad, tpw, &cnt);
+  const int64_t key0 = (int64_t)blockIdx.x * 4 * tpw * 32;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int64_t tile0 = key0 / 32 + (int64_t)wv * tpw;
+  const int64_t ntiles = ((int64_t)n + 31) / 32;
+  const int tcount = (int)max((int64_t)0, min((int64_t)tpw, ntiles - tile0));
+  const uint16_t* Kbh = K + bh * (int64_t)n * 64;
+  const float* knorm_bh = knorm + bh * n;
+  const int32_t* belong_bh = belong + bh * n;
+  // The first key tiles (see the ring below) load while the workgroup stages R.
+  constexpr int D = kAssignDepth;
+  u32x4 kb[D + 1][4];
+  float knb[D + 1];
+  int oldb[D + 1];
+#pragma unroll
+  for (int r = 0; r <= D; ++r) {
+    knb[r] = 0.f;
+    oldb[r] = 0;
+  }
+#pragma unroll
+  for (int r = 0; r < D; ++r)
+    load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(r, tcount - 1), n, q, h, kb[r], knb[r], oldb[r]);
   const double nmax = stage_reps<Npad>(R + bh * (int64_t)N * 64, nsplit + bh * N * 8, nrm64 + bh * N, N, Npad, L.Rs,
                                        L.Ns, red);
   const float nmaxf = (float)nmax * (1.0f + 0x1p-20f);
@@ -731,15 +778,6 @@ __global__ __launch_bounds__(256) void k_assign_reg(
     for (int s2 = 0; s2 < 4; ++s2) af[b][s2] = *(const u32x4*)(L.Rs + swz(b * 32 + q, 4 * h + s2));
   }
   const u32x4 ones = h == 0 ? u32x4{0x3f803f80u, 0x3f80u, 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
-
-  const int64_t key0 = (int64_t)blockIdx.x * 4 * tpw * 32;
-  const int wv = __builtin_amdgcn_readfirstlane(wave);
-  const int64_t tile0 = key0 / 32 + (int64_t)wv * tpw;
-  const int64_t ntiles = ((int64_t)n + 31) / 32;
-  const int tcount = (int)max((int64_t)0, min((int64_t)tpw, ntiles - tile0));
-  const uint16_t* Kbh = K + bh * (int64_t)n * 64;
-  const float* knorm_bh = knorm + bh * n;
-  const int32_t* belong_bh = belong + bh * n;
 
   int wn = 0, un = 0;  // this wave's moved / uncertain entries (wave-uniform)
   auto run = [&](const u32x4 (&kf)[4], float knv, int oldv, int t) __attribute__((always_inline)) {
@@ -759,18 +797,6 @@ __global__ __launch_bounds__(256) void k_assign_reg(
   // bound by the scoring, not by the loads).  Loads past the last tile repeat
   // it.  The scheduling barriers keep each prefetch ahead of the tile it
   // overlaps.
-  constexpr int D = kAssignDepth;
-  u32x4 kb[D + 1][4];
-  float knb[D + 1];
-  int oldb[D + 1];
-#pragma unroll
-  for (int r = 0; r <= D; ++r) {
-    knb[r] = 0.f;
-    oldb[r] = 0;
-  }
-#pragma unroll
-  for (int r = 0; r < D; ++r)
-    load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(r, tcount - 1), n, q, h, kb[r], knb[r], oldb[r]);
   for (int t0 = 0; t0 < tcount; t0 += D + 1) {
 #pragma unroll
     for (int r = 0; r <= D; ++r) {
@@ -1219,7 +1245,9 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
 }
 
 // ------------------------------------------------------------------ attention (bf16)
-// grid (ceil(Npad/4), BH), 256 threads: one wave per (padded) group, lane = feature.
+// grid (ceil(Npad/64), BH), 256 threads; groups g0 = 64 x .. (padded groups
+// past N get zeros).  Each wave reads 16 groups' rows (lane = feature), the
+// transposed value means go through LDS and out as whole row segments.
 // Vt holds the group's value MEAN vsum_j / count_j (bf16) so that the count
 // weight can move into the exponent: o_i = sum_j c_j e_ij mu_j / sum_j c_j e_ij
 // with c_j e_ij = exp2(t_ij + log2 c_j).  ginit_j = log2(c_j) / sl2e is added to
@@ -1229,18 +1257,37 @@ __global__ __launch_bounds__(256) void k_attend_prep(const float* __restrict__ c
                                                      const float* __restrict__ vsum, float inv_sl2e,
                                                      int N, int vts, uint16_t* __restrict__ Rq,
                                                      uint16_t* __restrict__ Vt, float* __restrict__ ginit) {
-  const int lane = threadIdx.x & 63;
-  const int g = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+  __shared__ uint16_t mt[64][66];  // [feature][group] value means, bf16
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bh = blockIdx.y;
   const int Npad = (N + 31) & ~31;
-  if (g >= Npad) return;
-  const bool valid = g < N;
-  const int64_t row = bh * N + g;
-  const int cnt = valid ? count[row] : 0;
-  if (Rq && valid) Rq[row * 64 + lane] = (uint16_t)f32_to_bf16(centroid[row * 64 + lane]);
-  const float mu = cnt > 0 ? vsum[row * 64 + lane] / (float)cnt : 0.f;
-  Vt[(bh * 64 + lane) * vts + g] = (uint16_t)f32_to_bf16(mu);
-  if (lane == 0) ginit[bh * Npad + g] = cnt > 0 ? log2f((float)cnt) * inv_sl2e : -INFINITY;
+  const int g0 = blockIdx.x * 64, ng = min(64, Npad - g0);
+  int cnt[16];
+  float vs[16], cen[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int g = g0 + wave * 16 + i;
+    const int64_t row = bh * N + min(g, N - 1);
+    cnt[i] = g < N ? count[row] : 0;
+    vs[i] = vsum[row * 64 + lane];
+    if (Rq) cen[i] = centroid[row * 64 + lane];
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int gl = wave * 16 + i, g = g0 + gl;
+    if (gl >= ng) break;
+    const int64_t row = bh * N + g;
+    if (Rq && g < N) Rq[row * 64 + lane] = (uint16_t)f32_to_bf16(cen[i]);
+    const float mu = cnt[i] > 0 ? vs[i] / (float)cnt[i] : 0.f;
+    mt[lane][gl] = (uint16_t)f32_to_bf16(mu);
+    if (lane == 0) ginit[bh * Npad + g] = cnt[i] > 0 ? log2f((float)cnt[i]) * inv_sl2e : -INFINITY;
+  }
+  __syncthreads();
+  const int np = ng / 2;  // group pairs per feature row
+  for (int idx = tid; idx < 64 * np; idx += 256) {
+    const int f = idx / np, pr = idx % np;
+    *(uint32_t*)(Vt + (bh * 64 + f) * vts + g0 + 2 * pr) = *(const uint32_t*)&mt[f][2 * pr];
+  }
 }
 
 // grid (ceil(tiles / (4 * tpw)), BH), 256 threads, N <= 32 NB (NB <= 8).
@@ -1669,7 +1716,7 @@ size_t workspace_layout(const Dims& d, Workspace* ws, void* base) {
 hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C, void* R,
                        double* nrm64, uint16_t* nsplit, int32_t* mcount, hipStream_t st) {
   TimedLaunch timed("init", st);
-  const dim3 grid(cdiv(d.N, 4), (unsigned)d.BH), block(256);
+  const dim3 grid(cdiv(d.N, 64), (unsigned)d.BH), block(256);
   if (d.dtype == 1)
     hipLaunchKernelGGL(k_init<BF16>, grid, block, 0, st, (const uint16_t*)K, init, d.n, d.N, C,
                        (uint16_t*)R, nrm64, nsplit, mcount);
@@ -1790,7 +1837,7 @@ hipError_t launch_attend_prep(const Dims& d, const float* centroid, const int32_
                               bool make_rq, hipStream_t st) {
   TimedLaunch timed("attend_prep", st);
   const int Npad = (d.N + 31) & ~31;
-  const dim3 grid(cdiv(Npad, 4), (unsigned)d.BH), block(256);
+  const dim3 grid(cdiv(Npad, 64), (unsigned)d.BH), block(256);
   hipLaunchKernelGGL(k_attend_prep, grid, block, 0, st, centroid, count, vsum, 1.0f / clamp_sl2e(scale), d.N,
                      vt_stride(d.N), make_rq ? Rq : (uint16_t*)nullptr, Vt, ginit);
   return hipGetLastError();
