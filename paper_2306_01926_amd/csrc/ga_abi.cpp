@@ -83,18 +83,25 @@ ga::Dims dims_of(const ga_shape_t& s, int32_t N) {
 
 // Grouping on validated arguments.
 // bf16: the first round sums every member; later rounds apply only the keys
-// that changed group (exact fp64 sums make the order irrelevant).  Round t's
-// moved-key records are counted in mcount[t % 2].  fp32: every round re-sums
-// the members in ascending key order (fp32 sums need not be exact).
+// that changed group (exact fp64 sums make the order irrelevant), with a
+// group-sum launch over round t's moved-key records, counted in mcount[t % 2].
+// For N <= kFusedG with few enough assign workgroups per slice the first
+// round's assign launch writes per-workgroup partition sums and a small launch
+// adds them.  fp32: every round re-sums the members in ascending key order
+// (fp32 sums need not be exact).
 int run_cluster(const ga::Dims& d, const void* K, int32_t iters, const float* init, int32_t* belong,
                 int32_t* count, float* C, const ga::Workspace& w, hipStream_t st) {
   GA_LAUNCH(ga::launch_init(d, K, init, C, w.R, w.nrm64, w.nsplit, w.mcount, st), "init launch");
+  const ga::FusedUpdate fu{w.Sp, w.cntp, w.pbits};
   for (int t = 0; t < iters; ++t) {
     int32_t* mc_cur = w.mcount + (t & 1) * d.BH;
     int32_t* mc_next = w.mcount + ((t + 1) & 1) * d.BH;
-    GA_LAUNCH(ga::launch_assign(d, K, w.R, w.nsplit, w.nrm64, w.knorm, belong, mc_cur, w.mrec, t == 0, st),
-              "assign launch");
-    if (d.dtype == GA_BF16) {
+    int parts = 0;
+    GA_LAUNCH(ga::launch_assign(d, K, w.R, w.nsplit, w.nrm64, w.knorm, belong, mc_cur, w.mrec, t == 0, fu, &parts,
+                                st), "assign launch");
+    if (parts > 0) {
+      GA_LAUNCH(ga::launch_part_finish(d, parts, fu, w.S64, count, C, w.R, w.nrm64, w.nsplit, st), "update launch");
+    } else if (d.dtype == GA_BF16) {
       GA_LAUNCH(ga::launch_gsum(d, t == 0 ? 0 : 1, K, belong, w.mrec, mc_cur, mc_next, w.S64, count, C, w.R,
                                 w.nrm64, w.nsplit, st), "update launch");
     } else {

@@ -29,6 +29,22 @@ struct Workspace {
   double* S64;       // [BH][N][64] fp64 member sums carried across rounds (bf16 path)
   int32_t* mcount;   // [2][BH] moved-key records of rounds t with t % 2 = 0, 1
   unsigned long long* mrec;  // [BH][n] records (key << 32 | old << 16 | new)
+  double* Sp;        // [BH][kFusedP][N][64] per-partition fp64 sums of the fused update
+  int32_t* cntp;     // [BH][kFusedP][N] per-partition member counts
+  uint32_t* pbits;   // [BH][kFusedP][4] groups with members in each partition (bit g)
+};
+
+// First-round centroid update of the bf16 path for N <= kFusedG: every assign
+// workgroup (one partition of a slice's keys, at most kFusedP per slice) sums
+// the rows of its keys per group into its own partition of Sp;
+// launch_part_finish adds the partitions into S64 and forms count, C, R,
+// |r|^2 and the split.
+constexpr int kFusedG = 128;
+constexpr int kFusedP = 8;
+struct FusedUpdate {
+  double* Sp;
+  int32_t* cntp;
+  uint32_t* pbits;
 };
 
 struct Dims {
@@ -53,9 +69,17 @@ size_t workspace_layout(const Dims& d, Workspace* ws, void* base);  // returns b
 
 hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C, void* R,
                        double* nrm64, uint16_t* nsplit, int32_t* mcount, hipStream_t st);
+// First round, bf16, N <= kFusedG and at most kFusedP workgroups per slice:
+// the assign launch also writes the partition sums of the round's update (fu)
+// and *parts is their number per slice, to be finished by launch_part_finish;
+// else *parts = 0 and the caller runs the update (fu unused).
 hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint16_t* nsplit,
                          const double* nrm64, float* knorm, int32_t* belong, int32_t* mcount,
-                         unsigned long long* mrec, bool first, hipStream_t st);
+                         unsigned long long* mrec, bool first, const FusedUpdate& fu, int* parts,
+                         hipStream_t st);
+hipError_t launch_part_finish(const Dims& d, int parts, const FusedUpdate& fu, double* S64,
+                              int32_t* count, float* C, void* R, double* nrm64, uint16_t* nsplit,
+                              hipStream_t st);
 // bf16 path: exact fp64 group sums, each workgroup finishing its own groups (see ga_kernels.hip)
 hipError_t launch_gsum(const Dims& d, int mode, const void* X, const int32_t* belong,
                        const unsigned long long* mrec, const int32_t* mcount_cur, int32_t* mcount_next,

@@ -470,37 +470,48 @@ __device__ __forceinline__ double stage_reps(const uint16_t* __restrict__ Rbh, c
   return fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
 }
 
-// Dynamic LDS of the assign kernels: -2R as [Npad][64] bf16 (swizzled), the
-// |r|^2 split as [Npad][8] bf16, then four arrays of 4 tpw 32 words: moved
-// records, uncertain queue, staged groups, staged |k| bounds / exact-decision
-// moved records.
+// Dynamic LDS of the assign kernels: region A = -2R as [Npad][64] bf16
+// (swizzled), the |r|^2 split as [Npad][8] bf16 and the uncertain queue
+// (4 tpw 32 words), then three arrays of 4 tpw 32 words: moved records, staged
+// groups, staged |k| bounds / exact-decision moved records.  Region A is dead
+// once the exact decisions are done; the partition sums reuse it (and need it
+// at least fused_bytes(...) long).
+// Partition sums: the sorted key list (groups padded to 8) then four
+// per-wave [8][64] fp64 transpose tiles.
+__host__ __device__ constexpr int fused_words(int Npad, int cap4) { return (cap4 + 7 * Npad + 3) & ~3; }
+__host__ __device__ constexpr int fused_bytes(int Npad, int cap4) { return fused_words(Npad, cap4) * 4 + 4 * 4096; }
+__host__ __device__ constexpr int assign_region_a(int Npad, int cap4, bool fused) {
+  return fused && fused_bytes(Npad, cap4) > Npad * 144 + cap4 * 4 ? fused_bytes(Npad, cap4) : Npad * 144 + cap4 * 4;
+}
+
 struct AssignLds {
   uint16_t* Rs;
   uint16_t* Ns;
   AssignLists lists;
 };
 
-__device__ __forceinline__ AssignLds assign_lds_layout(unsigned char* smem, int Npad, int tpw, AssignCounts* c) {
+__device__ __forceinline__ AssignLds assign_lds_layout(unsigned char* smem, int Npad, int tpw, bool fused,
+                                                       AssignCounts* c) {
   const int cap = tpw * 32;
   AssignLds l;
   l.Rs = (uint16_t*)smem;
   l.Ns = l.Rs + Npad * 64;
   l.lists.c = c;
   l.lists.cap = cap;
-  l.lists.wrec = (uint32_t*)(l.Ns + Npad * 8);
-  l.lists.uq = l.lists.wrec + 4 * cap;
-  l.lists.bst = (int32_t*)(l.lists.uq + 4 * cap);
+  l.lists.uq = (uint32_t*)(l.Ns + Npad * 8);
+  l.lists.wrec = (uint32_t*)(smem + assign_region_a(Npad, 4 * cap, fused));
+  l.lists.bst = (int32_t*)(l.lists.wrec + 4 * cap);
   l.lists.kx = (uint32_t*)(l.lists.bst + 4 * cap);
   return l;
 }
 
 // End of an assign workgroup (after each wave stored its counts): exact
 // decisions of the queued keys, then the staged groups (and first-round |k|
-// bounds) of keys key0 .. key0 + 4 tpw 32 (those below n) and the moved-key
-// records, one global atomic per workgroup.
-template <bool FIRST>
+// bounds) of keys key0 .. key0 + 4 tpw 32 (those below n); without the fused
+// update also the moved-key records, one global atomic per workgroup.
+template <bool FIRST, bool FUSED>
 __device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh, int64_t key0, int tpw,
-                                                const uint16_t* Rs, const double* __restrict__ nrm_bh, int n, int N,
+                                                const uint16_t* Rs, const double* nrm_bh, int n, int N,
                                                 int32_t* __restrict__ belong_bh, float* __restrict__ knorm_bh,
                                                 int32_t* __restrict__ mcount_bh,
                                                 unsigned long long* __restrict__ mrec_bh, uint16_t* kslot_w,
@@ -518,7 +529,7 @@ __device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh
     belong_bh[key0 + x] = sh.bst[x];
     if (FIRST) knorm_bh[key0 + x] = __uint_as_float(sh.kx[x]);
   }
-  if (!FIRST) {
+  if (!FIRST && !FUSED) {
     const int* wc = sh.c->wcnt;
     const int nw = wc[0] + wc[1] + wc[2] + wc[3];
     const int nm = nw + sh.c->nx;
@@ -530,6 +541,266 @@ __device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh
       mrec_bh[base + x] = ((unsigned long long)(key0 + (e & 2047u)) << 32) | (((e >> 11) & 1023u) << 16) |
                           (e >> 21);
     }
+  }
+}
+
+// ------------------------------------------------------------------ exact sums (bf16)
+// With bf16 keys and values every fp64 member sum is exact: a member is a
+// multiple of 2^(e_min - 7) (8-bit significand, e_min the smallest member
+// exponent) and every partial sum, in any order, is below 2^(e_max + 1 +
+// log2 count), so all of them are representable in fp64's 53 bits whenever
+// (e_max - e_min) + log2 count <= 45, e.g. at most 2^15 members with nonzero
+// magnitudes within 2^30 of each other.  The order of summation then cannot
+// change a bit, and the bf16 path sums without a stable order.
+
+constexpr int kGsumU = 8;        // 8-row chunks per batch
+
+// One batch of a wave's run: entries of chunks ch0 .. ch0 + U - 1 (clamped
+// to the run's last chunk, so every lane loads) and their row fragments.
+template <int U>
+__device__ __forceinline__ void gsum_load(const uint32_t* ent, const uint16_t* __restrict__ Xb, int ch0, int ce,
+                                          int slot, int j, uint32_t (&e)[U], u32x4 (&w)[U]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    e[u] = ent[min(ch0 + u, ce - 1) * 8 + slot];
+    const uint32_t key = e[u] == 0xffffffffu ? 0u : (e[u] & 0x7fffffffu);
+    w[u] = *(const u32x4*)(Xb + (int64_t)key * 64 + 8 * j);
+  }
+}
+
+// x summed over the 8 lanes l ^ {0, 8, 16, ..., 56} (lane bits 3, 4, 5), in
+// every lane: DPP row rotation by 8 (lane ^ 8 within 16-lane rows), then the
+// 16- and 32-lane half swaps.
+__device__ __forceinline__ double sum_slots8(double x) {
+  const uint32_t lo = (uint32_t)__double2loint(x), hi = (uint32_t)__double2hiint(x);
+  x += __hiloint2double((int)__builtin_amdgcn_update_dpp(0u, hi, 0x128, 0xf, 0xf, false),
+                        (int)__builtin_amdgcn_update_dpp(0u, lo, 0x128, 0xf, 0xf, false));
+  {
+    const auto l16 = __builtin_amdgcn_permlane16_swap((uint32_t)__double2loint(x), (uint32_t)__double2loint(x), false,
+                                                      false);
+    const auto h16 = __builtin_amdgcn_permlane16_swap((uint32_t)__double2hiint(x), (uint32_t)__double2hiint(x), false,
+                                                      false);
+    x = __hiloint2double((int)h16[0], (int)l16[0]) + __hiloint2double((int)h16[1], (int)l16[1]);
+  }
+  const u32x2 l32 = halves((uint32_t)__double2loint(x)), h32 = halves((uint32_t)__double2hiint(x));
+  return __hiloint2double((int)h32[0], (int)l32[0]) + __hiloint2double((int)h32[1], (int)l32[1]);
+}
+
+// ------------------------------------------------------------------ partition sums (bf16, N <= 128)
+// The member sums of the bf16 path are exact in fp64 (see above), so they may
+// be split into per-workgroup partitions and added in any order.  In the first
+// round, after its decisions, assign workgroup p of slice bh (keys key0 ..
+// key0 + nk - 1) sorts its keys by group in LDS; each wave sums the rows of a
+// run of whole groups in fp64 registers (8 rows per instruction, 16 bytes per
+// lane) and stores each finished group's row into partition p of Sp, together
+// with the member counts and a bitmask of the groups with members.
+// k_part_finish then adds the partitions.  (Later rounds move few keys; there
+// a separate launch over the moved-key records is faster than lengthening
+// every assign workgroup by its share of the sums.)
+struct PartLds {
+  int ecnt[kFusedG], eoff[kFusedG + 1], ecur[kFusedG], wbeg[5], wg0[4];
+};
+
+__device__ __forceinline__ void partition_sums(const uint16_t* __restrict__ Kbh, int64_t key0, int nk, int N,
+                                               const AssignLists& sh, uint32_t* ent, int tw_words, PartLds& fl,
+                                               const FusedUpdate& fu) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t bh = blockIdx.y;
+  const int p = (int)blockIdx.x;
+  if (tid < kFusedG) fl.ecnt[tid] = 0;
+  __syncthreads();
+  for (int x = tid; x < nk; x += 256) atomicAdd(&fl.ecnt[sh.bst[x]], 1);
+  __syncthreads();
+  // layout (wave 0, groups 2 lane and 2 lane + 1): each group's keys padded
+  // to a multiple of 8; wave w takes the groups from the first one starting at
+  // or after w tot / 4
+  if (wave == 0) {
+    const int ga = 2 * lane, gb = ga + 1;
+    const int ca = fl.ecnt[ga], cb = fl.ecnt[gb];
+    const int pa = (ca + 7) & ~7, pb = (cb + 7) & ~7;
+    int incl = pa + pb;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(incl, off);
+      if (lane >= off) incl += y;
+    }
+    const int sa = incl - pa - pb, sb = sa + pa, tot = __shfl(incl, 63);
+    fl.eoff[ga] = sa;
+    fl.eoff[gb] = sb;
+    fl.ecur[ga] = sa;
+    fl.ecur[gb] = sb;
+    for (int k = ca; k < pa; ++k) ent[sa + k] = 0xffffffffu;
+    for (int k = cb; k < pb; ++k) ent[sb + k] = 0xffffffffu;
+    if (lane == 0) {
+      fl.eoff[kFusedG] = tot;
+      fl.wbeg[0] = 0;
+      fl.wbeg[4] = tot;
+      fl.wg0[0] = 0;
+    }
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const int thr = w * tot / 4;
+      // the starts grow with g: the groups starting before thr are a prefix
+      const int g = (int)__popcll(__ballot(sa < thr)) + (int)__popcll(__ballot(sb < thr));
+      const int gsa = __shfl(sa, (g >> 1) & 63), gsb = __shfl(sb, (g >> 1) & 63);
+      if (lane == 0) {
+        fl.wbeg[w] = g < kFusedG ? ((g & 1) ? gsb : gsa) : tot;
+        fl.wg0[w] = g;
+      }
+    }
+    const uint64_t t0 = __ballot(fl.ecnt[lane] > 0), t1 = __ballot(fl.ecnt[lane + 64] > 0);
+    if (lane < 4) fu.pbits[(bh * kFusedP + p) * 4 + lane] = (uint32_t)((lane < 2 ? t0 : t1) >> (32 * (lane & 1)));
+  }
+  __syncthreads();
+  for (int x = tid; x < nk; x += 256) ent[atomicAdd(&fl.ecur[sh.bst[x]], 1)] = (uint32_t)x;
+  if (tid < N) fu.cntp[(bh * kFusedP + p) * N + tid] = fl.ecnt[tid];
+  __syncthreads();
+  // per-wave register sums over runs of whole groups into partition p
+  const int slot = lane >> 3, j = lane & 7;
+  const int cb = fl.wbeg[wave] / 8, ce = fl.wbeg[wave + 1] / 8;
+  const uint16_t* Xb = Kbh + key0 * 64;
+  double* Spp = fu.Sp + (bh * kFusedP + p) * (int64_t)N * 64;
+  // per-wave [8 slots][64 features] transpose tile after the entry list: the
+  // 8 slot rows of a finished group are added by lane = feature and stored as
+  // one row
+  double* tw = (double*)(ent + tw_words) + wave * 512;
+  double a[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+  int g = fl.wg0[wave], gend = 0;  // current group and its end chunk
+  auto flush = [&]() {
+#pragma unroll
+    for (int k = 0; k < 8; k += 2) *(double2*)(tw + slot * 64 + 8 * j + k) = double2{a[k], a[k + 1]};
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    double v = tw[lane];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) v += tw[k * 64 + lane];
+    Spp[g * 64 + lane] = v;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int k = 0; k < 8; ++k) a[k] = 0.0;
+  };
+  auto add = [&](int ch0, const uint32_t (&e)[kGsumU], const u32x4 (&w)[kGsumU]) {
+#pragma unroll
+    for (int u = 0; u < kGsumU; ++u) {
+      const int ch = ch0 + u;
+      if (ch >= ce) break;
+      if (ch >= gend) {  // next non-empty group (uniform)
+        if (ch > cb) flush();
+        while (fl.eoff[g + 1] <= ch * 8) ++g;
+        gend = fl.eoff[g + 1] / 8;
+      }
+      const double sg = e[u] == 0xffffffffu ? 0.0 : 1.0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const uint32_t bits = (k & 1) ? (w[u][k >> 1] >> 16) : (w[u][k >> 1] & 0xffffu);
+        a[k] = fma(sg, (double)bf16_to_f32(bits), a[k]);
+      }
+    }
+  };
+  if (cb < ce) {
+    uint32_t eA[kGsumU], eB[kGsumU];
+    u32x4 wA[kGsumU], wB[kGsumU];
+    gsum_load(ent, Xb, cb, ce, slot, j, eA, wA);
+    for (int ch0 = cb; ch0 < ce; ch0 += 2 * kGsumU) {
+      gsum_load(ent, Xb, ch0 + kGsumU, ce, slot, j, eB, wB);
+      __builtin_amdgcn_sched_barrier(0);
+      add(ch0, eA, wA);
+      if (ch0 + kGsumU >= ce) break;
+      gsum_load(ent, Xb, ch0 + 2 * kGsumU, ce, slot, j, eA, wA);
+      __builtin_amdgcn_sched_barrier(0);
+      add(ch0 + kGsumU, eB, wB);
+    }
+    flush();
+  }
+}
+
+// k_part_finish: grid (ceil(N / 32), BH), 256 threads; after a first-round
+// assign launch with partition sums (P partitions per slice).  Workgroup x
+// finishes groups g0 = 32 x .. g0 + 31 of slice bh: S64 = the sum over the
+// partitions with members of the group, count = their member counts, C =
+// (float)(S / count) (an empty group keeps C), R = bf16(C), the canonical fp64
+// |r|^2 (fma chain over c = 0..63, one lane per group) and its split.  Thread
+// t adds features 2 (t % 32), +1 of groups g0 + t / 32 + 8 u; only the rows of
+// (partition, group) pairs with members are read, all at once.
+template <int P>
+__global__ __launch_bounds__(256) void k_part_finish(const double* __restrict__ Sp, const int32_t* __restrict__ cntp,
+                                                     const uint32_t* __restrict__ pbits, int N,
+                                                     double* __restrict__ S64, int32_t* __restrict__ count,
+                                                     float* __restrict__ C, uint16_t* __restrict__ R,
+                                                     double* __restrict__ nrm64, uint16_t* __restrict__ nsplit) {
+  __shared__ uint32_t tb[P];  // bit g - g0: partition q has members of group g
+  __shared__ int ctl[P][32];
+  __shared__ uint32_t rsh[32][33];  // R rows as bf16 pairs
+  const int tid = threadIdx.x;
+  const int64_t bh = blockIdx.y;
+  const int g0 = blockIdx.x * 32, ng = min(32, N - g0);
+  if (tid < P * 32) {
+    const int q = tid >> 5, g = tid & 31;
+    const int cv = cntp[(bh * kFusedP + q) * N + g0 + min(g, ng - 1)];
+    const uint32_t bw = pbits[(bh * kFusedP + q) * 4 + (g0 >> 5)];
+    ctl[q][g] = cv;
+    if (g == 0) tb[q] = bw;
+  }
+  const int c2 = tid & 31, gq = tid >> 5;
+  const int64_t row0 = bh * N;
+  double2 sacc[4];
+  int pcnt[4];
+  f32x2 cold[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int gc = g0 + min(gq + 8 * u, ng - 1);
+    sacc[u] = double2{0.0, 0.0};
+    pcnt[u] = 0;
+    cold[u] = *(const f32x2*)(C + (row0 + gc) * 64 + 2 * c2);
+  }
+  __syncthreads();
+  double2 v[4][P];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int g = gq + 8 * u, gc = g0 + min(g, ng - 1);
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      const bool hit = (tb[q] >> g) & 1u;
+      v[u][q] = hit ? *(const double2*)(Sp + ((bh * kFusedP + q) * N + gc) * 64 + 2 * c2) : double2{0.0, 0.0};
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int g = gq + 8 * u;
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      sacc[u].x += v[u][q].x;
+      sacc[u].y += v[u][q].y;
+      pcnt[u] += ((tb[q] >> g) & 1u) ? ctl[q][g] : 0;
+    }
+    if (g >= ng) continue;
+    const int64_t row = row0 + g0 + g;
+    *(double2*)(S64 + row * 64 + 2 * c2) = sacc[u];
+    if (c2 == 0) count[row] = pcnt[u];
+    f32x2 cf = cold[u];
+    if (pcnt[u] > 0) {
+      cf.x = (float)(sacc[u].x / (double)pcnt[u]);
+      cf.y = (float)(sacc[u].y / (double)pcnt[u]);
+      *(f32x2*)(C + row * 64 + 2 * c2) = cf;
+    }
+    const uint32_t rp = f32_to_bf16(cf.x) | (f32_to_bf16(cf.y) << 16);
+    *(uint32_t*)(R + row * 64 + 2 * c2) = rp;
+    rsh[g][c2] = rp;
+  }
+  __syncthreads();
+  if (tid < ng) {
+    double nrm = 0.0;
+#pragma unroll 8
+    for (int c = 0; c < 64; ++c) {
+      const uint32_t w = rsh[tid][c >> 1];
+      const double rc = (double)bf16_to_f32((c & 1) ? (w >> 16) : (w & 0xffffu));
+      nrm = fma(rc, rc, nrm);
+    }
+    nrm64[row0 + g0 + tid] = nrm;
+    write_nsplit(nrm, nsplit + (row0 + g0 + tid) * 8);
   }
 }
 
@@ -558,7 +829,7 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
     const uint16_t* __restrict__ K, const uint16_t* __restrict__ R, const uint16_t* __restrict__ nsplit,
     const double* __restrict__ nrm64, float* __restrict__ knorm, int32_t* __restrict__ belong,
     int32_t* __restrict__ mcount, unsigned long long* __restrict__ mrec, int n, int N, int tpw, float cm,
-    float cp) {
+    float cp, FusedUpdate) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ double red[4];
   __shared__ AssignCounts cnt;
@@ -567,7 +838,7 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
   const int64_t bh = blockIdx.y;
   if (tid == 0) cnt.nx = 0;
-  const AssignLds L = assign_lds_layout(smem, Npad, tpw, &cnt);
+  const AssignLds L = assign_lds_layout(smem, Npad, tpw, false, &cnt);
   const uint16_t* Rs = L.Rs;
   const uint16_t* Ns = L.Ns;
   const double nmax = stage_reps<0>(R + bh * (int64_t)N * 64, nsplit + bh * N * 8, nrm64 + bh * N, N, Npad, L.Rs,
@@ -667,8 +938,8 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
     cnt.wcnt[wv] = wn;
     cnt.ucnt[wv] = un;
   }
-  assign_epilogue<FIRST>(Kbh, key0, tpw, Rs, nrm64 + bh * N, n, N, belong_bh, knorm + bh * n, mcount + bh,
-                         mrec + bh * n, kslot[wave], L.lists);
+  assign_epilogue<FIRST, false>(Kbh, key0, tpw, Rs, nrm64 + bh * N, n, N, belong_bh, knorm + bh * n, mcount + bh,
+                                mrec + bh * n, kslot[wave], L.lists);
 }
 
 // Key fragments of tile `tile` of a slice, and in later rounds the keys' |k|
@@ -727,13 +998,14 @@ __device__ __forceinline__ void score_tile(const u32x4 (&af)[NB][4], const u32x4
 // re-decisions read the LDS copy.  The key fragments of the next tile are
 // loaded while the current one is scored (two register sets used in turn, no
 // copies; the last tile's prefetch repeats it).  Same grid, LDS layout,
-// scores, certification and outputs as k_assign_bf16.
-template <bool FIRST, int NB>
-__global__ __launch_bounds__(256) void k_assign_reg(
-    const uint16_t* __restrict__ K, const uint16_t* __restrict__ R, const uint16_t* __restrict__ nsplit,
-    const double* __restrict__ nrm64, float* __restrict__ knorm, int32_t* __restrict__ belong,
-    int32_t* __restrict__ mcount, unsigned long long* __restrict__ mrec, int n, int N, int tpw, float cm,
-    float cp) {
+// scores, certification and outputs as k_assign_bf16.  FUSED (first round
+// only): the workgroup also forms its partition sums of the round's centroid
+// update (partition_sums), at most kFusedP per slice.
+template <bool FIRST, int NB, bool FUSED>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_assign_reg(
+    const uint16_t* __restrict__ K, const uint16_t* R, const uint16_t* nsplit, const double* nrm64,
+    float* __restrict__ knorm, int32_t* __restrict__ belong, int32_t* __restrict__ mcount,
+    unsigned long long* __restrict__ mrec, int n, int N, int tpw, float cm, float cp, FusedUpdate fu) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ double red[4];
   __shared__ AssignCounts cnt;
@@ -742,7 +1014,7 @@ __global__ __launch_bounds__(256) void k_assign_reg(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
   const int64_t bh = blockIdx.y;
   if (tid == 0) cnt.nx = 0;
-  const AssignLds L = assign_lds_layout(smem, Npad, tpw, &cnt);
+  const AssignLds L = assign_lds_layout(smem, Npad, tpw, FUSED, &cnt);
   const int64_t key0 = (int64_t)blockIdx.x * 4 * tpw * 32;
   const int wv = __builtin_amdgcn_readfirstlane(wave);
   const int64_t tile0 = key0 / 32 + (int64_t)wv * tpw;
@@ -812,8 +1084,14 @@ __global__ __launch_bounds__(256) void k_assign_reg(
     cnt.wcnt[wv] = wn;
     cnt.ucnt[wv] = un;
   }
-  assign_epilogue<FIRST>(Kbh, key0, tpw, L.Rs, nrm64 + bh * N, n, N, belong + bh * n, knorm + bh * n, mcount + bh,
-                         mrec + bh * n, kslot[wave], L.lists);
+  assign_epilogue<FIRST, FUSED>(Kbh, key0, tpw, L.Rs, nrm64 + bh * N, n, N, belong + bh * n, knorm + bh * n,
+                                mcount + bh, mrec + bh * n, kslot[wave], L.lists);
+  if (FUSED) {
+    __shared__ PartLds pl;
+    const int nk = (int)min((int64_t)4 * tpw * 32, (int64_t)n - key0);
+    static_assert(FIRST || !FUSED, "partition sums are formed in the first round only");
+    partition_sums(Kbh, key0, nk, N, L.lists, (uint32_t*)smem, fused_words(Npad, 4 * tpw * 32), pl, fu);
+  }
 }
 
 // ------------------------------------------------------------------ assign (exact)
@@ -962,15 +1240,6 @@ __global__ __launch_bounds__(256) void k_segsum(const typename S::T* __restrict_
   }
 }
 
-// ------------------------------------------------------------------ exact sums (bf16)
-// With bf16 keys and values every fp64 member sum is exact: a member is a
-// multiple of 2^(e_min - 7) (8-bit significand, e_min the smallest member
-// exponent) and every partial sum, in any order, is below 2^(e_max + 1 +
-// log2 count), so all of them are representable in fp64's 53 bits whenever
-// (e_max - e_min) + log2 count <= 45, e.g. at most 2^15 members with nonzero
-// magnitudes within 2^30 of each other.  The order of summation then cannot
-// change a bit, and the bf16 path sums without a stable order.
-
 // ------------------------------------------------------------------ group sums (bf16)
 // The member sums of the bf16 path are exact in fp64 (see above), so they can
 // be accumulated in any order and split any way: no global bucketing.
@@ -998,38 +1267,6 @@ __global__ __launch_bounds__(256) void k_segsum(const typename S::T* __restrict_
 // 3. finish the owned groups.
 constexpr int kGsumG = 32;
 constexpr int kGsumList = 8448;  // entry capacity of the sorted chunk list
-constexpr int kGsumU = 8;        // 8-row chunks per batch
-
-// One batch of a wave's run: entries of chunks ch0 .. ch0 + kGsumU - 1 (clamped
-// to the run's last chunk, so every lane loads) and their row fragments.
-__device__ __forceinline__ void gsum_load(const uint32_t* ent, const uint16_t* __restrict__ Xb, int ch0, int ce,
-                                          int slot, int j, uint32_t (&e)[kGsumU], u32x4 (&w)[kGsumU]) {
-#pragma unroll
-  for (int u = 0; u < kGsumU; ++u) {
-    e[u] = ent[min(ch0 + u, ce - 1) * 8 + slot];
-    const uint32_t key = e[u] == 0xffffffffu ? 0u : (e[u] & 0x7fffffffu);
-    w[u] = *(const u32x4*)(Xb + (int64_t)key * 64 + 8 * j);
-  }
-}
-
-// x summed over the 8 lanes l ^ {0, 8, 16, ..., 56} (lane bits 3, 4, 5), in
-// every lane: DPP row rotation by 8 (lane ^ 8 within 16-lane rows), then the
-// 16- and 32-lane half swaps.
-__device__ __forceinline__ double sum_slots8(double x) {
-  const uint32_t lo = (uint32_t)__double2loint(x), hi = (uint32_t)__double2hiint(x);
-  x += __hiloint2double((int)__builtin_amdgcn_update_dpp(0u, hi, 0x128, 0xf, 0xf, false),
-                        (int)__builtin_amdgcn_update_dpp(0u, lo, 0x128, 0xf, 0xf, false));
-  {
-    const auto l16 = __builtin_amdgcn_permlane16_swap((uint32_t)__double2loint(x), (uint32_t)__double2loint(x), false,
-                                                      false);
-    const auto h16 = __builtin_amdgcn_permlane16_swap((uint32_t)__double2hiint(x), (uint32_t)__double2hiint(x), false,
-                                                      false);
-    x = __hiloint2double((int)h16[0], (int)l16[0]) + __hiloint2double((int)h16[1], (int)l16[1]);
-  }
-  const u32x2 l32 = halves((uint32_t)__double2loint(x)), h32 = halves((uint32_t)__double2hiint(x));
-  return __hiloint2double((int)h32[0], (int)l32[0]) + __hiloint2double((int)h32[1], (int)l32[1]);
-}
-
 template <int MODE>
 __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, const int32_t* __restrict__ belong,
                                               const unsigned long long* __restrict__ mrec,
@@ -1614,9 +1851,9 @@ __global__ __launch_bounds__(256) void k_attend_f32(const float* __restrict__ Q,
 
 constexpr size_t kAssignLdsMax = 160 * 1024 - 1024;  // dynamic LDS budget (static arrays use the rest)
 
-size_t assign_lds(int N, int tpw = 12) {
-  const int Npad = (N + 31) & ~31;
-  return (size_t)Npad * 128 + (size_t)Npad * 16 + (size_t)4 * tpw * 32 * 16;  // see assign_lds_layout
+size_t assign_lds(int N, int tpw = 12, bool fused = false) {  // see assign_lds_layout
+  const int Npad = (N + 31) & ~31, cap4 = 4 * tpw * 32;
+  return (size_t)assign_region_a(Npad, cap4, fused) + (size_t)3 * cap4 * 4;
 }
 size_t bucket_lds(int N) { return (size_t)16 * N * 8 + (size_t)2 * N * 4; }
 size_t attend_lds(int N) {
@@ -1709,6 +1946,10 @@ size_t workspace_layout(const Dims& d, Workspace* ws, void* base) {
   w.S64 = (double*)take(BH * N * 64 * 8);
   w.mcount = (int32_t*)take(2 * BH * 4);
   w.mrec = (unsigned long long*)take(BH * n * 8);
+  const int64_t fp = d.dtype == 1 && Npad <= kFusedG ? kFusedP : 0;  // fused-update partitions
+  w.Sp = (double*)take(BH * fp * N * 64 * 8);
+  w.cntp = (int32_t*)take(BH * fp * N * 4);
+  w.pbits = (uint32_t*)take(BH * fp * 4 * 4);
   if (ws) *ws = w;
   return off;
 }
@@ -1728,9 +1969,11 @@ hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C
 
 hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint16_t* nsplit,
                          const double* nrm64, float* knorm, int32_t* belong, int32_t* mcount,
-                         unsigned long long* mrec, bool first, hipStream_t st) {
+                         unsigned long long* mrec, bool first, const FusedUpdate& fu, int* parts_out,
+                         hipStream_t st) {
   TimedLaunch timed("assign", st);
   set_lds_limits();
+  *parts_out = 0;
   if (d.dtype == 1) {
     const int64_t tiles = (d.n + 31) / 32;
     const int Npad = (d.N + 31) & ~31;
@@ -1741,32 +1984,55 @@ hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint
     // < 2^(4 - 23) of its magnitude.
     const float cm = (float)(kD + 4) * 0x1p-23f * (1.0f + 0x1p-10f);
     const float cp = 0x1p-19f * (1.0f + 0x1p-10f);
-    // Npad <= 128: the register-resident kernel, one instantiation per block count
     using AssignFn = void (*)(const uint16_t*, const uint16_t*, const uint16_t*, const double*, float*, int32_t*,
-                              int32_t*, unsigned long long*, int, int, int, float, float);
-    AssignFn kern = first ? k_assign_bf16<true> : k_assign_bf16<false>;
-    switch (Npad >> 5) {
-      case 1: kern = first ? k_assign_reg<true, 1> : k_assign_reg<false, 1>; break;
-      case 2: kern = first ? k_assign_reg<true, 2> : k_assign_reg<false, 2>; break;
-      case 3: kern = first ? k_assign_reg<true, 3> : k_assign_reg<false, 3>; break;
-      case 4: kern = first ? k_assign_reg<true, 4> : k_assign_reg<false, 4>; break;
-      default: break;
-    }
+                              int32_t*, unsigned long long*, int, int, int, float, float, FusedUpdate);
+    // Npad <= 128: the register-resident kernel, one instantiation per block
+    // count; the first round also with the partition sums
+    static const AssignFn reg[3][4] = {
+        {k_assign_reg<false, 1, false>, k_assign_reg<false, 2, false>, k_assign_reg<false, 3, false>,
+         k_assign_reg<false, 4, false>},
+        {k_assign_reg<true, 1, false>, k_assign_reg<true, 2, false>, k_assign_reg<true, 3, false>,
+         k_assign_reg<true, 4, false>},
+        {k_assign_reg<true, 1, true>, k_assign_reg<true, 2, true>, k_assign_reg<true, 3, true>,
+         k_assign_reg<true, 4, true>}};
+    const bool small = Npad <= kFusedG;
+    AssignFn kern = small ? reg[first][(Npad >> 5) - 1] : (first ? k_assign_bf16<true> : k_assign_bf16<false>);
     // one round of resident workgroups, the same number per slice, at most 16
     // tiles per wave (the LDS lists grow with tpw; the occupancy is taken at 16)
     int64_t tpw = 16;
     while (tpw > 1 && assign_lds(d.N, (int)tpw) > kAssignLdsMax) --tpw;
     tpw = tiles_per_wave(tiles, d.BH, resident_wgs((const void*)kern, assign_lds(d.N, (int)tpw)), tpw);
-    const dim3 grid(cdiv(tiles, 4 * tpw), (unsigned)d.BH), block(256);
-    const size_t lds = assign_lds(d.N, (int)tpw);
+    const int64_t parts = cdiv(tiles, 4 * tpw);
+    const bool fused = first && small && parts <= kFusedP;
+    if (fused) {
+      kern = reg[2][(Npad >> 5) - 1];
+      *parts_out = (int)parts;
+    }
+    const dim3 grid((unsigned)parts, (unsigned)d.BH), block(256);
+    const size_t lds = assign_lds(d.N, (int)tpw, fused);
     hipLaunchKernelGGL(kern, grid, block, lds, st, (const uint16_t*)K, (const uint16_t*)R, nsplit, nrm64, knorm,
-                       belong, mcount, mrec, d.n, d.N, (int)tpw, cm, cp);
+                       belong, mcount, mrec, d.n, d.N, (int)tpw, cm, cp, fu);
   } else {
     const int kpw = 4;
     const dim3 grid(cdiv(d.n, 4 * kpw), (unsigned)d.BH), block(256);
     hipLaunchKernelGGL(k_assign_exact<F32>, grid, block, 0, st, (const float*)K, (const float*)R, nrm64,
                        belong, d.n, d.N, kpw);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_part_finish(const Dims& d, int parts, const FusedUpdate& fu, double* S64,
+                              int32_t* count, float* C, void* R, double* nrm64, uint16_t* nsplit,
+                              hipStream_t st) {
+  TimedLaunch timed("part_finish", st);
+  if (parts < 1 || parts > kFusedP || d.N > kFusedG) return hipErrorInvalidValue;
+  using FinishFn = void (*)(const double*, const int32_t*, const uint32_t*, int, double*, int32_t*, float*,
+                            uint16_t*, double*, uint16_t*);
+  static const FinishFn fns[kFusedP] = {k_part_finish<1>, k_part_finish<2>, k_part_finish<3>, k_part_finish<4>,
+                                        k_part_finish<5>, k_part_finish<6>, k_part_finish<7>, k_part_finish<8>};
+  const dim3 grid(cdiv(d.N, 32), (unsigned)d.BH), block(256);
+  hipLaunchKernelGGL(fns[parts - 1], grid, block, 0, st, fu.Sp, fu.cntp, fu.pbits, d.N, S64, count, C,
+                     (uint16_t*)R, nrm64, nsplit);
   return hipGetLastError();
 }
 

@@ -102,6 +102,7 @@ def test_workspace_bytes():
     b = L.ga_workspace_bytes(shape(n=200), 8)
     c = L.ga_workspace_bytes(shape(n=200), 64)
     assert 0 < a < b < c
-    # the metric workload's workspace stays modest next to 288 GB of HBM
+    # the metric workload's workspace (about 112 MB, half of it the fused
+    # update's per-partition sums) stays modest next to 288 GB of HBM
     big = L.ga_workspace_bytes(ga.Shape(16, 8, 8000, 64, ga.GA_BF16), 128)
-    assert big < 64 * 2**20
+    assert big < 256 * 2**20
