@@ -223,21 +223,24 @@ __device__ __forceinline__ int swz(int r, int c) { return r * 64 + 8 * (c ^ ((r 
 // (volatile), which keeps the 64 widened key values out of registers.
 __device__ int exact_argmin_lds(const uint16_t* kl, const uint16_t* Rs, const double* __restrict__ nrm, int N) {
   const int lane = threadIdx.x & 63;
+  u32x4 kw[8];  // the key row (the same LDS words in every lane), read once
+#pragma unroll
+  for (int i = 0; i < 8; ++i) kw[i] = *(const u32x4*)(kl + 8 * i);
   double best = INFINITY;
   int bj = 0x7fffffff;
   for (int j = lane; j < N; j += 64) {
+    const double nj = nrm[j];  // in flight during the dot product
     double dot = 0.0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const u32x4 kwi = *(const volatile u32x4*)(kl + 8 * i);
       const u32x4 rw = *(const u32x4*)(Rs + swz(j, i));
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        dot = fma((double)bf16_to_f32(kwi[e] & 0xffffu), (double)(-0.5f * bf16_to_f32(rw[e] & 0xffffu)), dot);
-        dot = fma((double)bf16_to_f32(kwi[e] >> 16), (double)(-0.5f * bf16_to_f32(rw[e] >> 16)), dot);
+        dot = fma((double)bf16_to_f32(kw[i][e] & 0xffffu), (double)(-0.5f * bf16_to_f32(rw[e] & 0xffffu)), dot);
+        dot = fma((double)bf16_to_f32(kw[i][e] >> 16), (double)(-0.5f * bf16_to_f32(rw[e] >> 16)), dot);
       }
     }
-    const double sc = fma(-2.0, dot, nrm[j]);
+    const double sc = fma(-2.0, dot, nj);
     if (sc < best) {
       best = sc;
       bj = j;
