@@ -45,7 +45,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRs = 72;       // LDS row stride (bf16 elements) of the 32x16 MFMA A tiles
 constexpr int kAssignDepth = 1;  // key tiles loaded ahead per wave in k_assign_reg
-constexpr int kAttDepth = 1;     // query tiles loaded ahead per wave in k_attend_bf16
+constexpr int kAttDepth = 2;     // query tiles loaded ahead per wave in k_attend_bf16
 constexpr int kOs = 72;          // LDS row stride (bf16) of the attention output tiles
 constexpr int kAttMaxN = 256; // groups held in LDS by the bf16 attention kernel
 
