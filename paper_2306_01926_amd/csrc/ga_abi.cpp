@@ -295,17 +295,13 @@ int ga_forward(ga_shape_t s, const void* Q, const void* K, const void* V, int32_
   int32_t* cnt = count ? count : w.count;
   float* C = centroid ? centroid : w.C;
   GA_TRY(run_cluster(d, K, iters, nullptr, a, cnt, C, w, st));
-  if (d.dtype == GA_BF16) {
-    GA_TRY(run_valuesum(d, V, a, nullptr, w.vsum, w, st));
+  if (s.dtype == GA_BF16) {
+    // the value sums go straight into the attention's transposed means and bias
+    GA_LAUNCH(ga::launch_valuesum_prep(d, V, a, cnt, scale, w.Vt, w.ginit, st), "value-sum launch");
+    GA_LAUNCH(ga::launch_attend(d, Q, w.R, w.Vt, w.ginit, C, cnt, w.vsum, scale, O, st), "attention launch");
   } else {
     // the last stable bucket pass sorted the keys by the final assignment: reuse it
     GA_LAUNCH(ga::launch_valuesum(d, V, w.perm, w.goff, cnt, w.vsum, st), "value-sum launch");
-  }
-  if (s.dtype == GA_BF16) {
-    GA_LAUNCH(ga::launch_attend_prep(d, C, cnt, w.vsum, scale, w.Rq, w.Vt, w.ginit, false, st),
-              "attention prep launch");
-    GA_LAUNCH(ga::launch_attend(d, Q, w.R, w.Vt, w.ginit, C, cnt, w.vsum, scale, O, st), "attention launch");
-  } else {
     GA_LAUNCH(ga::launch_attend(d, Q, nullptr, nullptr, nullptr, C, cnt, w.vsum, scale, O, st),
               "attention launch");
   }

@@ -85,6 +85,10 @@ hipError_t launch_gsum(const Dims& d, int mode, const void* X, const int32_t* be
                        const unsigned long long* mrec, const int32_t* mcount_cur, int32_t* mcount_next,
                        double* S64, int32_t* count, float* out, void* R, double* nrm64, uint16_t* nsplit,
                        hipStream_t st);
+// bf16 forward: value sums straight into the attention inputs (Vt, ginit), in
+// place of launch_gsum(mode 2) + launch_attend_prep
+hipError_t launch_valuesum_prep(const Dims& d, const void* V, const int32_t* belong, const int32_t* count,
+                                float scale, uint16_t* Vt, float* ginit, hipStream_t st);
 hipError_t launch_bucket(const Dims& d, const int32_t* belong, int32_t* perm, int32_t* goff,
                          int32_t* count, hipStream_t st);
 hipError_t launch_update(const Dims& d, const void* K, const int32_t* perm, const int32_t* goff,

@@ -1254,6 +1254,8 @@ __global__ __launch_bounds__(256) void k_segsum(const typename S::T* __restrict_
 //           records, count += joins - leaves (groups without either are left
 //           alone)
 //   MODE 2 (value sums):  vsum = (float) sum of the member value rows
+//   MODE 3 (value sums for the attention): the bf16 value means, transposed,
+//           and the log2(count) score bias, as k_attend_prep forms them
 // MODE 0/1 then set C = (float)(S / count) (an empty group keeps C), R =
 // bf16(C), the canonical fp64 |r|^2 (fma chain over c = 0..63, one lane per
 // group) and its split.
@@ -1277,7 +1279,8 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
                                               int32_t* __restrict__ mcount_next, int n, int N,
                                               double* __restrict__ S64, int32_t* __restrict__ count,
                                               float* __restrict__ out, uint16_t* __restrict__ R,
-                                              double* __restrict__ nrm64, uint16_t* __restrict__ nsplit) {
+                                              double* __restrict__ nrm64, uint16_t* __restrict__ nsplit,
+                                              float inv_sl2e, int vts) {
   __shared__ uint32_t ent[kGsumList];  // key | leave << 31; 0xffffffff pads a group to 8k entries
   __shared__ double acc[kGsumG * 64];  // [g][c] sums of this workgroup's groups
   __shared__ int ecnt[kGsumG], eoff[kGsumG + 1], ecur[kGsumG], dcnt[kGsumG], hit[kGsumG], wbeg[5], wg0[4];
@@ -1330,7 +1333,7 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
         const int g = side ? gl[u] : gj[u];
         if ((unsigned)g < (unsigned)ng) {
           atomicAdd(&ecnt[g], 1);
-          if (MODE != 2) atomicAdd(&dcnt[g], side ? -1 : 1);
+          if (MODE < 2) atomicAdd(&dcnt[g], side ? -1 : 1);
           hit[g] = 1;
         }
       }
@@ -1439,9 +1442,31 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
     const int idx = tid + 256 * u, g = idx >> 6, c = idx & 63;
     const int64_t row = bh * N + g0 + min(g, ng - 1);
     prev[u] = MODE == 1 ? S64[row * 64 + c] : 0.0;
-    pc[u] = MODE == 1 ? count[row] : 0;
+    pc[u] = MODE == 1 || MODE == 3 ? count[row] : 0;
   }
   __syncthreads();  // (total == 0: dcnt, hit, acc initialised above)
+  if (MODE == 3) {
+    // value means mu = (float) sum / count (0 for an empty or padded group)
+    // as bf16, transposed through LDS into Vt[feature][group] (R, 8-byte
+    // segments), and the score bias log2(count) / sl2e (-inf if empty) into
+    // out[bh][Npad]
+    uint16_t* mt = (uint16_t*)ent;  // [64][36]
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      const int idx = tid + 256 * u, g = idx >> 6, c = idx & 63;
+      const float vs = g < ng ? (float)acc[g * 64 + c] : 0.f;
+      const int cnt = g < ng ? pc[u] : 0;
+      mt[c * 36 + g] = (uint16_t)f32_to_bf16(cnt > 0 ? vs / (float)cnt : 0.f);
+      if (c == 0) out[bh * ((N + 31) & ~31) + g0 + g] = cnt > 0 ? log2f((float)cnt) * inv_sl2e : -INFINITY;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int x = tid + 256 * u, f = x >> 3, q4 = x & 7;  // 64 features x 8 segments of 4 groups
+      *(uint2*)(R + (bh * 64 + f) * (int64_t)vts + g0 + 4 * q4) = *(const uint2*)(mt + f * 36 + 4 * q4);
+    }
+    return;
+  }
 #pragma unroll
   for (int u = 0; u < EPT; ++u) {
     const int idx = tid + 256 * u, g = idx >> 6, c = idx & 63;
@@ -2059,13 +2084,29 @@ hipError_t launch_gsum(const Dims& d, int mode, const void* X, const int32_t* be
   uint16_t* Rb = (uint16_t*)R;
   if (mode == 0)
     hipLaunchKernelGGL(k_gsum<0>, grid, block, lds, st, Xb, belong, mrec, mcount_cur, mcount_next, d.n, d.N, S64,
-                       count, out, Rb, nrm64, nsplit);
+                       count, out, Rb, nrm64, nsplit, 0.f, 0);
   else if (mode == 1)
     hipLaunchKernelGGL(k_gsum<1>, grid, block, lds, st, Xb, belong, mrec, mcount_cur, mcount_next, d.n, d.N, S64,
-                       count, out, Rb, nrm64, nsplit);
+                       count, out, Rb, nrm64, nsplit, 0.f, 0);
   else
     hipLaunchKernelGGL(k_gsum<2>, grid, block, lds, st, Xb, belong, mrec, mcount_cur, mcount_next, d.n, d.N, S64,
-                       count, out, Rb, nrm64, nsplit);
+                       count, out, Rb, nrm64, nsplit, 0.f, 0);
+  return hipGetLastError();
+}
+
+static float clamp_sl2e(float scale) {
+  const float s = fabsf(scale) * 1.4426950408889634f;
+  return s < 1e-30f ? 1e-30f : s;
+}
+
+hipError_t launch_valuesum_prep(const Dims& d, const void* V, const int32_t* belong, const int32_t* count,
+                                float scale, uint16_t* Vt, float* ginit, hipStream_t st) {
+  TimedLaunch timed("valuesum", st);
+  if (d.dtype != 1) return hipErrorInvalidValue;
+  const dim3 grid(cdiv(d.N, kGsumG), (unsigned)d.BH), block(256);
+  hipLaunchKernelGGL(k_gsum<3>, grid, block, 0, st, (const uint16_t*)V, belong, (const unsigned long long*)nullptr,
+                     (const int32_t*)nullptr, (int32_t*)nullptr, d.n, d.N, (double*)nullptr, (int32_t*)count,
+                     ginit, Vt, (double*)nullptr, (uint16_t*)nullptr, 1.0f / clamp_sl2e(scale), vt_stride(d.N));
   return hipGetLastError();
 }
 
@@ -2096,10 +2137,6 @@ hipError_t launch_valuesum(const Dims& d, const void* V, const int32_t* perm, co
   return hipGetLastError();
 }
 
-static float clamp_sl2e(float scale) {
-  const float s = fabsf(scale) * 1.4426950408889634f;
-  return s < 1e-30f ? 1e-30f : s;
-}
 
 hipError_t launch_attend_prep(const Dims& d, const float* centroid, const int32_t* count,
                               const float* vsum, float scale, uint16_t* Rq, uint16_t* Vt, float* ginit,
