@@ -91,8 +91,10 @@ ga::Dims dims_of(const ga_shape_t& s, int32_t N) {
 // (fp32 sums need not be exact).
 int run_cluster(const ga::Dims& d, const void* K, int32_t iters, const float* init, int32_t* belong,
                 int32_t* count, float* C, const ga::Workspace& w, hipStream_t st) {
-  GA_LAUNCH(ga::launch_init(d, K, init, C, w.R, w.nrm64, w.nsplit, w.mcount, st), "init launch");
-  const ga::FusedUpdate fu{w.Sp, w.cntp, w.pbits};
+  // with the fused first round the assign launch forms the initial centroids itself
+  if (ga::fused_first_parts(d) == 0)
+    GA_LAUNCH(ga::launch_init(d, K, init, C, w.R, w.nrm64, w.nsplit, w.mcount, st), "init launch");
+  const ga::FusedUpdate fu{w.Sp, w.cntp, w.pbits, init, C};
   for (int t = 0; t < iters; ++t) {
     int32_t* mc_cur = w.mcount + (t & 1) * d.BH;
     int32_t* mc_next = w.mcount + ((t + 1) & 1) * d.BH;

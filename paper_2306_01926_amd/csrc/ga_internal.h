@@ -34,17 +34,19 @@ struct Workspace {
   uint32_t* pbits;   // [BH][kFusedP][4] groups with members in each partition (bit g)
 };
 
-// First-round centroid update of the bf16 path for N <= kFusedG: every assign
-// workgroup (one partition of a slice's keys, at most kFusedP per slice) sums
-// the rows of its keys per group into its own partition of Sp;
-// launch_part_finish adds the partitions into S64 and forms count, C, R,
-// |r|^2 and the split.
+// First round of the bf16 path for N <= kFusedG: every assign workgroup (one
+// partition of a slice's keys, at most kFusedP per slice) forms the initial
+// representatives itself (no init launch), then sums the rows of its keys per
+// group into its own partition of Sp; launch_part_finish adds the partitions
+// into S64 and forms count, C, R, |r|^2 and the split.
 constexpr int kFusedG = 128;
 constexpr int kFusedP = 8;
 struct FusedUpdate {
   double* Sp;
   int32_t* cntp;
   uint32_t* pbits;
+  const float* init;  // [BH][N][64] given initial centroids, or null (strided keys)
+  float* C;           // [BH][N][64] receives the initial centroids
 };
 
 struct Dims {
@@ -69,6 +71,9 @@ size_t workspace_layout(const Dims& d, Workspace* ws, void* base);  // returns b
 
 hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C, void* R,
                        double* nrm64, uint16_t* nsplit, int32_t* mcount, hipStream_t st);
+// Partitions per slice of the first round's fused assign launch (which then
+// also does the init), 0 if that launch is not used for d.
+int fused_first_parts(const Dims& d);
 // First round, bf16, N <= kFusedG and at most kFusedP workgroups per slice:
 // the assign launch also writes the partition sums of the round's update (fu)
 // and *parts is their number per slice, to be finished by launch_part_finish;

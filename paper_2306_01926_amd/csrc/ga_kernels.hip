@@ -473,6 +473,83 @@ __device__ __forceinline__ double stage_reps(const uint16_t* __restrict__ Rbh, c
   return fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
 }
 
+// First round with partition sums: the initial representatives straight from
+// the keys (C_j = k_{floor(j n / N)}, R = C) or from a given init (C_j =
+// init_j, R = bf16(C)), staged like stage_reps, without a separate init
+// launch.  The canonical |r|^2 (fma chain over c = 0..63, one thread per
+// group) goes to nrm_l and its split to Ns; C_bh, if given, receives C.  Ends
+// with a barrier; returns the slice's largest |r|^2.
+template <int NPAD>
+__device__ __forceinline__ double stage_init(const uint16_t* __restrict__ Kbh, const float* __restrict__ init_bh,
+                                             int n, int N, float* __restrict__ C_bh, uint16_t* Rs, uint16_t* Ns,
+                                             double* nrm_l, double* red) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int IT = NPAD * 8 / 256;
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int idx = tid + it * 256, row = idx >> 3, ch = idx & 7;
+    u32x4 r = {0u, 0u, 0u, 0u};
+    if (row < N) {
+      float c[8];
+      if (init_bh) {
+        const float4 a = *(const float4*)(init_bh + row * 64 + ch * 8);
+        const float4 b = *(const float4*)(init_bh + row * 64 + ch * 8 + 4);
+        c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w; c[4] = b.x; c[5] = b.y; c[6] = b.z; c[7] = b.w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r[e] = f32_to_bf16(c[2 * e]) | (f32_to_bf16(c[2 * e + 1]) << 16);
+      } else {
+        r = *(const u32x4*)(Kbh + ((int64_t)row * n / N) * 64 + ch * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          c[2 * e] = bf16_to_f32(r[e] & 0xffffu);
+          c[2 * e + 1] = bf16_to_f32(r[e] >> 16);
+        }
+      }
+      if (C_bh) {
+        *(float4*)(C_bh + row * 64 + ch * 8) = float4{c[0], c[1], c[2], c[3]};
+        *(float4*)(C_bh + row * 64 + ch * 8 + 4) = float4{c[4], c[5], c[6], c[7]};
+      }
+    }
+    u32x4 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t lo = __float_as_uint(bf16_to_f32(r[e] & 0xffffu) * -2.0f) >> 16;
+      const uint32_t hi = __float_as_uint(bf16_to_f32(r[e] >> 16) * -2.0f) >> 16;
+      v[e] = lo | (hi << 16);
+    }
+    *(u32x4*)(Rs + swz(row, ch)) = v;
+  }
+  __syncthreads();
+  double mx = 0.0;
+  if (tid < NPAD) {
+    const int j = tid;
+    double nrm = 0.0;
+    if (j < N) {
+#pragma unroll
+      for (int ch = 0; ch < 8; ++ch) {
+        const u32x4 v = *(const u32x4*)(Rs + swz(j, ch));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const double lo = (double)(-0.5f * bf16_to_f32(v[e] & 0xffffu));
+          const double hi = (double)(-0.5f * bf16_to_f32(v[e] >> 16));
+          nrm = fma(lo, lo, nrm);
+          nrm = fma(hi, hi, nrm);
+        }
+      }
+      write_nsplit(nrm, Ns + j * 8);
+      mx = nrm;
+    } else {
+      *(u32x4*)(Ns + j * 8) = u32x4{0x7f7fu, 0u, 0u, 0u};
+    }
+    nrm_l[j] = nrm;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  return fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+}
+
 // Dynamic LDS of the assign kernels: region A = -2R as [Npad][64] bf16
 // (swizzled), the |r|^2 split as [Npad][8] bf16 and the uncertain queue
 // (4 tpw 32 words), then three arrays of 4 tpw 32 words: moved records, staged
@@ -1039,8 +1116,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
   for (int r = 0; r < D; ++r)
     load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(r, tcount - 1), n, q, h, kb[r], knb[r], oldb[r]);
-  const double nmax = stage_reps<Npad>(R + bh * (int64_t)N * 64, nsplit + bh * N * 8, nrm64 + bh * N, N, Npad, L.Rs,
-                                       L.Ns, red);
+  // FUSED (first round): the initial representatives from the keys or the
+  // given init; workgroup 0 of the slice writes C and clears the moved-key
+  // counters of the next rounds
+  __shared__ double nrm_l[FUSED ? Npad : 1];
+  if (FUSED && blockIdx.x == 0 && tid == 0) {
+    mcount[bh] = 0;
+    mcount[gridDim.y + bh] = 0;
+  }
+  const double nmax =
+      FUSED ? stage_init<Npad>(Kbh, fu.init ? fu.init + bh * (int64_t)N * 64 : nullptr, n, N,
+                               blockIdx.x == 0 ? fu.C + bh * (int64_t)N * 64 : nullptr, L.Rs, L.Ns, nrm_l, red)
+            : stage_reps<Npad>(R + bh * (int64_t)N * 64, nsplit + bh * N * 8, nrm64 + bh * N, N, Npad, L.Rs, L.Ns,
+                               red);
+  const double* nrm_x = FUSED ? (const double*)nrm_l : nrm64 + bh * N;  // |r|^2 for the exact decisions
   const float nmaxf = (float)nmax * (1.0f + 0x1p-20f);
   const float rmaxf = sqrtf(nmaxf) * (1.0f + 0x1p-20f);
   const Certify cf = {nmaxf, rmaxf, cm, cp};
@@ -1087,7 +1176,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     cnt.wcnt[wv] = wn;
     cnt.ucnt[wv] = un;
   }
-  assign_epilogue<FIRST, FUSED>(Kbh, key0, tpw, L.Rs, nrm64 + bh * N, n, N, belong + bh * n, knorm + bh * n,
+  assign_epilogue<FIRST, FUSED>(Kbh, key0, tpw, L.Rs, nrm_x, n, N, belong + bh * n, knorm + bh * n,
                                 mcount + bh, mrec + bh * n, kslot[wave], L.lists);
   if (FUSED) {
     __shared__ PartLds pl;
@@ -1995,6 +2084,47 @@ hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C
   return hipGetLastError();
 }
 
+using AssignFn = void (*)(const uint16_t*, const uint16_t*, const uint16_t*, const double*, float*, int32_t*,
+                          int32_t*, unsigned long long*, int, int, int, float, float, FusedUpdate);
+struct AssignPlan {
+  AssignFn kern;
+  int64_t tpw, parts;
+  bool fused;
+};
+
+// bf16 kernel choice and grid: one round of resident workgroups, the same
+// number per slice, at most 16 tiles per wave (the LDS lists grow with tpw;
+// the occupancy is taken at 16).
+static AssignPlan plan_assign(const Dims& d, bool first) {
+  const int64_t tiles = (d.n + 31) / 32;
+  const int Npad = (d.N + 31) & ~31;
+  // Npad <= 128: the register-resident kernel, one instantiation per block
+  // count; the first round also with the partition sums
+  static const AssignFn reg[3][4] = {
+      {k_assign_reg<false, 1, false>, k_assign_reg<false, 2, false>, k_assign_reg<false, 3, false>,
+       k_assign_reg<false, 4, false>},
+      {k_assign_reg<true, 1, false>, k_assign_reg<true, 2, false>, k_assign_reg<true, 3, false>,
+       k_assign_reg<true, 4, false>},
+      {k_assign_reg<true, 1, true>, k_assign_reg<true, 2, true>, k_assign_reg<true, 3, true>,
+       k_assign_reg<true, 4, true>}};
+  const bool small = Npad <= kFusedG;
+  AssignPlan p;
+  p.kern = small ? reg[first][(Npad >> 5) - 1] : (first ? k_assign_bf16<true> : k_assign_bf16<false>);
+  int64_t tpw = 16;
+  while (tpw > 1 && assign_lds(d.N, (int)tpw) > kAssignLdsMax) --tpw;
+  p.tpw = tiles_per_wave(tiles, d.BH, resident_wgs((const void*)p.kern, assign_lds(d.N, (int)tpw)), tpw);
+  p.parts = cdiv(tiles, 4 * p.tpw);
+  p.fused = first && small && p.parts <= kFusedP;
+  if (p.fused) p.kern = reg[2][(Npad >> 5) - 1];
+  return p;
+}
+
+int fused_first_parts(const Dims& d) {
+  if (d.dtype != 1) return 0;
+  const AssignPlan p = plan_assign(d, true);
+  return p.fused ? (int)p.parts : 0;
+}
+
 hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint16_t* nsplit,
                          const double* nrm64, float* knorm, int32_t* belong, int32_t* mcount,
                          unsigned long long* mrec, bool first, const FusedUpdate& fu, int* parts_out,
@@ -2003,8 +2133,6 @@ hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint
   set_lds_limits();
   *parts_out = 0;
   if (d.dtype == 1) {
-    const int64_t tiles = (d.n + 31) / 32;
-    const int Npad = (d.N + 31) & ~31;
     // |MFMA fp32 accumulation error| <= (d + 4) 2^-24 * 2 * sum|terms| (each of the
     // d products and the three |r|^2 terms added with at most one rounding,
     // sequential model, 2x margin; the split itself is within 2^-24 |r|^2);
@@ -2012,34 +2140,12 @@ hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint
     // < 2^(4 - 23) of its magnitude.
     const float cm = (float)(kD + 4) * 0x1p-23f * (1.0f + 0x1p-10f);
     const float cp = 0x1p-19f * (1.0f + 0x1p-10f);
-    using AssignFn = void (*)(const uint16_t*, const uint16_t*, const uint16_t*, const double*, float*, int32_t*,
-                              int32_t*, unsigned long long*, int, int, int, float, float, FusedUpdate);
-    // Npad <= 128: the register-resident kernel, one instantiation per block
-    // count; the first round also with the partition sums
-    static const AssignFn reg[3][4] = {
-        {k_assign_reg<false, 1, false>, k_assign_reg<false, 2, false>, k_assign_reg<false, 3, false>,
-         k_assign_reg<false, 4, false>},
-        {k_assign_reg<true, 1, false>, k_assign_reg<true, 2, false>, k_assign_reg<true, 3, false>,
-         k_assign_reg<true, 4, false>},
-        {k_assign_reg<true, 1, true>, k_assign_reg<true, 2, true>, k_assign_reg<true, 3, true>,
-         k_assign_reg<true, 4, true>}};
-    const bool small = Npad <= kFusedG;
-    AssignFn kern = small ? reg[first][(Npad >> 5) - 1] : (first ? k_assign_bf16<true> : k_assign_bf16<false>);
-    // one round of resident workgroups, the same number per slice, at most 16
-    // tiles per wave (the LDS lists grow with tpw; the occupancy is taken at 16)
-    int64_t tpw = 16;
-    while (tpw > 1 && assign_lds(d.N, (int)tpw) > kAssignLdsMax) --tpw;
-    tpw = tiles_per_wave(tiles, d.BH, resident_wgs((const void*)kern, assign_lds(d.N, (int)tpw)), tpw);
-    const int64_t parts = cdiv(tiles, 4 * tpw);
-    const bool fused = first && small && parts <= kFusedP;
-    if (fused) {
-      kern = reg[2][(Npad >> 5) - 1];
-      *parts_out = (int)parts;
-    }
-    const dim3 grid((unsigned)parts, (unsigned)d.BH), block(256);
-    const size_t lds = assign_lds(d.N, (int)tpw, fused);
-    hipLaunchKernelGGL(kern, grid, block, lds, st, (const uint16_t*)K, (const uint16_t*)R, nsplit, nrm64, knorm,
-                       belong, mcount, mrec, d.n, d.N, (int)tpw, cm, cp, fu);
+    const AssignPlan p = plan_assign(d, first);
+    if (p.fused) *parts_out = (int)p.parts;
+    const dim3 grid((unsigned)p.parts, (unsigned)d.BH), block(256);
+    const size_t lds = assign_lds(d.N, (int)p.tpw, p.fused);
+    hipLaunchKernelGGL(p.kern, grid, block, lds, st, (const uint16_t*)K, (const uint16_t*)R, nsplit, nrm64, knorm,
+                       belong, mcount, mrec, d.n, d.N, (int)p.tpw, cm, cp, fu);
   } else {
     const int kpw = 4;
     const dim3 grid(cdiv(d.n, 4 * kpw), (unsigned)d.BH), block(256);
