@@ -25,12 +25,15 @@ METRIC = "group-attention queries/sec (B·H·n) at n=8000,N=128; % HBM roofline"
 def kernel_work(name, w, N, BH):
     """(bound, algorithmic work per launch, unit, peak) of each kernel, or None.
 
-    assign:    per key its row of K, |k| bound and previous group (read) and
-               its group (written): d*es + 12 bytes (the first round writes the
-               bound instead of reading bound and group: d*es + 8).  Its
+    assign:    the later rounds: per key its row of K, |k| bound and previous
+               group (read) and its group (written): d*es + 12 bytes.  Its
                arithmetic intensity, 2 N d flop per d*es + 12 bytes (~117
                flop/B at N = 128), is below MI355X's ridge (2.5 PF / 8 TB/s =
                312 flop/B), so the roofline that bounds it is HBM.
+    assign_first: the first round (scores, the initial centroids and, for
+               N <= 128, the partition sums of the update in one launch): per
+               key its row of K (read once in the algorithm) and its |k| bound
+               and group (written): d*es + 8 bytes.
     attend:    Q read + O write, 2 n d storage elements per slice (4 N d flop
                per query is below the ridge too).
     sums_full, valuesum: one pass over K (or V) and the groups, n (d*es + 4).
@@ -38,8 +41,9 @@ def kernel_work(name, w, N, BH):
     es = 2 if w.dtype == "bf16" else 4
     n, d = w.n, w.d
     if name == "assign":
-        per_key = (d * es + 8 + 9 * (d * es + 12)) / 10.0  # mean over the first and the later rounds
-        return "hbm", per_key * n * BH / 1e9, "GB/s", HBM_PEAK_GBS
+        return "hbm", (d * es + 12) * n * BH / 1e9, "GB/s", HBM_PEAK_GBS
+    if name == "assign_first":
+        return "hbm", (d * es + 8) * n * BH / 1e9, "GB/s", HBM_PEAK_GBS
     if name == "attend":
         return "hbm", 2.0 * n * d * es * BH / 1e9, "GB/s", HBM_PEAK_GBS
     if name in ("sums_full", "valuesum", "update"):

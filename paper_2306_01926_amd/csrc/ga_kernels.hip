@@ -2129,7 +2129,7 @@ hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint
                          const double* nrm64, float* knorm, int32_t* belong, int32_t* mcount,
                          unsigned long long* mrec, bool first, const FusedUpdate& fu, int* parts_out,
                          hipStream_t st) {
-  TimedLaunch timed("assign", st);
+  TimedLaunch timed(first ? "assign_first" : "assign", st);
   set_lds_limits();
   *parts_out = 0;
   if (d.dtype == 1) {
