@@ -70,7 +70,10 @@ typedef struct {
 } ga_shape_t;
 
 /* Bytes of device workspace any entry point needs for shape s and N groups
- * (0 if the shape is invalid).  One workspace of this size serves all calls. */
+ * (0 if the shape is invalid).  One workspace of this size serves all calls
+ * made one after another; calls that may run at the same time (on different
+ * streams) each need a workspace of their own: the workspace carries state
+ * between the launches of one call. */
 size_t ga_workspace_bytes(ga_shape_t s, int32_t N);
 
 /*

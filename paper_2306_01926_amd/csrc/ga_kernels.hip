@@ -615,8 +615,10 @@ __device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh
     const int nm = nw + sh.c->nx;
     if (tid == 0) sh.c->moved_base = nm ? atomicAdd(mcount_bh, nm) : 0;
     __syncthreads();
+    // a slice records at most n moved keys in a round; the bound only guards
+    // against a counter that was not cleared (a corrupted workspace)
     const int base = sh.c->moved_base;
-    for (int x = tid; x < nm; x += 256) {
+    for (int x = tid; x < nm && (int64_t)base + x < n; x += 256) {
       const uint32_t e = x < nw ? region_entry(sh.wrec, sh.cap, wc, x) : sh.kx[x - nw];
       mrec_bh[base + x] = ((unsigned long long)(key0 + (e & 2047u)) << 32) | (((e >> 11) & 1023u) << 16) |
                           (e >> 21);
@@ -1383,7 +1385,9 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
     hit[tid] = 0;
   }
 
-  const int64_t total = MODE == 1 ? (int64_t)mcount_cur[bh] : (int64_t)n;
+  // (a slice records at most n moved keys; the clamp keeps the loads below in
+  // bounds even if the workspace was corrupted, e.g. shared by overlapping calls)
+  const int64_t total = MODE == 1 ? min((int64_t)mcount_cur[bh], (int64_t)n) : (int64_t)n;
   // entries per chunk: at most 2 per record (join, leave) plus 7 padding per group
   constexpr int CH = MODE == 1 ? 4096 : 8192;
   constexpr int PER = CH / 256;
@@ -1397,7 +1401,7 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
       const int64_t e = c0 + tid + 256 * u, ec = min(e, total - 1);
       if (MODE == 1) {
         const unsigned long long r = mrec[bh * n + ec];
-        kv[u] = (int)(r >> 32);
+        kv[u] = min((int)(r >> 32) & 0x7fffffff, n - 1);
         gj[u] = (int)(r & 0xffffu) - g0;
         gl[u] = (int)((r >> 16) & 0xffffu) - g0;
       } else {

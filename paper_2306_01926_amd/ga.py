@@ -107,7 +107,12 @@ def workspace_bytes(shape: Shape, N: int) -> int:
 
 
 def workspace(shape: Shape, N: int, device) -> tuple:
-    """A cached device workspace (uint8 tensor) large enough for (shape, N)."""
+    """A cached device workspace (uint8 tensor) large enough for (shape, N).
+
+    One buffer per device, shared by every call that does not pass ws: calls
+    that may overlap (on different streams) must each pass a workspace of
+    their own (torch.empty(workspace_bytes(shape, N), dtype=torch.uint8)).
+    """
     nbytes = max(workspace_bytes(shape, N), 256)
     key = torch.device(device)
     ws = _ws_cache.get(key)
