@@ -5,22 +5,26 @@
 // contraction K R^T.  Aggregation and group softmax: Section 4.2, Eq. 3,
 // Algorithm 1.
 //
-// Kernels, in the order the forward runs them:
-//   k_init          C0_j = k_{floor(j n / N)} (or a given init); R = round(C);
-//                   canonical fp64 |r_j|^2
-//   k_assign_bf16   MFMA 32x32x16 bf16 scores |r_j|^2 - 2 k.r_j with an
-//                   in-register top-2 per key; keys whose top-2 gap is inside
-//                   a rigorous error band are re-decided with the exact fp64
-//                   definition (k_assign_exact's routine)
-//   k_assign_exact  fp64 fma-chain scores for every (key, group) (fp32 data)
-//   k_bucket        stable counting sort of keys by group (one workgroup per
-//                   slice): counts, group offsets, permutation
-//   k_segsum        one wave per group sums its members' rows in ascending key
-//                   order in fp64 (lane = feature): centroid update or value sums
-//   k_attend_prep   bf16 representatives, per-group value means (transposed)
-//                   and the log2(count) score bias
-//   k_attend_bf16   MFMA scores, block-wise online group softmax, MFMA combine
-//   k_attend_f32    the same in fp32 VALU (one thread per query)
+// Kernels, in the order the forward runs them (bf16, N <= 128):
+//   k_assign_reg<true, NB, true>   first round: initial centroids C0_j =
+//                   k_{floor(j n / N)} (or a given init), R = round(C), the
+//                   canonical fp64 |r_j|^2; MFMA 32x32x16 bf16 scores
+//                   |r_j|^2 - 2 k.r_j with an in-register top-2 per key; keys
+//                   whose top-2 gap is inside a rigorous error band are
+//                   re-decided with the exact fp64 definition; then the
+//                   workgroup's fp64 partition of the group sums
+//   k_part_finish   adds the partitions: counts, C, R, |r|^2
+//   k_assign_reg<false, NB, false> + k_gsum<1>   each later round: the same
+//                   assignment, then the member sums of the groups changed by
+//                   the moved keys only
+//   k_gsum<3>       value sums, written as the attention's bf16 value means
+//                   (transposed) and log2(count) score bias
+//   k_attend_bf16   MFMA scores, block-wise group softmax, MFMA combine
+// Also: k_init, k_assign_bf16 (N <= 1024), k_gsum<0> (first-round sums
+// without partitions), k_gsum<2> (value sums), k_attend_prep; the fp32 path
+// k_assign_exact (fp64 fma-chain scores for every (key, group)), k_bucket
+// (stable counting sort of keys by group), k_segsum (one wave per group sums
+// its members in ascending key order in fp64) and k_attend_f32.
 #include <hip/hip_runtime.h>
 
 #include <float.h>
