@@ -1685,38 +1685,11 @@ __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict_
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
   uint16_t* Ow = (uint16_t*)(gi + Npad) + wave * 32 * kOs;  // this wave's output tile
   const int64_t bh = blockIdx.y;
-  const uint16_t* Rbh = R + bh * (int64_t)N * 64;
-  for (int idx = tid; idx < Npad * 8; idx += 256) {
-    const int row = idx >> 3, ch = idx & 7;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (row < N) {
-      v = *(const u32x4*)(Rbh + (int64_t)row * 64 + ch * 8);
-      v ^= u32x4{rsign, rsign, rsign, rsign};
-    }
-    *(u32x4*)(Rs + row * kRs + ch * 8) = v;
-  }
-  const uint16_t* Vbh = Vt + bh * 64 * (int64_t)vts;
-  // rows of Vt are 8-byte aligned (vts = 128k + 4 keeps the combine's LDS reads conflict-free)
-  for (int idx = tid; idx < 64 * (Npad / 4); idx += 256) {
-    const int row = idx / (Npad / 4), ch = idx % (Npad / 4);
-    *(u32x2*)(Vs + row * vts + ch * 4) = *(const u32x2*)(Vbh + (int64_t)row * vts + ch * 4);
-  }
-  bool nonempty = false;
-  for (int j = tid; j < Npad; j += 256) {
-    const float x = ginit[bh * Npad + j];
-    gi[j] = x;
-    nonempty |= (x != -INFINITY);
-  }
-  const int any = __syncthreads_or(nonempty);
-
   const int64_t tile0 = ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(wave)) * tpw;
   const int64_t ntiles = ((int64_t)n + 31) / 32;
   const int tcount = (int)max((int64_t)0, min((int64_t)tpw, ntiles - tile0));
   const uint16_t* Qbh = Q + bh * (int64_t)n * 64;
   uint16_t* Obh = O + bh * (int64_t)n * 64;
-  // A operand of the denominator tile: row 0 (lane 0 and its h = 1 partner) all ones
-  const u32x4 ones_row = q == 0 ? u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u} : u32x4{0u, 0u, 0u, 0u};
-
   // Query tile t in row-major order: lane l holds 16 bytes (chunk l % 8) of
   // rows l / 8 + 8 k, so each load instruction reads 8 whole 128-byte rows.
   auto qload = [&](int t, u32x4 (&qc)[4]) __attribute__((always_inline)) {
@@ -1726,6 +1699,47 @@ __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict_
       qc[k] = *(const u32x4*)(Qbh + qi * 64 + (lane & 7) * 8);
     }
   };
+  // The first query tiles (see the ring below) load while the workgroup
+  // stages R, the value means and the bias; every staging load is issued
+  // (rows clamped into the slice) before any of them is stored.
+  constexpr int D = kAttDepth;
+  u32x4 qb[D + 1][4];
+#pragma unroll
+  for (int r = 0; r < D; ++r) qload(min(r, max(tcount - 1, 0)), qb[r]);
+  const uint16_t* Rbh = R + bh * (int64_t)N * 64;
+  const uint16_t* Vbh = Vt + bh * 64 * (int64_t)vts;
+  constexpr int RIT = Npad * 8 / 256, VIT = 64 * (Npad / 4) / 256;
+  u32x4 rv[RIT];
+  u32x2 vv[VIT];
+#pragma unroll
+  for (int it = 0; it < RIT; ++it) {
+    const int idx = tid + 256 * it, row = idx >> 3, ch = idx & 7;
+    rv[it] = *(const u32x4*)(Rbh + (int64_t)min(row, N - 1) * 64 + ch * 8);
+  }
+  // rows of Vt are 8-byte aligned (vts = 128k + 4 keeps the combine's LDS reads conflict-free)
+#pragma unroll
+  for (int it = 0; it < VIT; ++it) {
+    const int idx = tid + 256 * it, row = idx / (Npad / 4), ch = idx % (Npad / 4);
+    vv[it] = *(const u32x2*)(Vbh + (int64_t)row * vts + ch * 4);
+  }
+  const float gx = tid < Npad ? ginit[bh * Npad + tid] : -INFINITY;
+#pragma unroll
+  for (int it = 0; it < RIT; ++it) {
+    const int idx = tid + 256 * it, row = idx >> 3, ch = idx & 7;
+    const u32x4 v = row < N ? rv[it] ^ u32x4{rsign, rsign, rsign, rsign} : u32x4{0u, 0u, 0u, 0u};
+    *(u32x4*)(Rs + row * kRs + ch * 8) = v;
+  }
+#pragma unroll
+  for (int it = 0; it < VIT; ++it) {
+    const int idx = tid + 256 * it, row = idx / (Npad / 4), ch = idx % (Npad / 4);
+    *(u32x2*)(Vs + row * vts + ch * 4) = vv[it];
+  }
+  if (tid < Npad) gi[tid] = gx;
+  const int any = __syncthreads_or(gx != -INFINITY);
+
+  // A operand of the denominator tile: row 0 (lane 0 and its h = 1 partner) all ones
+  const u32x4 ones_row = q == 0 ? u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u} : u32x4{0u, 0u, 0u, 0u};
+
   auto run = [&](int t, const u32x4 (&qc)[4]) __attribute__((always_inline)) {
     // to MFMA B fragments through the wave's LDS tile: lane (h, q) takes
     // features 32 h + 8 s .. +7 of query q at k-step s
@@ -1895,10 +1909,6 @@ __global__ __launch_bounds__(256) void k_attend_bf16(const uint16_t* __restrict_
   // Ring of kAttDepth + 1 register sets: tile t + kAttDepth is loaded while
   // tile t is processed.  Loads past the last tile repeat it.  The scheduling
   // barriers keep each prefetch ahead of the tile it overlaps.
-  constexpr int D = kAttDepth;
-  u32x4 qb[D + 1][4];
-#pragma unroll
-  for (int r = 0; r < D; ++r) qload(min(r, tcount - 1), qb[r]);
   for (int t0 = 0; t0 < tcount; t0 += D + 1) {
 #pragma unroll
     for (int r = 0; r <= D; ++r) {
