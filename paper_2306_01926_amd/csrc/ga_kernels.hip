@@ -1378,6 +1378,7 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
                                               float inv_sl2e, int vts) {
   __shared__ uint32_t ent[kGsumList];  // key | leave << 31; 0xffffffff pads a group to 8k entries
   __shared__ double acc[kGsumG * 64];  // [g][c] sums of this workgroup's groups
+  __shared__ double tws[4][8 * 64];    // per-wave [slot][feature] transpose tile of a finished group
   __shared__ int ecnt[kGsumG], eoff[kGsumG + 1], ecur[kGsumG], dcnt[kGsumG], hit[kGsumG], wbeg[5], wg0[4];
   float* rsh = (float*)ent;            // [32][65] bf16 representatives, after the sums
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1483,13 +1484,23 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
       const int cb = wbeg[wave] / 8, ce = wbeg[wave + 1] / 8;
       double a[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
       int g = wg0[wave], gend = 0;  // current group and its end chunk
+      // a finished group: the 8 slot rows go through the wave's LDS tile,
+      // lane = feature adds them and adds the sum into the group's LDS row
+      // (other waves may add to the same group)
+      double* tw = tws[wave];
       auto flush = [&]() {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) a[k] = sum_slots8(a[k]);
-        if (slot == 0) {
+        for (int k = 0; k < 8; k += 2) *(double2*)(tw + slot * 64 + 8 * j + k) = double2{a[k], a[k + 1]};
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        double v = tw[lane];
 #pragma unroll
-          for (int k = 0; k < 8; ++k) atomicAdd(&acc[g * 64 + 8 * j + k], a[k]);
-        }
+        for (int k = 1; k < 8; ++k) v += tw[k * 64 + lane];
+        atomicAdd(&acc[g * 64 + lane], v);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
         for (int k = 0; k < 8; ++k) a[k] = 0.0;
       };
