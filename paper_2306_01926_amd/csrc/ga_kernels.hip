@@ -608,10 +608,14 @@ __device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh
     exact_decide_queue<FIRST>(Kbh, key0, Rs, nrm_bh, N, kslot_w, sh, nunc);
     __syncthreads();
   }
-  const int nk = (int)min((int64_t)4 * tpw * 32, (int64_t)n - key0);
-  for (int x = tid; x < nk; x += 256) {
-    belong_bh[key0 + x] = sh.bst[x];
-    if (FIRST) knorm_bh[key0 + x] = __uint_as_float(sh.kx[x]);
+  // the first round writes every key's group; later rounds only those of the
+  // keys that moved (the others keep theirs)
+  if (FIRST) {
+    const int nk = (int)min((int64_t)4 * tpw * 32, (int64_t)n - key0);
+    for (int x = tid; x < nk; x += 256) {
+      belong_bh[key0 + x] = sh.bst[x];
+      knorm_bh[key0 + x] = __uint_as_float(sh.kx[x]);
+    }
   }
   if (!FIRST && !FUSED) {
     const int* wc = sh.c->wcnt;
@@ -622,10 +626,12 @@ __device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh
     // a slice records at most n moved keys in a round; the bound only guards
     // against a counter that was not cleared (a corrupted workspace)
     const int base = sh.c->moved_base;
-    for (int x = tid; x < nm && (int64_t)base + x < n; x += 256) {
+    for (int x = tid; x < nm; x += 256) {
       const uint32_t e = x < nw ? region_entry(sh.wrec, sh.cap, wc, x) : sh.kx[x - nw];
-      mrec_bh[base + x] = ((unsigned long long)(key0 + (e & 2047u)) << 32) | (((e >> 11) & 1023u) << 16) |
-                          (e >> 21);
+      belong_bh[key0 + (e & 2047u)] = (int32_t)(e >> 21);
+      if ((int64_t)base + x < n)
+        mrec_bh[base + x] = ((unsigned long long)(key0 + (e & 2047u)) << 32) | (((e >> 11) & 1023u) << 16) |
+                            (e >> 21);
     }
   }
 }
