@@ -117,6 +117,41 @@ def test_cluster_stepwise_against_trace(oracle_mod, dev):
         prev = ref["trace_centroid"][t]
 
 
+# One slice, so every workgroup of the first round covers 4 tiles of 32 keys:
+# n keys make ceil(ceil(n / 32) / 4) partitions of the first round's fused
+# update, 1 to 8, then 9 (too many: the separate update runs instead).
+PARTITION_CASES = [
+    # n, N, partitions
+    (100, 20, 1), (200, 50, 2), (380, 90, 3), (500, 128, 4), (620, 33, 5),
+    (750, 64, 6), (890, 100, 7), (1000, 127, 8), (1030, 128, 9),
+]
+
+
+@pytest.mark.parametrize("case", PARTITION_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_first_round_partitions(oracle_mod, dev, case):
+    n, N, parts = case
+    say(f"first-round partitions n={n} N={N} parts={parts}")
+    _, K, _ = inputs.make_qkv(1, 1, n, 64, "bf16", 40 + n, max(4, N // 2), 0.05, 0.3)
+    ga.timing_enable(True)
+    try:
+        got, ref = cluster_both(oracle_mod, K, N, 2, "bf16", dev)
+    finally:
+        ga.timing_enable(False)
+        launches = ga.timing_collect()
+    assert_groups_equal(got, ref)
+    assert ("part_finish" in launches) == (parts <= 8), sorted(launches)
+
+
+@pytest.mark.parametrize("n", [700, 3000])
+def test_cluster_single_round_with_caller_init(oracle_mod, dev, n):
+    """One round only: the fused first round (n = 700) and the separate update (n = 3000)."""
+    say(f"single round with caller init n={n}")
+    _, K, _ = inputs.make_qkv(1, 2, n, 64, "bf16", 6, 60, 0.05, 0.3)
+    init = torch.from_numpy(np.random.default_rng(n).standard_normal((1, 2, 96, 64)).astype(np.float32) * 0.2)
+    got, ref = cluster_both(oracle_mod, K, 96, 1, "bf16", dev, init=init)
+    assert_groups_equal(got, ref)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_aggregate_bit_exact(oracle_mod, dev, dtype):
     say(f"aggregate {dtype}")
@@ -218,6 +253,40 @@ def test_forward_is_deterministic(dev):
     for x, y in zip(a, b):
         assert torch.equal(x.view(torch.uint8) if x.dtype == torch.bfloat16 else x,
                            y.view(torch.uint8) if y.dtype == torch.bfloat16 else y)
+
+
+def test_forward_single_round(oracle_mod, dev):
+    say("forward, one grouping round")
+    Q, K, V = inputs.make_qkv(2, 1, 900, 64, "bf16", 17, 50, 0.05, 0.3)
+    O, bel, cnt, cen = ga.forward(Q.to(dev), K.to(dev), V.to(dev), 80, 1, return_groups=True)
+    torch.cuda.synchronize()
+    ref = oracle_mod.forward(f64(Q), f64(K), f64(V), 80, 1, 1 / 8, "bf16")
+    assert_groups_equal((bel.cpu().numpy(), cnt.cpu().numpy(), cen.cpu().numpy()), ref)
+    check_close(O, ref["O"], TOL["bf16"])
+
+
+def test_concurrent_forwards_separate_workspaces(dev):
+    """Two forwards overlapping on two streams, each with its own workspace,
+    give the results of the same forwards run one after the other."""
+    say("concurrent forwards on two streams")
+    args = [(inputs.make_qkv(2, 2, 2500, 64, "bf16", s, 128, 0.05, 0.3), N) for s, N in ((31, 128), (32, 100))]
+    args = [(tuple(t.to(dev) for t in qkv), N) for qkv, N in args]
+    seq = [ga.forward(*qkv, N, 5, return_groups=True) for qkv, N in args]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(dev) for _ in args]
+    wss = [torch.empty(ga.workspace_bytes(ga.shape_of(qkv[0]), N), dtype=torch.uint8, device=dev)
+           for qkv, N in args]
+    outs = [None, None]
+    for r in range(3):
+        for i, ((qkv, N), s) in enumerate(zip(args, streams)):
+            s.wait_stream(torch.cuda.current_stream(dev))
+            with torch.cuda.stream(s):
+                outs[i] = ga.forward(*qkv, N, 5, return_groups=True, ws=wss[i])
+        torch.cuda.synchronize()
+        for a, b in zip(seq, outs):
+            for x, y in zip(a, b):
+                assert torch.equal(x.view(torch.uint8) if x.dtype == torch.bfloat16 else x,
+                                   y.view(torch.uint8) if y.dtype == torch.bfloat16 else y), f"repeat {r}"
 
 
 def _sampled_full_size(oracle_mod, dev, w, seed, N, slices, queries=512):
