@@ -48,7 +48,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRs = 72;       // LDS row stride (bf16 elements) of the 32x16 MFMA A tiles
-constexpr int kAssignDepth = 1;  // key tiles loaded ahead per wave in k_assign_reg
 constexpr int kAttDepth = 2;     // query tiles loaded ahead per wave in k_attend_bf16
 constexpr int kOs = 72;          // LDS row stride (bf16) of the attention output tiles
 constexpr int kAttMaxN = 256; // groups held in LDS by the bf16 attention kernel
@@ -347,24 +346,30 @@ __device__ __forceinline__ void wave_append(bool mine, uint32_t rec, uint32_t* r
   n += (int)__popcll(mask);
 }
 
-// Decision for the 32 keys of one tile, given each lane's top-2 over its half
-// of the groups: merge the halves (both halves compute the same result),
-// certify the packed best against the error bound E, stage the group and
-// (later rounds) record keys whose group changed.  Keys that fail the test
+// Decision for the keys of two tiles A and B at once, given each lane's top-2
+// over its half of the groups for both: one lane swap per value leaves lane
+// q < 32 with both halves of key q of A and lane 32 + q with both halves of
+// key q of B, so every lane decides one key.  The lane merges its halves,
+// certifies the packed best against the error bound E, stages the group and
+// (later rounds) records keys whose group changed.  Keys that fail the test
 // are queued for exact_decide_queue (their staged group is provisional).
+// knv, oldv, lk: the lane's own key; stage: its tile exists (for B possibly
+// not, after an odd tile count); valid: also a key below n.
 //
 // E bounds |packed - exact| for the best and for any group that could beat
 // it: the MFMA part cm * M (M = max |r|^2 + 2 |k| max |r| bounds the sum of
 // |terms|) and the packing part cp * (|M1| + 3 cm M); the last two terms cover
 // the fp32 evaluation of E and of M1 + 2E.
 template <bool FIRST>
-__device__ __forceinline__ void decide_tile(float M1, float M2, int B1, float knv, int oldv, int lk, bool valid,
-                                            int N, const Certify& cf, const AssignLists& sh, int wave, int& wn,
-                                            int& un) {
-  const int h = (threadIdx.x >> 5) & 1;
-  const u32x2 p1 = halves(__float_as_uint(M1)), p2 = halves(__float_as_uint(M2)), pb = halves((uint32_t)B1);
+__device__ __forceinline__ void decide_pair(float M1a, float M2a, int B1a, float M1b, float M2b, int B1b, float knv,
+                                            int oldv, int lk, bool stage, bool valid, int N, const Certify& cf,
+                                            const AssignLists& sh, int wave, int& wn, int& un) {
+  const auto p1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(M1a), __float_as_uint(M1b), false, false);
+  const auto p2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(M2a), __float_as_uint(M2b), false, false);
+  const auto pb = __builtin_amdgcn_permlane32_swap((uint32_t)B1a, (uint32_t)B1b, false, false);
+  // [0]: the best over the groups held by lanes 0-31, [1]: by lanes 32-63
   const float a1 = __uint_as_float(p1[0]), b1 = __uint_as_float(p1[1]);
-  // the half h = 1 wins only with a strictly smaller best
+  // the half held by lanes 32-63 wins only with a strictly smaller best
   const bool hi_wins = b1 < a1;
   const uint32_t vw = __float_as_uint(hi_wins ? b1 : a1) & kPackMask;
   const int jstar = 32 * (int)(hi_wins ? pb[1] : pb[0]) + 8 * (int)(vw >> 2) + (hi_wins ? 4 : 0) + (int)(vw & 3);
@@ -374,11 +379,10 @@ __device__ __forceinline__ void decide_tile(float M1, float M2, int B1, float kn
   const float aM1 = fabsf(best);
   const float E = (cf.cm * Mk + cf.cp * (aM1 + 3.0f * cf.cm * Mk)) * (1.0f + 0x1p-20f) + 0x1p-22f * aM1 + 1e-30f;
   const bool certain = (second > best + 2.0f * E) && (jstar < N);
-  const bool mine = valid && h == 0;
-  sh.bst[lk] = jstar;
-  wave_append(mine && !certain, (uint32_t)lk | ((uint32_t)oldv << 11), sh.uq + wave * sh.cap, un);
+  if (stage) sh.bst[lk] = jstar;
+  wave_append(valid && !certain, (uint32_t)lk | ((uint32_t)oldv << 11), sh.uq + wave * sh.cap, un);
   if (!FIRST)
-    wave_append(mine && certain && oldv != jstar,
+    wave_append(valid && certain && oldv != jstar,
                 (uint32_t)lk | ((uint32_t)oldv << 11) | ((uint32_t)jstar << 21), sh.wrec + wave * sh.cap, wn);
 }
 
@@ -391,7 +395,7 @@ __device__ __forceinline__ uint32_t region_entry(const uint32_t* base, int cap, 
 
 // After every tile of the workgroup is scored: the four waves take the queued
 // keys in turn and decide each with exact_argmin_lds (the key row staged in
-// the wave's LDS slot), then stage and record it like decide_tile.
+// the wave's LDS slot), then stage and record it like decide_pair.
 template <bool FIRST>
 __device__ __forceinline__ void exact_decide_queue(const uint16_t* __restrict__ Kbh, int64_t key0, const uint16_t* Rs,
                                                    const double* __restrict__ nrm_bh, int N, uint16_t* kslot_w,
@@ -1014,10 +1018,9 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
 #pragma unroll
       for (int u = 0; u < 2; ++u) reduce_block(acc[u], blk, M1[u], M2[u], B1[u]);
     }
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-      if (tt + u < tcount)
-        decide_tile<FIRST>(M1[u], M2[u], B1[u], kn[u], old[u], lk[u], valid[u], N, cf, L.lists, wv, wn, un);
+    // lanes h = 0 decide the keys of tile tt, lanes h = 1 those of tile tt + 1
+    decide_pair<FIRST>(M1[0], M2[0], B1[0], M1[1], M2[1], B1[1], h ? kn[1] : kn[0], h ? old[1] : old[0],
+                       h ? lk[1] : lk[0], tt + h < tcount, h ? valid[1] : valid[0], N, cf, L.lists, wv, wn, un);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
 #pragma unroll
@@ -1052,35 +1055,54 @@ __device__ __forceinline__ void load_keys(const uint16_t* __restrict__ Kbh, cons
   }
 }
 
-// Scores of one tile against all NB blocks of groups and the lane's top-2.
-// Block b + 1's five MFMAs are interleaved with block b's reduction (all in
-// one straight-line region), so the matrix cores and the VALU work together.
+// The |r|^2 part of every score: block b's MFMA of the split row (A) with
+// ones in the first three k slots of lanes h = 0 (B), the same for every tile.
 template <int NB>
-__device__ __forceinline__ void score_tile(const u32x4 (&af)[NB][4], const u32x4 (&an)[NB], const u32x4& ones,
-                                           const u32x4 (&kf)[4], float& M1, float& M2, int& B1) {
+__device__ __forceinline__ void norm_terms(const u32x4 (&an)[NB], const u32x4& ones, f32x16 (&nacc)[NB]) {
   const f32x16 zero = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    nacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, an[b]),
+                                                      __builtin_bit_cast(bf16x8, ones), zero, 0, 0, 0);
+}
+
+// Scores of one tile against all NB blocks of groups and the lane's top-2.
+// HOISTED: the |r|^2 parts (norm_terms) were formed once per workgroup and
+// start each block's accumulation (four MFMAs per block); else they are the
+// block's fifth MFMA, after the four k-steps (an order the error bound allows:
+// it holds for any order of the terms).  Block b + 1's MFMAs are interleaved
+// with block b's reduction (all in one straight-line region), so the matrix
+// cores and the VALU work together.
+template <int NB, bool HOISTED>
+__device__ __forceinline__ void score_tile(const u32x4 (&af)[NB][4], const u32x4 (&an)[NB], const u32x4& ones,
+                                           const f32x16 (&nacc)[NB], const u32x4 (&kf)[4], float& M1, float& M2,
+                                           int& B1) {
+  const f32x16 zero = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  constexpr int kM = HOISTED ? 4 : 5;  // MFMAs per block
   f32x16 acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, an[b]),
-                                                     __builtin_bit_cast(bf16x8, ones), zero, 0, 0, 0);
+    acc[b] = HOISTED ? nacc[b] : zero;
 #pragma unroll
     for (int s2 = 0; s2 < 4; ++s2)
       acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[b][s2]),
                                                        __builtin_bit_cast(bf16x8, kf[s2]), acc[b], 0, 0, 0);
+    if (!HOISTED)
+      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, an[b]),
+                                                       __builtin_bit_cast(bf16x8, ones), acc[b], 0, 0, 0);
   }
   M1 = FLT_MAX;
   M2 = FLT_MAX;
   B1 = 0;
 #pragma unroll
   for (int b = 0; b < NB; ++b) reduce_block(acc[b], b, M1, M2, B1);
-  __builtin_amdgcn_sched_group_barrier(0x008, 5, 0);  // block 0's MFMAs
+  __builtin_amdgcn_sched_group_barrier(0x008, kM, 0);  // block 0's MFMAs
 #pragma unroll
   for (int b = 1; b < NB; ++b)
 #pragma unroll
-    for (int g = 0; g < 5; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA of block b
-      __builtin_amdgcn_sched_group_barrier(0x002, 9, 0);  // VALU of block b - 1
+    for (int g = 0; g < kM; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // one MFMA of block b
+      __builtin_amdgcn_sched_group_barrier(0x002, HOISTED ? 11 : 9, 0);  // VALU of block b - 1
     }
 }
 
@@ -1115,19 +1137,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   const uint16_t* Kbh = K + bh * (int64_t)n * 64;
   const float* knorm_bh = knorm + bh * n;
   const int32_t* belong_bh = belong + bh * n;
-  // The first key tiles (see the ring below) load while the workgroup stages R.
-  constexpr int D = kAssignDepth;
-  u32x4 kb[D + 1][4];
-  float knb[D + 1];
-  int oldb[D + 1];
-#pragma unroll
-  for (int r = 0; r <= D; ++r) {
-    knb[r] = 0.f;
-    oldb[r] = 0;
-  }
-#pragma unroll
-  for (int r = 0; r < D; ++r)
-    load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(r, tcount - 1), n, q, h, kb[r], knb[r], oldb[r]);
+  // The first key tile (see the loop below) loads while the workgroup stages R.
+  u32x4 kb[2][4];
+  float knb[2] = {0.f, 0.f};
+  int oldb[2] = {0, 0};
+  load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(0, tcount - 1), n, q, h, kb[0], knb[0], oldb[0]);
   // FUSED (first round): the initial representatives from the keys or the
   // given init; workgroup 0 of the slice writes C and clears the moved-key
   // counters of the next rounds
@@ -1154,35 +1168,42 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     for (int s2 = 0; s2 < 4; ++s2) af[b][s2] = *(const u32x4*)(L.Rs + swz(b * 32 + q, 4 * h + s2));
   }
   const u32x4 ones = h == 0 ? u32x4{0x3f803f80u, 0x3f80u, 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
+  // later rounds: the |r|^2 parts of the scores once for all tiles (the first
+  // round, which holds more state, adds them per tile)
+  constexpr bool kHoist = !FIRST;
+  f32x16 nacc[NB];
+  if (kHoist) norm_terms<NB>(an, ones, nacc);
 
   int wn = 0, un = 0;  // this wave's moved / uncertain entries (wave-uniform)
-  auto run = [&](const u32x4 (&kf)[4], float knv, int oldv, int t) __attribute__((always_inline)) {
-    const int lk = (wv * tpw + t) * 32 + q;
-    const bool valid = key0 + lk < n;
+  auto score = [&](const u32x4 (&kf)[4], float& knv, int t, float& M1, float& M2, int& B1)
+                   __attribute__((always_inline)) {
     if (FIRST) {
       knv = key_norm_bound(kf);
-      L.lists.kx[lk] = __float_as_uint(knv);
+      L.lists.kx[(wv * tpw + t) * 32 + q] = __float_as_uint(knv);
     }
-    float M1, M2;
-    int B1;
-    score_tile<NB>(af, an, ones, kf, M1, M2, B1);
-    decide_tile<FIRST>(M1, M2, B1, knv, oldv, lk, valid, N, cf, L.lists, wv, wn, un);
+    score_tile<NB, kHoist>(af, an, ones, nacc, kf, M1, M2, B1);
   };
-  // Ring of kAssignDepth + 1 register sets: tile t + kAssignDepth is loaded
-  // while tile t is scored (deeper rings measured no faster: the loop is
-  // bound by the scoring, not by the loads).  Loads past the last tile repeat
-  // it.  The scheduling barriers keep each prefetch ahead of the tile it
-  // overlaps.
-  for (int t0 = 0; t0 < tcount; t0 += D + 1) {
-#pragma unroll
-    for (int r = 0; r <= D; ++r) {
-      const int t = t0 + r;
-      if (t >= tcount) break;
-      const int w = (r + D) % (D + 1);
-      load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(t + D, tcount - 1), n, q, h, kb[w], knb[w], oldb[w]);
-      __builtin_amdgcn_sched_barrier(0);
-      run(kb[r], knb[r], oldb[r], t);
-    }
+  // Two register sets used in turn: tile t + 1 is loaded while tile t is
+  // scored (deeper rings measured no faster: the loop is bound by the
+  // scoring, not by the loads); loads past the last tile repeat it.  The
+  // tiles are decided in pairs (decide_pair).  The scheduling barriers keep
+  // each prefetch ahead of the tile it overlaps.
+  for (int t = 0; t < tcount; t += 2) {
+    float M1a, M2a, M1b, M2b;
+    int B1a, B1b;
+    load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(t + 1, tcount - 1), n, q, h, kb[1], knb[1], oldb[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    score(kb[0], knb[0], t, M1a, M2a, B1a);
+    const float kna = knb[0];
+    const int olda = oldb[0];
+    load_keys<FIRST>(Kbh, knorm_bh, belong_bh, tile0 + min(t + 2, tcount - 1), n, q, h, kb[0], knb[0], oldb[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    score(kb[1], knb[1], min(t + 1, tcount - 1), M1b, M2b, B1b);  // past the last tile: a repeat, not staged
+    // lanes h = 0 decide the keys of tile t, lanes h = 1 those of tile t + 1
+    const int lk = (wv * tpw + t + h) * 32 + q;
+    const bool stage = t + h < tcount;
+    decide_pair<FIRST>(M1a, M2a, B1a, M1b, M2b, B1b, h ? knb[1] : kna, h ? oldb[1] : olda, lk, stage,
+                       stage && key0 + lk < n, N, cf, L.lists, wv, wn, un);
   }
   if (lane == 0) {
     cnt.wcnt[wv] = wn;
