@@ -268,24 +268,27 @@ __device__ int exact_argmin_lds(const uint16_t* kl, const uint16_t* Rs, const do
 // group of a packed best (v, block b, half h) is 32 b + 8 (v/4) + 4 h + v%4.
 constexpr uint32_t kPackMask = 15u;
 
-// Top-2 of one block's 16 scores merged into the running (M1, M2, B1 = block
-// of M1).  Over pairs: with m1 <= m2 the two smallest so far, the second
-// smallest of {m1, m2, x, y} is min(m2, med3(m1, x, y)).  Equal packed values
-// in two blocks keep the earlier block; such a key is never certified (its
-// gap is 0), so the choice does not matter.
+// Top-2 of one block's 16 scores folded into the running (M1, M2, B1 = block
+// of M1).  Over quads: with m1 <= m2 the two smallest so far and
+// a = min3(m1, x0, x1), the two smallest of {m1, m2, x0, x1, x2, x3} are
+// min3(a, x2, x3) and min3(m2, med3(m1, x0, x1), med3(a, x2, x3)).  A packed
+// value equal to M1 from a later block keeps the earlier block; such a key is
+// never certified (its gap is 0), so the choice does not matter.
 __device__ __forceinline__ void reduce_block(const f32x16& acc, int blk, float& M1, float& M2, int& B1) {
-  float m1 = FLT_MAX, m2 = FLT_MAX;
+  const float prev = M1;
 #pragma unroll
-  for (int v = 0; v < 16; v += 2) {
-    const float x = __uint_as_float((__float_as_uint(acc[v]) & ~kPackMask) | (uint32_t)v);
-    const float y = __uint_as_float((__float_as_uint(acc[v + 1]) & ~kPackMask) | (uint32_t)(v + 1));
-    m2 = min2(m2, __builtin_amdgcn_fmed3f(m1, x, y));
-    m1 = min3f(m1, x, y);
+  for (int v = 0; v < 16; v += 4) {
+    float x[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      x[e] = __uint_as_float((__float_as_uint(acc[v + e]) & ~kPackMask) | (uint32_t)(v + e));
+    const float t01 = __builtin_amdgcn_fmed3f(M1, x[0], x[1]);
+    const float a = min3f(M1, x[0], x[1]);
+    const float t23 = __builtin_amdgcn_fmed3f(a, x[2], x[3]);
+    M1 = min3f(a, x[2], x[3]);
+    M2 = min3f(M2, t01, t23);
   }
-  B1 = m1 < M1 ? blk : B1;
-  const float nm2 = min2(max2(M1, m1), min2(M2, m2));
-  M1 = min2(M1, m1);
-  M2 = nm2;
+  B1 = M1 < prev ? blk : B1;
 }
 
 // Bounds shared by every tile of a slice: the largest |r|^2 and |r| (with
@@ -1102,7 +1105,7 @@ __device__ __forceinline__ void score_tile(const u32x4 (&af)[NB][4], const u32x4
 #pragma unroll
     for (int g = 0; g < kM; ++g) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // one MFMA of block b
-      __builtin_amdgcn_sched_group_barrier(0x002, HOISTED ? 11 : 9, 0);  // VALU of block b - 1
+      __builtin_amdgcn_sched_group_barrier(0x002, HOISTED ? 10 : 8, 0);  // VALU of block b - 1
     }
 }
 
