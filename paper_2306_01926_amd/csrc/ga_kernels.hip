@@ -44,12 +44,14 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef double f64x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRs = 72;       // LDS row stride (bf16 elements) of the 32x16 MFMA A tiles
 constexpr int kAttDepth = 2;     // query tiles loaded ahead per wave in k_attend_bf16
 constexpr int kOs = 72;          // LDS row stride (bf16) of the attention output tiles
+constexpr int kExactB = 4;       // queued keys decided together by one wave in k_assign_reg
 constexpr int kAttMaxN = 256; // groups held in LDS by the bf16 attention kernel
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
@@ -219,46 +221,79 @@ __global__ __launch_bounds__(256) void k_init(const typename S::T* __restrict__ 
 // logical chunk then hit 16 distinct groups of 4 banks (no padding needed).
 __device__ __forceinline__ int swz(int r, int c) { return r * 64 + 8 * (c ^ ((r >> 1) & 7)); }
 
-// Exact assignment of one bf16 key by a whole wave, the representatives read
-// from the LDS copy of -2R (r = -0.5 * (-2r) exactly).  Same definition as
-// exact_argmin_wave: fp64 fma chain over c = 0..63, lowest index among minima.
-// The key row sits in a per-wave LDS slot and is re-read for every group
-// (volatile), which keeps the 64 widened key values out of registers.
-__device__ int exact_argmin_lds(const uint16_t* kl, const uint16_t* Rs, const double* __restrict__ nrm, int N) {
+// Exact assignment of NK bf16 keys at once by a whole wave, the
+// representatives read from the LDS copy of -2R.  Same definition as
+// exact_argmin_wave (score fma(-2, k.r, |r|^2) with k.r an fp64 fma chain over
+// c = 0..63, lowest index among minima): x = -2r is exact in bf16 and every
+// partial sum of the chain over k_c x_c is exactly -2 times the one over
+// k_c r_c (the partial sums stay far from the fp64 subnormal range), so the
+// score is |r|^2 + (chain over k_c x_c) with one rounding.  kd: the keys as
+// fp64 rows [NK][64] in LDS (the same words in every lane).  Lane l takes
+// groups l, l + 64, l + 128, ... in ascending order, two at a time, and each
+// converts its representatives' features once for all NK keys.
+template <int NK>
+__device__ void exact_argmin_keys(const double* kd, const uint16_t* Rs, const double* __restrict__ nrm, int N,
+                                  int* jb) {
   const int lane = threadIdx.x & 63;
-  u32x4 kw[8];  // the key row (the same LDS words in every lane), read once
+  double best[NK];
+  int bj[NK];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) kw[i] = *(const u32x4*)(kl + 8 * i);
-  double best = INFINITY;
-  int bj = 0x7fffffff;
-  for (int j = lane; j < N; j += 64) {
-    const double nj = nrm[j];  // in flight during the dot product
-    double dot = 0.0;
+  for (int b = 0; b < NK; ++b) {
+    best[b] = INFINITY;
+    bj[b] = 0x7fffffff;
+  }
+  for (int j0 = lane; j0 < N; j0 += 128) {
+    const int j1 = j0 + 64;
+    const bool two = j1 < N;
+    const int j1r = two ? j1 : j0;  // a row that exists
+    const double n0 = nrm[j0], n1 = nrm[j1r];  // in flight during the dot products
+    double d0[NK], d1[NK];
 #pragma unroll
+    for (int b = 0; b < NK; ++b) d0[b] = d1[b] = 0.0;
+#pragma unroll 2
     for (int i = 0; i < 8; ++i) {
-      const u32x4 rw = *(const u32x4*)(Rs + swz(j, i));
+      const u32x4 w0 = *(const u32x4*)(Rs + swz(j0, i)), w1 = *(const u32x4*)(Rs + swz(j1r, i));
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        dot = fma((double)bf16_to_f32(kw[i][e] & 0xffffu), (double)(-0.5f * bf16_to_f32(rw[e] & 0xffffu)), dot);
-        dot = fma((double)bf16_to_f32(kw[i][e] >> 16), (double)(-0.5f * bf16_to_f32(rw[e] >> 16)), dot);
+        const double x0 = (double)bf16_to_f32(w0[e] & 0xffffu), y0 = (double)bf16_to_f32(w0[e] >> 16);
+        const double x1 = (double)bf16_to_f32(w1[e] & 0xffffu), y1 = (double)bf16_to_f32(w1[e] >> 16);
+#pragma unroll
+        for (int b = 0; b < NK; ++b) {
+          const f64x2 kk = *(const f64x2*)(kd + b * 64 + 8 * i + 2 * e);
+          d0[b] = fma(kk[0], x0, d0[b]);
+          d0[b] = fma(kk[1], y0, d0[b]);
+          d1[b] = fma(kk[0], x1, d1[b]);
+          d1[b] = fma(kk[1], y1, d1[b]);
+        }
       }
     }
-    const double sc = fma(-2.0, dot, nj);
-    if (sc < best) {
-      best = sc;
-      bj = j;
+#pragma unroll
+    for (int b = 0; b < NK; ++b) {
+      const double s0 = n0 + d0[b];
+      if (s0 < best[b]) {
+        best[b] = s0;
+        bj[b] = j0;
+      }
+      const double s1 = n1 + d1[b];
+      if (two && s1 < best[b]) {
+        best[b] = s1;
+        bj[b] = j1;
+      }
     }
   }
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const double ob = __shfl_xor(best, off);
-    const int oj = __shfl_xor(bj, off);
-    if (ob < best || (ob == best && oj < bj)) {
-      best = ob;
-      bj = oj;
+  for (int b = 0; b < NK; ++b) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const double ob = __shfl_xor(best[b], off);
+      const int oj = __shfl_xor(bj[b], off);
+      if (ob < best[b] || (ob == best[b] && oj < bj[b])) {
+        best[b] = ob;
+        bj[b] = oj;
+      }
     }
+    jb[b] = bj[b];
   }
-  return bj;
 }
 
 // Scores are ranked as packed floats: the low 4 mantissa bits of a score are
@@ -396,23 +431,41 @@ __device__ __forceinline__ uint32_t region_entry(const uint32_t* base, int cap, 
   return base[r * cap + u];
 }
 
-// After every tile of the workgroup is scored: the four waves take the queued
-// keys in turn and decide each with exact_argmin_lds (the key row staged in
-// the wave's LDS slot), then stage and record it like decide_pair.
-template <bool FIRST>
+// After every tile of the workgroup is scored: each wave takes a quarter of
+// the queued keys (consecutive entries) and decides them B at a time
+// with exact_argmin_keys (their rows widened to fp64 in the wave's LDS slot
+// kd_w, [B][64]), then stages and records each like decide_pair.
+template <bool FIRST, int B>
 __device__ __forceinline__ void exact_decide_queue(const uint16_t* __restrict__ Kbh, int64_t key0, const uint16_t* Rs,
-                                                   const double* __restrict__ nrm_bh, int N, uint16_t* kslot_w,
+                                                   const double* __restrict__ nrm_bh, int N, double* kd_w,
                                                    const AssignLists& sh, int nunc) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int u = wave; u < nunc; u += 4) {
-    const uint32_t e = region_entry(sh.uq, sh.cap, sh.c->ucnt, u);
-    const int lk = (int)(e & 2047u), oldv = (int)(e >> 11);
-    if (lane < 8) *(u32x4*)(kslot_w + lane * 8) = *(const u32x4*)(Kbh + (key0 + lk) * 64 + lane * 8);
-    const int jb = exact_argmin_lds(kslot_w, Rs, nrm_bh, N);
+  const int per = (nunc + 3) >> 2;
+  const int u_end = min(nunc, (wave + 1) * per);
+  for (int u0 = wave * per; u0 < u_end; u0 += B) {
+    const int nb = min(B, u_end - u0);
+    uint32_t e[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      e[b] = b < nb ? region_entry(sh.uq, sh.cap, sh.c->ucnt, u0 + b) : 0u;
+      if (b < nb) kd_w[b * 64 + lane] = (double)bf16_to_f32(Kbh[(key0 + (e[b] & 2047u)) * 64 + lane]);
+    }
+    int jb[B];
+    switch (nb) {  // wave-uniform
+      case 1: exact_argmin_keys<1>(kd_w, Rs, nrm_bh, N, jb); break;
+      case 2: exact_argmin_keys<(B >= 2 ? 2 : 1)>(kd_w, Rs, nrm_bh, N, jb); break;
+      case 3: exact_argmin_keys<(B >= 3 ? 3 : 1)>(kd_w, Rs, nrm_bh, N, jb); break;
+      default: exact_argmin_keys<B>(kd_w, Rs, nrm_bh, N, jb); break;
+    }
     if (lane == 0) {
-      sh.bst[lk] = jb;
-      if (!FIRST && oldv != jb)
-        sh.kx[atomicAdd(&sh.c->nx, 1)] = (uint32_t)lk | ((uint32_t)oldv << 11) | ((uint32_t)jb << 21);
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        if (b >= nb) break;
+        const int lk = (int)(e[b] & 2047u), oldv = (int)(e[b] >> 11);
+        sh.bst[lk] = jb[b];
+        if (!FIRST && oldv != jb[b])
+          sh.kx[atomicAdd(&sh.c->nx, 1)] = (uint32_t)lk | ((uint32_t)oldv << 11) | ((uint32_t)jb[b] << 21);
+      }
     }
   }
 }
@@ -600,19 +653,19 @@ __device__ __forceinline__ AssignLds assign_lds_layout(unsigned char* smem, int 
 // decisions of the queued keys, then the staged groups (and first-round |k|
 // bounds) of keys key0 .. key0 + 4 tpw 32 (those below n); without the fused
 // update also the moved-key records, one global atomic per workgroup.
-template <bool FIRST, bool FUSED>
+template <bool FIRST, bool FUSED, int B>
 __device__ __forceinline__ void assign_epilogue(const uint16_t* __restrict__ Kbh, int64_t key0, int tpw,
                                                 const uint16_t* Rs, const double* nrm_bh, int n, int N,
                                                 int32_t* __restrict__ belong_bh, float* __restrict__ knorm_bh,
                                                 int32_t* __restrict__ mcount_bh,
-                                                unsigned long long* __restrict__ mrec_bh, uint16_t* kslot_w,
+                                                unsigned long long* __restrict__ mrec_bh, double* kd_w,
                                                 const AssignLists& sh) {
   const int tid = threadIdx.x;
   __syncthreads();
   const int* uc = sh.c->ucnt;
   const int nunc = uc[0] + uc[1] + uc[2] + uc[3];
   if (nunc) {  // uniform: read after the barrier
-    exact_decide_queue<FIRST>(Kbh, key0, Rs, nrm_bh, N, kslot_w, sh, nunc);
+    exact_decide_queue<FIRST, B>(Kbh, key0, Rs, nrm_bh, N, kd_w, sh, nunc);
     __syncthreads();
   }
   // the first round writes every key's group; later rounds only those of the
@@ -914,7 +967,7 @@ __global__ __launch_bounds__(256) void k_part_finish(const double* __restrict__ 
 // If second - best > 2E, where E bounds |packed - exact| (the MFMA fp32
 // accumulation, the split of |r|^2 and the packing), the packed best is
 // provably the exact fp64 argmin; otherwise the key is queued and re-decided
-// by exact_argmin_lds once the workgroup's tiles are done.  Later rounds
+// by exact_argmin_keys once the workgroup's tiles are done.  Later rounds
 // (FIRST = false) also emit the keys whose group changed as records
 // (key, old, new).
 //
@@ -932,7 +985,7 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ double red[4];
   __shared__ AssignCounts cnt;
-  __shared__ __align__(16) uint16_t kslot[4][64];  // key row of a queued key, per wave
+  __shared__ __align__(16) double kd[4][64];  // fp64 row of a queued key, per wave
   const int Npad = (N + 31) & ~31;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
   const int64_t bh = blockIdx.y;
@@ -1036,8 +1089,8 @@ __global__ __launch_bounds__(256) void k_assign_bf16(
     cnt.wcnt[wv] = wn;
     cnt.ucnt[wv] = un;
   }
-  assign_epilogue<FIRST, false>(Kbh, key0, tpw, Rs, nrm64 + bh * N, n, N, belong_bh, knorm + bh * n, mcount + bh,
-                                mrec + bh * n, kslot[wave], L.lists);
+  assign_epilogue<FIRST, false, 1>(Kbh, key0, tpw, Rs, nrm64 + bh * N, n, N, belong_bh, knorm + bh * n, mcount + bh,
+                                   mrec + bh * n, kd[wave], L.lists);
 }
 
 // Key fragments of tile `tile` of a slice, and in later rounds the keys' |k|
@@ -1126,7 +1179,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ double red[4];
   __shared__ AssignCounts cnt;
-  __shared__ __align__(16) uint16_t kslot[4][64];  // key row of a queued key, per wave
+  __shared__ __align__(16) double kd[4][kExactB * 64];  // fp64 rows of queued keys, per wave
   constexpr int Npad = NB * 32;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
   const int64_t bh = blockIdx.y;
@@ -1212,8 +1265,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     cnt.wcnt[wv] = wn;
     cnt.ucnt[wv] = un;
   }
-  assign_epilogue<FIRST, FUSED>(Kbh, key0, tpw, L.Rs, nrm_x, n, N, belong + bh * n, knorm + bh * n,
-                                mcount + bh, mrec + bh * n, kslot[wave], L.lists);
+  assign_epilogue<FIRST, FUSED, kExactB>(Kbh, key0, tpw, L.Rs, nrm_x, n, N, belong + bh * n, knorm + bh * n,
+                                          mcount + bh, mrec + bh * n, kd[wave], L.lists);
   if (FUSED) {
     __shared__ PartLds pl;
     const int nk = (int)min((int64_t)4 * tpw * 32, (int64_t)n - key0);
@@ -2025,7 +2078,7 @@ __global__ __launch_bounds__(256) void k_attend_f32(const float* __restrict__ Q,
   }
 }
 
-constexpr size_t kAssignLdsMax = 160 * 1024 - 1024;  // dynamic LDS budget (static arrays use the rest)
+constexpr size_t kAssignLdsMax = 160 * 1024 - 3 * 1024;  // dynamic LDS budget (static arrays use the rest)
 
 size_t assign_lds(int N, int tpw = 12, bool fused = false) {  // see assign_lds_layout
   const int Npad = (N + 31) & ~31, cap4 = 4 * tpw * 32;
