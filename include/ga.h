@@ -129,6 +129,44 @@ int ga_forward(ga_shape_t s, const void *Q, const void *K, const void *V, int32_
                float *centroid, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * Attention block of the RITA encoder (bf16 only): the encoder is a
+ * Transformer encoder whose self-attention is replaced by group attention
+ * (Section 3), with the bias-free projections Q = X W_Q, K = X W_K,
+ * V = X W_V of Eq. 1, one d = 64 slice per head, and the heads' outputs
+ * concatenated and projected by W_O.  D = d_model = 64 H.
+ *
+ * Layouts (all bf16, dense, row-major):
+ *   X, Y  [B, n, D] token embeddings in / block output;
+ *   Wqkv  [3D, D]: one OUTPUT feature per row, the input axis contiguous
+ *         (rows 0..D-1 give Q, D..2D-1 give K, 2D..3D-1 give V; within each,
+ *         row 64 h + c is feature c of head h), i.e. the transpose of the
+ *         column-per-feature W_Q | W_K | W_V of Eq. 1;
+ *   Wo    [D, D]: row o holds the weights of output feature o over the
+ *         concatenated heads (input index 64 h + c = feature c of head h);
+ *   Q, K, V, O  [B, H, n, 64] as everywhere in this library.
+ * Products are accumulated in fp32 on the matrix cores and rounded once to
+ * bf16 (round to nearest even); each output is within one bf16 unit in the
+ * last place of the exactly rounded product.  s.d must be 64, s.dtype
+ * GA_BF16 (GA_ERR_UNSUPPORTED otherwise), H <= 64, N <= min(n, 256).
+ * Pointer, stream and error conventions as above; B = 0 or H = 0 enqueues
+ * nothing.
+ */
+size_t ga_block_workspace_bytes(ga_shape_t s, int32_t N); /* 0 if invalid */
+
+/* Q, K, V [B,H,n,64] = per-head slices of X Wqkv^T (Eq. 1). */
+int ga_project_qkv(ga_shape_t s, const void *X, const void *Wqkv, void *Q, void *K, void *V, void *stream);
+
+/* Y [B,n,D] = concat_h(O[:, h]) Wo^T. */
+int ga_project_out(ga_shape_t s, const void *O, const void *Wo, void *Y, void *stream);
+
+/* Y = attention block of X: ga_project_qkv, ga_forward (strided init,
+ * `iters` rounds, `scale`), ga_project_out.  The workspace
+ * (ga_block_workspace_bytes) holds Q, K, V, O and the forward's workspace. */
+int ga_attention_block(ga_shape_t s, const void *X, const void *Wqkv, const void *Wo, int32_t N,
+                       int32_t iters, float scale, void *Y, void *workspace, size_t workspace_bytes,
+                       void *stream);
+
+/*
  * Per-kernel timing for measurement tools.  While enabled (per calling
  * thread), every kernel launch of this library is bracketed by a pair of
  * hipEvents recorded on the launch stream.  ga_timing_collect waits for the

@@ -136,3 +136,45 @@ def round_bf16(x):
     u = np.ascontiguousarray(np.asarray(x, np.float32)).view(np.uint32).astype(np.uint64)
     u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
     return u.astype(np.uint32).view(np.float32)
+
+
+def round_bf16_f64(x):
+    """bf16 round-to-nearest-even of float64 values in ONE rounding (no
+    intermediate float32), as float64.  Normal bf16 range only."""
+    m, e = np.frexp(np.asarray(x, np.float64))  # x = m 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.rint(m * 256.0), e - 8)  # 8 significant bits; rint ties to even
+
+
+def project_qkv(X, Wqkv, H: int):
+    """Eq. 1 projections Q = X W_Q, K = X W_K, V = X W_V of token embeddings
+    X [B, n, D] with Wqkv [3D, D] holding one output feature per row (Q rows,
+    then K, then V; row 64 h + c = feature c of head h): exact fp64 products,
+    each rounded once to bf16.  Returns Q, K, V as [B, H, n, 64] float64."""
+    X, W = _f64(X), _f64(Wqkv)
+    B, n, D = X.shape
+    P = round_bf16_f64(X @ W.T)  # [B, n, 3D]
+    heads = P.reshape(B, n, 3, H, 64).transpose(2, 0, 3, 1, 4)  # [3, B, H, n, 64]
+    return tuple(np.ascontiguousarray(heads[i]) for i in range(3))
+
+
+def project_out(O, Wo):
+    """Output projection of the Transformer encoder's multi-head attention:
+    the heads' outputs O [B, H, n, 64] concatenated per token (feature 64 h + c)
+    times Wo^T (Wo [D, D], one output feature per row), rounded once to bf16."""
+    O, W = _f64(O), _f64(Wo)
+    B, H, n, d = O.shape
+    cat = O.transpose(0, 2, 1, 3).reshape(B, n, H * d)
+    return round_bf16_f64(cat @ W.T)
+
+
+def attention_block(X, Wqkv, Wo, H: int, N: int, iters: int, scale: float):
+    """RITA encoder attention block (Section 3: a Transformer encoder whose
+    self-attention is group attention): projections (Eq. 1), the group
+    attention forward of every (b, h) slice in bf16 storage, its output rounded
+    to bf16, then the output projection.  Returns dict(Y, Q, K, V, O, belong,
+    count, centroid)."""
+    Q, K, V = project_qkv(X, Wqkv, H)
+    r = forward(Q, K, V, N, iters, scale, "bf16")
+    O = round_bf16_f64(r["O"])
+    Y = project_out(O, Wo)
+    return dict(Y=Y, Q=Q, K=K, V=V, O=O, belong=r["belong"], count=r["count"], centroid=r["centroid"])

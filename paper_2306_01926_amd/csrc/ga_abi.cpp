@@ -127,6 +127,60 @@ int run_valuesum(const ga::Dims& d, const void* V, const int32_t* belong, int32_
   return GA_OK;
 }
 
+// Whole forward on validated arguments (belong / count / centroid may be NULL).
+int run_forward(const ga::Dims& d, const void* Q, const void* K, const void* V, int32_t iters, float scale, void* O,
+                int32_t* belong, int32_t* count, float* centroid, const ga::Workspace& w, hipStream_t st) {
+  int32_t* a = belong ? belong : w.belong;
+  int32_t* cnt = count ? count : w.count;
+  float* C = centroid ? centroid : w.C;
+  GA_TRY(run_cluster(d, K, iters, nullptr, a, cnt, C, w, st));
+  if (d.dtype == GA_BF16) {
+    // the value sums go straight into the attention's transposed means and bias
+    GA_LAUNCH(ga::launch_valuesum_prep(d, V, a, cnt, scale, w.Vt, w.ginit, st), "value-sum launch");
+    GA_LAUNCH(ga::launch_attend(d, Q, w.R, w.Vt, w.ginit, C, cnt, w.vsum, scale, O, st), "attention launch");
+  } else {
+    // the last stable bucket pass sorted the keys by the final assignment: reuse it
+    GA_LAUNCH(ga::launch_valuesum(d, V, w.perm, w.goff, cnt, w.vsum, st), "value-sum launch");
+    GA_LAUNCH(ga::launch_attend(d, Q, nullptr, nullptr, nullptr, C, cnt, w.vsum, scale, O, st),
+              "attention launch");
+  }
+  return GA_OK;
+}
+
+// Shape checks of the attention block (bf16 only, d = 64, d_model = 64 H <= 4096).
+// with_groups: also check N against n and the bf16 attention limit.
+int check_block_shape(const ga_shape_t& s, int32_t N, bool with_groups, bool* empty) {
+  *empty = false;
+  if (s.dtype != GA_BF16 && s.dtype != GA_F32) return fail(GA_ERR_INVALID_ARG, "unknown dtype %d", s.dtype);
+  if (s.dtype != GA_BF16) return fail(GA_ERR_UNSUPPORTED, "the attention block is bf16 only");
+  if (s.B < 0 || s.H < 0) return fail(GA_ERR_INVALID_ARG, "negative batch/head count (B=%d, H=%d)", s.B, s.H);
+  if (s.n < 1) return fail(GA_ERR_INVALID_ARG, "n must be >= 1 (got %d)", s.n);
+  if (s.d != ga::kD) return fail(GA_ERR_UNSUPPORTED, "only d = 64 is supported (got %d)", s.d);
+  if (s.H > 64) return fail(GA_ERR_UNSUPPORTED, "d_model = 64 H must be <= 4096 (H=%d)", s.H);
+  if ((int64_t)s.B * s.H > 65535) return fail(GA_ERR_UNSUPPORTED, "B*H exceeds 65535");
+  if (s.n > (1 << 30)) return fail(GA_ERR_UNSUPPORTED, "n = %d too large", s.n);
+  if (with_groups) {
+    if (N < 1 || N > s.n || N > 256)
+      return fail(N > 256 && N <= s.n ? GA_ERR_UNSUPPORTED : GA_ERR_INVALID_ARG,
+                  "N must satisfy 1 <= N <= min(n, 256) (N=%d, n=%d)", N, s.n);
+  }
+  *empty = s.B == 0 || s.H == 0;
+  return GA_OK;
+}
+
+// Block workspace: Q, K, V, O [B][H][n][64] bf16, then the group-attention
+// workspace.  Returns the bytes; with base set, fills qkvo and w.
+size_t block_ws_layout(const ga_shape_t& s, int32_t N, void* base, void** qkvo, ga::Workspace* w) {
+  const size_t t = ((size_t)s.B * s.H * s.n * 64 * 2 + 255) & ~(size_t)255;
+  const ga::Dims d = dims_of(s, N);
+  const size_t rest = ga::workspace_layout(d, nullptr, nullptr);
+  if (base) {
+    for (int i = 0; i < 4; ++i) qkvo[i] = (char*)base + i * t;
+    ga::workspace_layout(d, w, (char*)base + 4 * t);
+  }
+  return 4 * t + rest;
+}
+
 // ---------------------------------------------------------------- kernel timing
 struct TimingRec {
   const char* name;
@@ -292,21 +346,67 @@ int ga_forward(ga_shape_t s, const void* Q, const void* K, const void* V, int32_
   const ga::Dims d = dims_of(s, N);
   ga::Workspace w;
   GA_TRY(check_ws(d, workspace, workspace_bytes, &w));
+  return run_forward(d, Q, K, V, iters, scale, O, belong, count, centroid, w, (hipStream_t)stream);
+}
+
+size_t ga_block_workspace_bytes(ga_shape_t s, int32_t N) {
+  bool empty;
+  const std::string keep = g_last_error;
+  const int rc = check_block_shape(s, N, true, &empty);
+  g_last_error = keep;
+  if (rc != GA_OK) return 0;
+  return block_ws_layout(s, N, nullptr, nullptr, nullptr);
+}
+
+int ga_project_qkv(ga_shape_t s, const void* X, const void* Wqkv, void* Q, void* K, void* V, void* stream) {
+  bool empty;
+  GA_TRY(check_block_shape(s, 1, false, &empty));
+  GA_TRY(check_ptr(X, "X", true));
+  GA_TRY(check_ptr(Wqkv, "Wqkv", true));
+  GA_TRY(check_ptr(Q, "Q", true));
+  GA_TRY(check_ptr(K, "K", true));
+  GA_TRY(check_ptr(V, "V", true));
+  if (empty) return GA_OK;
+  GA_LAUNCH(ga::launch_project(0, s.B, s.n, s.H, X, Wqkv, Q, K, V, (hipStream_t)stream), "projection launch");
+  return GA_OK;
+}
+
+int ga_project_out(ga_shape_t s, const void* O, const void* Wo, void* Y, void* stream) {
+  bool empty;
+  GA_TRY(check_block_shape(s, 1, false, &empty));
+  GA_TRY(check_ptr(O, "O", true));
+  GA_TRY(check_ptr(Wo, "Wo", true));
+  GA_TRY(check_ptr(Y, "Y", true));
+  if (empty) return GA_OK;
+  GA_LAUNCH(ga::launch_project(1, s.B, s.n, s.H, O, Wo, Y, nullptr, nullptr, (hipStream_t)stream),
+            "projection launch");
+  return GA_OK;
+}
+
+int ga_attention_block(ga_shape_t s, const void* X, const void* Wqkv, const void* Wo, int32_t N, int32_t iters,
+                       float scale, void* Y, void* workspace, size_t workspace_bytes, void* stream) {
+  bool empty;
+  GA_TRY(check_block_shape(s, N, true, &empty));
+  if (iters < 1) return fail(GA_ERR_INVALID_ARG, "iters must be >= 1 (got %d)", iters);
+  if (!isfinite(scale)) return fail(GA_ERR_INVALID_ARG, "scale must be finite");
+  GA_TRY(check_ptr(X, "X", true));
+  GA_TRY(check_ptr(Wqkv, "Wqkv", true));
+  GA_TRY(check_ptr(Wo, "Wo", true));
+  GA_TRY(check_ptr(Y, "Y", true));
+  if (empty) return GA_OK;
+  const size_t need = block_ws_layout(s, N, nullptr, nullptr, nullptr);
+  if (!workspace) return fail(GA_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (((uintptr_t)workspace & 255u) != 0) return fail(GA_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(GA_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+  void* qkvo[4];
+  ga::Workspace w;
+  block_ws_layout(s, N, workspace, qkvo, &w);
   hipStream_t st = (hipStream_t)stream;
-  int32_t* a = belong ? belong : w.belong;
-  int32_t* cnt = count ? count : w.count;
-  float* C = centroid ? centroid : w.C;
-  GA_TRY(run_cluster(d, K, iters, nullptr, a, cnt, C, w, st));
-  if (s.dtype == GA_BF16) {
-    // the value sums go straight into the attention's transposed means and bias
-    GA_LAUNCH(ga::launch_valuesum_prep(d, V, a, cnt, scale, w.Vt, w.ginit, st), "value-sum launch");
-    GA_LAUNCH(ga::launch_attend(d, Q, w.R, w.Vt, w.ginit, C, cnt, w.vsum, scale, O, st), "attention launch");
-  } else {
-    // the last stable bucket pass sorted the keys by the final assignment: reuse it
-    GA_LAUNCH(ga::launch_valuesum(d, V, w.perm, w.goff, cnt, w.vsum, st), "value-sum launch");
-    GA_LAUNCH(ga::launch_attend(d, Q, nullptr, nullptr, nullptr, C, cnt, w.vsum, scale, O, st),
-              "attention launch");
-  }
+  GA_LAUNCH(ga::launch_project(0, s.B, s.n, s.H, X, Wqkv, qkvo[0], qkvo[1], qkvo[2], st), "projection launch");
+  GA_TRY(run_forward(dims_of(s, N), qkvo[0], qkvo[1], qkvo[2], iters, scale, qkvo[3], nullptr, nullptr, nullptr, w,
+                     st));
+  GA_LAUNCH(ga::launch_project(1, s.B, s.n, s.H, qkvo[3], Wo, Y, nullptr, nullptr, st), "projection launch");
   return GA_OK;
 }
 

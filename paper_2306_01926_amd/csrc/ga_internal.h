@@ -109,4 +109,10 @@ hipError_t launch_attend(const Dims& d, const void* Q, const void* R, const uint
                          const float* ginit, const float* centroid, const int32_t* count,
                          const float* vsum, float scale, void* O, hipStream_t st);
 
+// Projections of the attention block (ga_block.hip), bf16 with fp32
+// accumulation.  mode 0: X [B][n][64H] x Wqkv[192H][64H]^T -> out0/1/2 = Q, K, V
+// [B][H][n][64];  mode 1: O [B][H][n][64] x Wo[64H][64H]^T -> out0 = Y [B][n][64H].
+hipError_t launch_project(int mode, int B, int n, int H, const void* A, const void* W, void* out0, void* out1,
+                          void* out2, hipStream_t st);
+
 }  // namespace ga

@@ -18,6 +18,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libga.so")
 GA_F32, GA_BF16 = 0, 1
 STATUS = {0: "GA_OK", 1: "GA_ERR_INVALID_ARG", 2: "GA_ERR_UNSUPPORTED", 3: "GA_ERR_WORKSPACE", 4: "GA_ERR_HIP"}
 SYMBOLS = ("ga_workspace_bytes", "ga_cluster", "ga_aggregate", "ga_attend", "ga_forward",
+           "ga_block_workspace_bytes", "ga_project_qkv", "ga_project_out", "ga_attention_block",
            "ga_timing_enable", "ga_timing_collect", "ga_status_string", "ga_last_error")
 
 
@@ -53,7 +54,13 @@ def lib() -> ctypes.CDLL:
         L.ga_aggregate.argtypes = [Shape, P, P, i32, P, P, ctypes.c_size_t, P]
         L.ga_attend.argtypes = [Shape, P, P, P, P, i32, ctypes.c_float, P, P, ctypes.c_size_t, P]
         L.ga_forward.argtypes = [Shape, P, P, P, i32, i32, ctypes.c_float, P, P, P, P, P, ctypes.c_size_t, P]
-        for f in ("ga_cluster", "ga_aggregate", "ga_attend", "ga_forward"):
+        L.ga_block_workspace_bytes.argtypes = [Shape, i32]
+        L.ga_block_workspace_bytes.restype = ctypes.c_size_t
+        L.ga_project_qkv.argtypes = [Shape, P, P, P, P, P, P]
+        L.ga_project_out.argtypes = [Shape, P, P, P, P]
+        L.ga_attention_block.argtypes = [Shape, P, P, P, i32, i32, ctypes.c_float, P, P, ctypes.c_size_t, P]
+        for f in ("ga_cluster", "ga_aggregate", "ga_attend", "ga_forward", "ga_project_qkv", "ga_project_out",
+                  "ga_attention_block"):
             getattr(L, f).restype = ctypes.c_int
         L.ga_timing_enable.argtypes = [ctypes.c_int]
         L.ga_timing_enable.restype = ctypes.c_int
@@ -184,6 +191,48 @@ def forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, N: int, iters: in
     _check(lib().ga_forward(s, _p(Q), _p(K), _p(V), int(N), int(iters), scale, _p(O), _p(belong), _p(count),
                             _p(centroid), wp, nb, _stream(dev)))
     return (O, belong, count, centroid) if return_groups else O
+
+
+def block_shape(X: torch.Tensor, H: int) -> Shape:
+    """Shape of the attention block for token embeddings X [B, n, 64 H]."""
+    if X.dim() != 3 or X.shape[2] != 64 * H:
+        raise ValueError(f"expected X of shape [B, n, {64 * H}]")
+    return Shape(X.shape[0], H, X.shape[1], 64, _dtype_code(X))
+
+
+def project_qkv(X: torch.Tensor, Wqkv: torch.Tensor, H: int):
+    """(Q, K, V) [B, H, n, 64] = per-head slices of X Wqkv^T (Wqkv [3D, D], rows = outputs)."""
+    s = block_shape(X, H)
+    B, n, _ = X.shape
+    Q, K, V = (torch.empty((B, H, n, 64), dtype=X.dtype, device=X.device) for _ in range(3))
+    _check(lib().ga_project_qkv(s, _p(X), _p(Wqkv), _p(Q), _p(K), _p(V), _stream(X.device)))
+    return Q, K, V
+
+
+def project_out(O: torch.Tensor, Wo: torch.Tensor) -> torch.Tensor:
+    """Y [B, n, D] = heads of O [B, H, n, 64] concatenated, times Wo^T (Wo [D, D])."""
+    B, H, n, d = O.shape
+    Y = torch.empty((B, n, H * d), dtype=O.dtype, device=O.device)
+    _check(lib().ga_project_out(Shape(B, H, n, d, _dtype_code(O)), _p(O), _p(Wo), _p(Y), _stream(O.device)))
+    return Y
+
+
+def block_workspace_bytes(shape: Shape, N: int) -> int:
+    return int(lib().ga_block_workspace_bytes(shape, int(N)))
+
+
+def attention_block(X: torch.Tensor, Wqkv: torch.Tensor, Wo: torch.Tensor, H: int, N: int, iters: int,
+                    scale: float | None = None, out: torch.Tensor | None = None, ws=None) -> torch.Tensor:
+    """Attention block: projections, group-attention forward, output projection.
+    ws: a uint8 device tensor of block_workspace_bytes(shape, N) (allocated if None)."""
+    s = block_shape(X, H)
+    scale = 1.0 / 8.0 if scale is None else float(scale)
+    Y = torch.empty_like(X) if out is None else out
+    if ws is None:
+        ws = torch.empty(max(block_workspace_bytes(s, N), 256), dtype=torch.uint8, device=X.device)
+    _check(lib().ga_attention_block(s, _p(X), _p(Wqkv), _p(Wo), int(N), int(iters), scale, _p(Y), _p(ws),
+                                    ws.numel(), _stream(X.device)))
+    return Y
 
 
 def timing_enable(on: bool = True) -> None:

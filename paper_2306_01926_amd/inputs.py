@@ -17,6 +17,12 @@ produce recurring, similar windows and hence clustered keys.  Per (b, h) slice:
 
 Everything is drawn in float32 from numpy's PCG64 and then rounded to the
 storage dtype (bfloat16 with round-to-nearest-even, or kept as float32).
+
+The attention block (projections around group attention) takes token
+embeddings X [B, n, D] instead: per (batch, channel) the sum of four sinusoids
+A sin(2 pi t / P + phi), A ~ U[0.5, 1.5], P log-uniform in [8, 1000],
+phi ~ U[0, 2 pi), plus N(0, 0.1^2) noise (the periodic series of the paper's
+premise), and weights W ~ N(0, 1/D), all rounded to bf16.
 """
 from __future__ import annotations
 
@@ -57,6 +63,27 @@ WORKLOADS = {
     "n8000_N128_bf16": Workload("n8000_N128_bf16", 16, 8, 8000, 64, 128, "bf16", 10, 128, 0.05, 0.3),
     "n20000_Nvar_bf16": Workload("n20000_Nvar_bf16", 4, 8, 20000, 64, None, "bf16", 10, 256, 0.05, 0.3,
                                  N_choices=(32, 64, 128, 256)),
+}
+
+
+@dataclasses.dataclass(frozen=True)
+class BlockWorkload:
+    """Attention block: projections of D = 64 H embeddings around group attention."""
+
+    name: str
+    B: int
+    n: int
+    H: int
+    N: int
+    iters: int
+
+    @property
+    def D(self) -> int:
+        return 64 * self.H
+
+
+BLOCK_WORKLOADS = {
+    "encoder_n4000_N128_bf16": BlockWorkload("encoder_n4000_N128_bf16", 32, 4000, 8, 128, 10),
 }
 
 
@@ -112,3 +139,22 @@ def sha256(t: torch.Tensor) -> str:
     """Digest of the raw bytes of a tensor (to record which inputs were used)."""
     b = t.detach().to("cpu").contiguous().view(torch.uint8).numpy().tobytes()
     return hashlib.sha256(b).hexdigest()
+
+
+def block_inputs(B: int, n: int, H: int, seed: int):
+    """(X [B, n, D], Wqkv [3D, D], Wo [D, D]) bf16 CPU tensors, D = 64 H
+    (recipe in the module docstring; weight rows are output features)."""
+    D = 64 * H
+    rng = np.random.Generator(np.random.PCG64(seed))
+    t = np.arange(n, dtype=np.float32)[None, :, None]
+    X = np.zeros((B, n, D), np.float32)
+    for _ in range(4):
+        A = rng.uniform(0.5, 1.5, size=(B, 1, D)).astype(np.float32)
+        P = np.exp(rng.uniform(np.log(8.0), np.log(1000.0), size=(B, 1, D))).astype(np.float32)
+        phi = rng.uniform(0.0, 2 * np.pi, size=(B, 1, D)).astype(np.float32)
+        X += A * np.sin(np.float32(2 * np.pi) * t / P + phi)
+    X += np.float32(0.1) * rng.standard_normal((B, n, D), dtype=np.float32)
+    sd = np.float32(1.0 / np.sqrt(D))
+    Wqkv = sd * rng.standard_normal((3 * D, D), dtype=np.float32)
+    Wo = sd * rng.standard_normal((D, D), dtype=np.float32)
+    return to_storage(X, "bf16"), to_storage(Wqkv, "bf16"), to_storage(Wo, "bf16")

@@ -106,3 +106,32 @@ def test_workspace_bytes():
     # update's per-partition sums) stays modest next to 288 GB of HBM
     big = L.ga_workspace_bytes(ga.Shape(16, 8, 8000, 64, ga.GA_BF16), 128)
     assert big < 256 * 2**20
+
+
+def test_block_entry_points_validate():
+    L = ga.lib()
+    s = shape(B=2, H=8, n=300)
+    nb = L.ga_block_workspace_bytes(s, 32)
+    assert nb > 4 * 2 * 8 * 300 * 64 * 2  # Q, K, V, O plus the forward's workspace
+    assert L.ga_block_workspace_bytes(shape(dtype=ga.GA_F32), 8) == 0
+    assert L.ga_block_workspace_bytes(s, 0) == 0
+    assert L.ga_project_qkv(shape(dtype=ga.GA_F32), P(), P(), P(), P(), P(), None) == 2
+    assert L.ga_project_qkv(shape(d=32), P(), P(), P(), P(), P(), None) == 2
+    assert L.ga_project_qkv(shape(H=65), P(), P(), P(), P(), P(), None) == 2
+    assert L.ga_project_qkv(s, None, P(), P(), P(), P(), None) == 1
+    assert L.ga_project_qkv(s, P(), P(FAKE + 2), P(), P(), P(), None) == 1
+    assert L.ga_project_qkv(shape(B=0, H=8), P(), P(), P(), P(), P(), None) == 0
+    assert L.ga_project_out(s, P(), None, P(), None) == 1
+    assert L.ga_project_out(shape(n=0), P(), P(), P(), None) == 1
+    assert L.ga_project_out(shape(B=0), P(), P(), P(), None) == 0
+    blk = lambda s, N=32, iters=2, scale=0.125, ws=FAKE, nbytes=nb: L.ga_attention_block(
+        s, P(), P(), P(), N, iters, scale, P(), P(ws) if ws else None, nbytes, None)
+    assert blk(s, N=0) == 1
+    assert blk(s, N=301) == 1
+    assert blk(shape(B=2, H=8, n=1000), N=300) == 2
+    assert blk(s, iters=0) == 1
+    assert blk(s, scale=float("inf")) == 1
+    assert blk(s, ws=0) == 3
+    assert blk(s, ws=FAKE + 64) == 3
+    assert blk(s, nbytes=nb - 1) == 3
+    assert blk(shape(B=0, H=8), ws=0) == 0
