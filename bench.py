@@ -48,6 +48,12 @@ def kernel_work(name, w, N, BH):
         return "hbm", 2.0 * n * d * es * BH / 1e9, "GB/s", HBM_PEAK_GBS
     if name in ("sums_full", "valuesum", "update"):
         return "hbm", 1.0 * n * (d * es + 4) * BH / 1e9, "GB/s", HBM_PEAK_GBS
+    if name in ("proj_qkv", "proj_out"):
+        # dense contractions over D = 64 H: 2 M Dout D flop, M = B n tokens
+        H = BH // w.B
+        D = 64 * H
+        dout = 3 * D if name == "proj_qkv" else D
+        return "mfma", 2.0 * w.B * n * dout * D / 1e12, "TFLOP/s", MFMA_BF16_PEAK_TFS
     return None
 
 
@@ -90,6 +96,8 @@ def main():
 
     from paper_2306_01926_amd import ga, inputs
 
+    if args.workload in inputs.BLOCK_WORKLOADS:
+        return bench_block(args)
     dev = torch.device("cuda:0")
     w = inputs.WORKLOADS[args.workload]
     N = inputs.draw_group_count(w, args.seed, 0)
@@ -199,6 +207,100 @@ def main():
         "pct_hbm_roofline": pct_hbm, "compulsory_bytes": compulsory,
         "roofline": roofline, "cpu_baseline": cpu,
         "kernels": kernels, "ms_per_step_with_kernel_events": ms_timed, "parity_sample": parity,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def per_kernel_report(per_kernel, steps, w, N, BH):
+    kernels = {}
+    for name, (launches, tot) in per_kernel.items():
+        avg = tot / launches
+        kernels[name] = dict(launches_per_step=launches / steps, avg_ms=avg)
+        kw = kernel_work(name, w, N, BH)
+        if kw:
+            bound, work, unit, peak = kw
+            ach = work / (avg / 1e3)
+            kernels[name].update(bound=bound, achieved=ach, unit=unit, frac=ach / peak)
+    return kernels
+
+
+def bench_block(args):
+    """Attention block (projections, group attention, output projection) on
+    token embeddings X [B, n, 64 H]: one step = one ga_attention_block."""
+    import types
+
+    import numpy as np
+    import torch
+
+    from paper_2306_01926_amd import ga, inputs
+
+    dev = torch.device("cuda:0")
+    bw = inputs.BLOCK_WORKLOADS[args.workload]
+    w = types.SimpleNamespace(B=bw.B, n=bw.n, d=64, dtype="bf16")
+    BH = bw.B * bw.H
+    print(f"bench: attention block {bw.name} B={bw.B} n={bw.n} H={bw.H} D={bw.D} N={bw.N} iters={bw.iters} bf16",
+          file=sys.stderr, flush=True)
+    host = [inputs.block_inputs(bw.B, bw.n, bw.H, args.seed + k) for k in range(2)]
+    sets = [tuple(t.to(dev) for t in s) for s in host]
+    outs = [torch.empty_like(s[0]) for s in sets]
+    ws = torch.empty(ga.block_workspace_bytes(ga.block_shape(sets[0][0], bw.H), bw.N), dtype=torch.uint8,
+                     device=dev)
+
+    def step(k):
+        X, Wqkv, Wo = sets[k % 2]
+        ga.attention_block(X, Wqkv, Wo, bw.H, bw.N, bw.iters, 0.125, out=outs[k % 2], ws=ws)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for k in range(args.steps):
+        step(k)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    ga.timing_enable(True)
+    for k in range(args.steps):
+        step(k)
+    torch.cuda.synchronize()
+    ga.timing_enable(False)
+    per_kernel = ga.timing_collect()
+    kernels = per_kernel_report(per_kernel, args.steps, w, bw.N, BH)
+    dom = max((k for k in per_kernel if "frac" in kernels[k]), key=lambda k: per_kernel[k][1])
+    kd = kernels[dom]
+    roofline = dict(kernel=dom, bound=kd["bound"], achieved=round(kd["achieved"], 3),
+                    peak=kernel_work(dom, w, bw.N, BH)[3], unit=kd["unit"], frac=round(kd["frac"], 4),
+                    traffic=traffic_for(dom, bw.name), avg_launch_ms=round(kd["avg_ms"], 5))
+    tokens = bw.B * bw.n
+    flops = 2.0 * tokens * 4 * bw.D * bw.D + 2.0 * BH * bw.n * bw.N * 64 * (bw.iters + 2)
+
+    cpu = parity = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        X0, W0, O0 = (inputs.as_float64(t) for t in host[0])
+        threads = oracle.threads()
+        c0 = time.perf_counter()
+        ref = oracle.attention_block(X0[:1], W0, O0, bw.H, bw.N, bw.iters, 0.125)
+        cpu_s = time.perf_counter() - c0
+        cpu = dict(value=bw.n / cpu_s, unit="tokens/s", cores=threads, kind="oracle",
+                   sample=f"batch 0 of {bw.B} ({bw.n} tokens, {bw.H} heads): fp64 projections, all {bw.iters} "
+                          f"grouping rounds, aggregation, attention, output projection; {cpu_s:.1f} s wall on "
+                          f"{threads} threads")
+        step(0)
+        torch.cuda.synchronize()
+        Yg = outs[0][:1].float().cpu().numpy().astype(np.float64)
+        parity = dict(batches=1, out_max_rel_err=float(np.abs(Yg - ref["Y"]).max() / np.abs(ref["Y"]).max()))
+
+    line = {
+        "metric": "attention-block tokens/sec (B·n) at n=4000, d_model=512, H=8, N=128", "value": tokens / (ms / 1e3),
+        "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": bw.name, "B": bw.B, "n": bw.n, "H": bw.H, "d_model": bw.D, "N": bw.N,
+                   "iters": bw.iters, "input_sets": 2},
+        "mfma_frac_of_step": flops / (ms / 1e3) / (MFMA_BF16_PEAK_TFS * 1e12),
+        "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels, "parity_sample": parity,
     }
     print(json.dumps(line), flush=True)
 

@@ -48,13 +48,18 @@ constexpr int kTO = 128;  // output features per tile
 constexpr int kXBytes = kTM * 128;  // one k-chunk (64 bf16) of the token rows
 constexpr int kWBytes = kTO * 128;  // one k-chunk of the weight rows
 
-// LDS byte offset of 16-byte granule q (0..7) of row r of a token tile: the
-// granule index is XORed with r mod 8 so that lanes reading the same granule
-// of 8 consecutive rows hit 8 different bank groups.
-__device__ __forceinline__ int xoff(int r, int q) { return r * 128 + ((q ^ (r & 7)) << 4); }
-// Same for the weight tile, whose MFMA reads take rows {0..3, 16..19} + 4 j
-// together (see wrow): key = bits 0, 1 and 4 of the row.
-__device__ __forceinline__ int woff(int r, int q) { return r * 128 + ((q ^ ((r & 3) | ((r >> 2) & 4))) << 4); }
+// LDS byte offset of 16-byte granule q (0..7) of row r of a token tile.  The
+// granule index is XORed with a 3-bit key of the row so that the 16-byte
+// reads of one MFMA operand (lane i: row i, the same granule) hit distinct
+// bank groups both per 8 lanes (128 bytes) and per 16 lanes (256 bytes): the
+// key takes all 8 values on 8 aligned consecutive rows, and on the even and
+// on the odd rows of 16 (a 256-byte line holds an even and an odd row).
+__device__ __forceinline__ int xkey(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+__device__ __forceinline__ int xoff(int r, int q) { return r * 128 + ((q ^ xkey(r)) << 4); }
+// The weight tile is read in the order of wrow below (lane rho: row
+// wrow(rho)): its key is xkey of that read rank.
+__device__ __forceinline__ int wkey(int r) { return ((r & 3) | ((r >> 2) & 4)) ^ ((r >> 2) & 1); }
+__device__ __forceinline__ int woff(int r, int q) { return r * 128 + ((q ^ wkey(r)) << 4); }
 
 // Weight row (within a 32-row block) fed to MFMA row rho: output row
 // rho = 8 (i / 4) + 4 h + (i % 4) of accumulator register i on lane half h
