@@ -53,6 +53,8 @@ def _load():
         lib.ga_oracle_aggregate.restype = i64
         lib.ga_oracle_attend.argtypes = [i32, i32, i32, i32, i32, P, P, P, P, i32, f64, P]
         lib.ga_oracle_attend.restype = None
+        lib.ga_oracle_merge_plan.argtypes = [i32, i32, i32, i32, P, P, P, P, P, i32, f64, f64, P, P, P, P]
+        lib.ga_oracle_merge_plan.restype = None
         lib.ga_oracle_threads.argtypes = [i32]
         lib.ga_oracle_threads.restype = i32
         _lib = lib
@@ -129,6 +131,37 @@ def forward(Q, K, V, N: int, iters: int, scale: float, dtype: str, init=None):
     vsum, inexact_v = aggregate(V, cl["belong"], N)
     O = attend(Q, cl["centroid"], cl["count"], vsum, N, scale, dtype)
     return dict(O=O, vsum=vsum, inexact_v=inexact_v, **cl)
+
+
+def merge_plan(Q, K, belong, centroid, count, N: int, scale: float, eps: float):
+    """Adaptive scheduler's merge plan (Section 5.1, Lemma 1, Eq. 5) of a
+    grouping: per slice the group radii, the distance threshold
+    dthr = ln(eps) / (2 |scale| max|q|), each S2 group's lowest S1 partner
+    (-1 if not mergeable) and the number of mergeable groups."""
+    import math
+
+    Q, K = _f64(Q), _f64(K)
+    B, H, n, d = K.shape
+    bel = np.ascontiguousarray(np.asarray(belong, np.int32))
+    cen = np.ascontiguousarray(np.asarray(centroid, np.float32))
+    cnt = np.ascontiguousarray(np.asarray(count, np.int32))
+    radius = np.empty((B, H, N), np.float64)
+    dthr = np.empty((B, H), np.float64)
+    partner = np.empty((B, H, N), np.int32)
+    merges = np.empty((B, H), np.int32)
+    _load().ga_oracle_merge_plan(B, H, n, d, _ptr(Q), _ptr(K), _ptr(bel), _ptr(cen), _ptr(cnt), N, float(scale),
+                                 math.log(eps), _ptr(radius), _ptr(dthr), _ptr(partner), _ptr(merges))
+    return dict(radius=radius, dthr=dthr, partner=partner, merges=merges)
+
+
+def next_group_count(N: int, merges, alpha: float) -> int:
+    """Momentum update of the group count (Section 5.1):
+    N_new = alpha (N - D) + (1 - alpha) N, with D the fewest mergeable groups
+    over the slices (so that every slice keeps its bound), rounded to the
+    nearest integer (halves up) and kept in [1, N]."""
+    D = int(np.min(np.asarray(merges))) if np.size(merges) else 0
+    x = alpha * (N - D) + (1.0 - alpha) * N
+    return int(min(N, max(1, np.floor(x + 0.5))))
 
 
 def round_bf16(x):

@@ -11,7 +11,10 @@
  *     the same for every centre and drops out of the argmin);
  *   - embedding aggregation: per-group SUM of the value vectors (Section 4.2,
  *     Algorithm 1, embedding-aggregation loop);
- *   - group softmax (Eq. 3) and output combine (Algorithm 1).
+ *   - group softmax (Eq. 3) and output combine (Algorithm 1);
+ *   - the adaptive scheduler's merge plan (Section 5.1: Lemma 1 turns the
+ *     error bound eps into a distance threshold, the simplified rule of Eq. 5
+ *     marks mergeable groups).
  *
  * Readings where the paper is silent (each also listed in the design doc):
  *   init     C0_j = k_{floor(j*n/N)} (strided), or a caller-given fp32 init.
@@ -264,5 +267,88 @@ void ga_oracle_attend(int B, int H, int n, int d, int dtype, const double *Q,
         }
         free(R);
         free(p);
+    }
+}
+
+/* Squared Euclidean distance of x and y as an fp64 fma chain over c = 0..d-1
+ * from 0; every difference is exact in fp64 (bf16 / fp32 operands). */
+static double canon_dist2(const double *x, const double *y, int d) {
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) {
+        const double t = x[c] - y[c];
+        acc = fma(t, t, acc);
+    }
+    return acc;
+}
+
+/*
+ * Merge plan of the adaptive scheduler (Section 5.1) for every (b, h) slice.
+ *   Lemma 1: if every key lies within dthr of its group's representative and
+ *     dthr <= ln(eps) / (2 R'), the restored attention is within a factor eps
+ *     of the exact one; R' bounds the (scaled) query norms, which is what the
+ *     proof uses: R' = |scale| max_i |q_i|.  dthr = log_eps / (2 R') (+inf if
+ *     R' = 0).
+ *   Lemma 2 / Eq. 5 (simplified rule): the groups are halved into
+ *     S1 = [0, ceil(N/2)) and S2 = [ceil(N/2), N); a group j of S2 is marked
+ *     when some i of S1 has |c_i - c_j| + rad_i <= dthr and
+ *     |c_j - c_i| + rad_j <= dthr / 2, where c is the group centroid and
+ *     rad_g = max over the members x of g of |x - c_g|.
+ * Readings: only non-empty groups take part (an empty group has radius 0, is
+ * never marked and is never a partner); partner_j = the lowest such i (-1 if
+ * none, and -1 for every group of S1); merges = number of marked groups.
+ * Evaluation: squared distances by canon_dist2, radius = sqrt of the largest
+ * squared member distance, qmax = sqrt of the largest squared query norm,
+ * R' = |scale| * qmax, dthr = log_eps / (2 * R'), sums in fp64.
+ *   Q, K [B,H,n,d] doubles; belong [B,H,n]; centroid [B,H,N,d] floats;
+ *   count [B,H,N].  Out: radius [B,H,N], dthr [B,H], partner [B,H,N],
+ *   merges [B,H].
+ */
+void ga_oracle_merge_plan(int B, int H, int n, int d, const double *Q, const double *K,
+                          const int32_t *belong, const float *centroid, const int32_t *count, int N,
+                          double scale, double log_eps, double *radius, double *dthr,
+                          int32_t *partner, int32_t *merges) {
+    const int64_t BH = (int64_t)B * H;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t u = 0; u < BH; ++u) {
+        double *C = (double *)malloc(sizeof(double) * (size_t)N * d);
+        double *rad2 = (double *)calloc((size_t)N, sizeof(double));
+        const int32_t *cnt = count + u * (int64_t)N;
+        for (int64_t x = 0; x < (int64_t)N * d; ++x) C[x] = (double)centroid[u * (int64_t)N * d + x];
+        double qmax2 = 0.0;
+        for (int i = 0; i < n; ++i) {
+            const double *q = Q + (u * (int64_t)n + i) * d;
+            double acc = 0.0;
+            for (int c = 0; c < d; ++c) acc = fma(q[c], q[c], acc);
+            if (acc > qmax2) qmax2 = acc;
+            const int g = belong[u * (int64_t)n + i];
+            if (g < 0 || g >= N) continue;
+            const double r2 = canon_dist2(K + (u * (int64_t)n + i) * d, C + (size_t)g * d, d);
+            if (r2 > rad2[g]) rad2[g] = r2;
+        }
+        const double rprime = fabs(scale) * sqrt(qmax2);
+        const double t = log_eps / (2.0 * rprime);
+        dthr[u] = t;
+        int32_t marked = 0;
+        const int half = (N + 1) / 2;
+        for (int j = 0; j < N; ++j) radius[u * (int64_t)N + j] = sqrt(rad2[j]);
+        for (int j = 0; j < N; ++j) {
+            int32_t pj = -1;
+            if (j >= half && cnt[j] > 0) {
+                const double rj = sqrt(rad2[j]);
+                for (int i = 0; i < half; ++i) {
+                    if (cnt[i] <= 0) continue;
+                    const double dij = sqrt(canon_dist2(C + (size_t)i * d, C + (size_t)j * d, d));
+                    if (dij + sqrt(rad2[i]) <= t && dij + rj <= 0.5 * t) {
+                        pj = i;
+                        break;
+                    }
+                }
+            }
+            partner[u * (int64_t)N + j] = pj;
+            marked += pj >= 0;
+        }
+        merges[u] = marked;
+        free(C);
+        free(rad2);
     }
 }

@@ -1,7 +1,8 @@
 """Each plausible single mistake planted in the oracle must fail the pins.
 
 The mutants are built on the CPU from a patched copy of oracle/ga_oracle.c
-and the pin suite (test_oracle_pins.py) is run against each in a subprocess.
+and the pin suites (test_oracle_merge.py, test_oracle_pins.py) are run
+against each in a subprocess.
 """
 import os
 import subprocess
@@ -31,7 +32,15 @@ MUTANTS = {
     "numerator_counts_twice": ("o[c] += e * vs[(size_t)j * d + c];", "o[c] += cnt[j] * e * vs[(size_t)j * d + c];"),
     "attend_ignores_representative_rounding": ("R[x] = round_dt(centroid[u * (int64_t)N * d + x], dtype);",
                                                "R[x] = (double)centroid[u * (int64_t)N * d + x];"),
+    # merge plan (adaptive group count)
+    "merge_rule_symmetric_threshold": ("dij + rj <= 0.5 * t", "dij + rj <= t"),
+    "merge_threshold_without_factor_two": ("log_eps / (2.0 * rprime)", "log_eps / rprime"),
+    "merge_query_norm_unscaled": ("fabs(scale) * sqrt(qmax2)", "sqrt(qmax2)"),
+    "merge_radius_of_last_member": ("if (r2 > rad2[g]) rad2[g] = r2;", "rad2[g] = r2;"),
+    "merge_partner_searched_in_both_halves": ("for (int i = 0; i < half; ++i) {", "for (int i = 0; i < N; ++i) {"),
+    "merge_empty_groups_take_part": ("if (cnt[i] <= 0) continue;\n", "\n"),
 }
+PIN_FILES = ("test_oracle_merge.py", "test_oracle_pins.py")
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
@@ -47,6 +56,6 @@ def test_planted_mistake_fails_the_pins(name, tmp_path):
     lib = oracle.build(force=True, src=str(src), out=str(tmp_path / "libmutant.so"))
     env = dict(os.environ, GA_ORACLE_LIB=lib, OMP_NUM_THREADS="2")
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                        *(os.path.join(ROOT, "tests", f) for f in PIN_FILES)],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} passed every pin:\n{r.stdout[-2000:]}"
