@@ -138,6 +138,29 @@ def main():
     per_kernel = ga.timing_collect()
     ms_timed = t0.elapsed_time(t1) / args.steps
 
+    # the adaptive scheduler's merge plan of the same grouping (run once per
+    # training step, outside the forward): timed on its own
+    sched = None
+    if w.dtype == "bf16" and N <= 256:
+        Q0, K0, V0 = sets[0]
+        _, bel0, cnt0, cen0 = ga.forward(Q0, K0, V0, N, w.iters, scale, return_groups=True, ws=ws)
+        for _ in range(2):
+            ga.merge_plan(Q0, K0, bel0, cen0, cnt0, N, scale, 2.0)
+        torch.cuda.synchronize()
+        ga.timing_enable(True)
+        for _ in range(args.steps):
+            plan = ga.merge_plan(Q0, K0, bel0, cen0, cnt0, N, scale, 2.0)
+        torch.cuda.synchronize()
+        ga.timing_enable(False)
+        tk = ga.timing_collect()  # merge_zero, merge_norms, merge_pairs per call
+        avg = sum(t for _, t in tk.values()) / args.steps
+        # algorithmic bytes: Q and K rows, the groups, the centroids and counts read once
+        mbytes = BH * (w.n * (2 * w.d * 2 + 4) + N * (w.d * 4 + 4))
+        sched = dict(kernel="merge_plan", launches={k: t / l for k, (l, t) in tk.items()}, eps=2.0, avg_ms=avg,
+                     bound="hbm", achieved=mbytes / (avg / 1e3) / 1e9,
+                     peak=HBM_PEAK_GBS, unit="GB/s", frac=mbytes / (avg / 1e3) / 1e9 / HBM_PEAK_GBS,
+                     merges_min=int(plan["merges"].min()), next_N=ga.next_group_count(N, plan["merges"], 0.5))
+
     queries = BH * w.n
     es = 2 if w.dtype == "bf16" else 4
     compulsory = 4.0 * queries * w.d * es  # read Q, K, V once, write O once
@@ -207,6 +230,7 @@ def main():
         "pct_hbm_roofline": pct_hbm, "compulsory_bytes": compulsory,
         "roofline": roofline, "cpu_baseline": cpu,
         "kernels": kernels, "ms_per_step_with_kernel_events": ms_timed, "parity_sample": parity,
+        "scheduler": sched,
     }
     print(json.dumps(line), flush=True)
 

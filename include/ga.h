@@ -167,6 +167,41 @@ int ga_attention_block(ga_shape_t s, const void *X, const void *Wqkv, const void
                        void *stream);
 
 /*
+ * Adaptive group count (Section 5.1): the merge plan of a grouping.
+ *   Lemma 1: if every key lies within dthr of its group's representative and
+ *   dthr <= ln(eps) / (2 R'), each restored attention weight is within a
+ *   factor eps of the exact one; R' = |scale| max_i |q_i| bounds the scaled
+ *   query norms (the quantity the proof bounds).  Per slice
+ *   dthr = ln(eps) / (2 R') (+inf if R' = 0).
+ *   Eq. 5 (simplified merge rule): the groups are halved into
+ *   S1 = [0, ceil(N/2)) and S2 = [ceil(N/2), N); group j of S2 is marked when
+ *   some i of S1 has |c_i - c_j| + rad_i <= dthr and
+ *   |c_j - c_i| + rad_j <= dthr / 2 (c: centroid, rad_g: largest distance of
+ *   a member of g to c_g).  Only non-empty groups take part.
+ * Arguments: Q, K [B,H,n,d] in s.dtype; belong, centroid, count as output by
+ * ga_cluster; eps > 1 (finite).  Outputs (device): radius [B,H,N] fp64
+ * (0 for an empty group), dthr [B,H] fp64, partner [B,H,N] int32 (for a
+ * marked S2 group the lowest qualifying S1 group, else -1), merges [B,H]
+ * int32 (marked groups).  Every value is computed in fp64 exactly as the
+ * definition states (squares summed as fma chains over the features in
+ * order, IEEE square roots) and matches the fp64 CPU definition bit for bit.
+ * N <= 256 (GA_ERR_UNSUPPORTED above).
+ */
+int ga_merge_plan(ga_shape_t s, const void *Q, const void *K, const int32_t *belong, const float *centroid,
+                  const int32_t *count, int32_t N, float scale, double eps, double *radius, double *dthr,
+                  int32_t *partner, int32_t *merges, void *stream);
+
+/*
+ * Momentum update of the group count (Section 5.1), on the HOST:
+ * N_new = alpha (N - D) + (1 - alpha) N with D the smallest of the `slices`
+ * per-slice merge counts (host array; every slice then keeps its bound),
+ * rounded to the nearest integer (halves up) and kept in [1, N].
+ * Returns N_new, or 0 (and ga_last_error) for N < 1, alpha outside [0, 1],
+ * slices < 0 or merges NULL with slices > 0.
+ */
+int32_t ga_next_group_count(int32_t N, const int32_t *merges, int64_t slices, double alpha);
+
+/*
  * Per-kernel timing for measurement tools.  While enabled (per calling
  * thread), every kernel launch of this library is bracketed by a pair of
  * hipEvents recorded on the launch stream.  ga_timing_collect waits for the

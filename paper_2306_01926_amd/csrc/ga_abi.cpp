@@ -410,6 +410,42 @@ int ga_attention_block(ga_shape_t s, const void* X, const void* Wqkv, const void
   return GA_OK;
 }
 
+int ga_merge_plan(ga_shape_t s, const void* Q, const void* K, const int32_t* belong, const float* centroid,
+                  const int32_t* count, int32_t N, float scale, double eps, double* radius, double* dthr,
+                  int32_t* partner, int32_t* merges, void* stream) {
+  bool empty;
+  GA_TRY(check_shape(s, N, &empty));
+  if (!isfinite(scale)) return fail(GA_ERR_INVALID_ARG, "scale must be finite");
+  if (!(eps > 1.0) || !isfinite(eps)) return fail(GA_ERR_INVALID_ARG, "eps must be a finite bound > 1 (got %g)", eps);
+  if (N > ga::merge_max_groups())
+    return fail(GA_ERR_UNSUPPORTED, "the merge plan supports N <= %d (got %d)", ga::merge_max_groups(), N);
+  GA_TRY(check_ptr(Q, "Q", true));
+  GA_TRY(check_ptr(K, "K", true));
+  GA_TRY(check_ptr(belong, "belong", true));
+  GA_TRY(check_ptr(centroid, "centroid", true));
+  GA_TRY(check_ptr(count, "count", true));
+  GA_TRY(check_ptr(radius, "radius", true));
+  GA_TRY(check_ptr(dthr, "dthr", true));
+  GA_TRY(check_ptr(partner, "partner", true));
+  GA_TRY(check_ptr(merges, "merges", true));
+  if (empty) return GA_OK;
+  GA_LAUNCH(ga::launch_merge_plan(dims_of(s, N), Q, K, belong, centroid, count, fabs((double)scale), log(eps), radius,
+                                  dthr, partner, merges, (hipStream_t)stream),
+            "merge-plan launch");
+  return GA_OK;
+}
+
+int32_t ga_next_group_count(int32_t N, const int32_t* merges, int64_t slices, double alpha) {
+  if (N < 1) return fail(GA_ERR_INVALID_ARG, "N must be >= 1 (got %d)", N), 0;
+  if (!(alpha >= 0.0 && alpha <= 1.0)) return fail(GA_ERR_INVALID_ARG, "alpha must lie in [0, 1]"), 0;
+  if (slices < 0 || (slices > 0 && !merges)) return fail(GA_ERR_INVALID_ARG, "merges must hold `slices` counts"), 0;
+  int64_t D = 0;
+  for (int64_t u = 0; u < slices; ++u) D = u == 0 || merges[u] < D ? merges[u] : D;
+  const double x = alpha * (double)(N - D) + (1.0 - alpha) * (double)N;
+  const double r = floor(x + 0.5);
+  return r < 1.0 ? 1 : (r > N ? N : (int32_t)r);
+}
+
 const char* ga_status_string(int status) {
   switch (status) {
     case GA_OK: return "GA_OK";

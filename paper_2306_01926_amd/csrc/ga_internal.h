@@ -115,4 +115,11 @@ hipError_t launch_attend(const Dims& d, const void* Q, const void* R, const uint
 hipError_t launch_project(int mode, int B, int n, int H, const void* A, const void* W, void* out0, void* out1,
                           void* out2, hipStream_t st);
 
+// Merge plan of the adaptive group count (ga_merge.hip): per slice the group
+// radii, the Lemma 1 threshold and the lowest S1 partner of each S2 group.
+int merge_max_groups();
+hipError_t launch_merge_plan(const Dims& d, const void* Q, const void* K, const int32_t* belong,
+                             const float* centroid, const int32_t* count, double abs_scale, double log_eps,
+                             double* radius, double* dthr, int32_t* partner, int32_t* merges, hipStream_t st);
+
 }  // namespace ga

@@ -19,6 +19,7 @@ GA_F32, GA_BF16 = 0, 1
 STATUS = {0: "GA_OK", 1: "GA_ERR_INVALID_ARG", 2: "GA_ERR_UNSUPPORTED", 3: "GA_ERR_WORKSPACE", 4: "GA_ERR_HIP"}
 SYMBOLS = ("ga_workspace_bytes", "ga_cluster", "ga_aggregate", "ga_attend", "ga_forward",
            "ga_block_workspace_bytes", "ga_project_qkv", "ga_project_out", "ga_attention_block",
+           "ga_merge_plan", "ga_next_group_count",
            "ga_timing_enable", "ga_timing_collect", "ga_status_string", "ga_last_error")
 
 
@@ -59,8 +60,11 @@ def lib() -> ctypes.CDLL:
         L.ga_project_qkv.argtypes = [Shape, P, P, P, P, P, P]
         L.ga_project_out.argtypes = [Shape, P, P, P, P]
         L.ga_attention_block.argtypes = [Shape, P, P, P, i32, i32, ctypes.c_float, P, P, ctypes.c_size_t, P]
+        L.ga_merge_plan.argtypes = [Shape, P, P, P, P, P, i32, ctypes.c_float, ctypes.c_double, P, P, P, P, P]
+        L.ga_next_group_count.argtypes = [i32, P, ctypes.c_int64, ctypes.c_double]
+        L.ga_next_group_count.restype = i32
         for f in ("ga_cluster", "ga_aggregate", "ga_attend", "ga_forward", "ga_project_qkv", "ga_project_out",
-                  "ga_attention_block"):
+                  "ga_attention_block", "ga_merge_plan"):
             getattr(L, f).restype = ctypes.c_int
         L.ga_timing_enable.argtypes = [ctypes.c_int]
         L.ga_timing_enable.restype = ctypes.c_int
@@ -233,6 +237,33 @@ def attention_block(X: torch.Tensor, Wqkv: torch.Tensor, Wo: torch.Tensor, H: in
     _check(lib().ga_attention_block(s, _p(X), _p(Wqkv), _p(Wo), int(N), int(iters), scale, _p(Y), _p(ws),
                                     ws.numel(), _stream(X.device)))
     return Y
+
+
+def merge_plan(Q: torch.Tensor, K: torch.Tensor, belong: torch.Tensor, centroid: torch.Tensor,
+               count: torch.Tensor, N: int, scale: float | None = None, eps: float = 2.0) -> dict:
+    """Merge plan of the adaptive group count (Lemma 1 threshold, Eq. 5 rule):
+    dict(radius [B,H,N] fp64, dthr [B,H] fp64, partner [B,H,N] int32, merges [B,H] int32)."""
+    s = shape_of(K)
+    dev = K.device
+    B, H = K.shape[:2]
+    scale = 1.0 / math.sqrt(K.shape[3]) if scale is None else float(scale)
+    radius = torch.empty((B, H, N), dtype=torch.float64, device=dev)
+    dthr = torch.empty((B, H), dtype=torch.float64, device=dev)
+    partner = torch.empty((B, H, N), dtype=torch.int32, device=dev)
+    merges = torch.empty((B, H), dtype=torch.int32, device=dev)
+    _check(lib().ga_merge_plan(s, _p(Q), _p(K), _p(belong), _p(centroid), _p(count), int(N), scale, float(eps),
+                               _p(radius), _p(dthr), _p(partner), _p(merges), _stream(dev)))
+    return dict(radius=radius, dthr=dthr, partner=partner, merges=merges)
+
+
+def next_group_count(N: int, merges, alpha: float) -> int:
+    """Momentum update of N from per-slice merge counts (copied to the host)."""
+    m = torch.as_tensor(merges).to("cpu", torch.int32).contiguous().reshape(-1)
+    r = lib().ga_next_group_count(int(N), ctypes.c_void_p(m.data_ptr()) if m.numel() else None, m.numel(),
+                                  float(alpha))
+    if r == 0:
+        raise GAError(1, lib().ga_last_error().decode())
+    return int(r)
 
 
 def timing_enable(on: bool = True) -> None:

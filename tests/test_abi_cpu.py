@@ -135,3 +135,39 @@ def test_block_entry_points_validate():
     assert blk(s, ws=FAKE + 64) == 3
     assert blk(s, nbytes=nb - 1) == 3
     assert blk(shape(B=0, H=8), ws=0) == 0
+
+
+def test_merge_plan_validates():
+    L = ga.lib()
+    s = shape(B=1, H=2, n=300)
+    mp = lambda s=s, N=16, scale=0.125, eps=2.0, Q=FAKE, radius=FAKE: L.ga_merge_plan(
+        s, P(Q), P(), P(), P(), P(), N, scale, eps, P(radius) if radius else None, P(), P(), P(), None)
+    assert mp(eps=1.0) == 1
+    assert mp(eps=0.5) == 1
+    assert mp(eps=float("inf")) == 1
+    assert mp(eps=float("nan")) == 1
+    assert mp(scale=float("nan")) == 1
+    assert mp(N=0) == 1
+    assert mp(s=shape(n=1000), N=300) == 2
+    assert mp(Q=0) == 1
+    assert mp(radius=0) == 1
+    assert mp(radius=FAKE + 8) == 1
+    assert mp(s=shape(B=0)) == 0
+
+
+def test_next_group_count_matches_the_definition(oracle_mod):
+    import numpy as np
+
+    L = ga.lib()
+    rng = np.random.default_rng(0)
+    for _ in range(300):
+        N = int(rng.integers(1, 1025))
+        m = rng.integers(0, N + 3, size=int(rng.integers(1, 40))).astype(np.int32)
+        alpha = float(rng.choice([0.0, 1.0, rng.uniform()]))
+        got = L.ga_next_group_count(N, m.ctypes.data_as(ctypes.c_void_p), m.size, alpha)
+        assert got == oracle_mod.next_group_count(N, m, alpha), (N, m, alpha)
+    assert L.ga_next_group_count(10, None, 0, 0.5) == 10
+    assert L.ga_next_group_count(0, None, 0, 0.5) == 0
+    assert L.ga_next_group_count(10, None, 0, 1.5) == 0
+    assert L.ga_next_group_count(10, None, 3, 0.5) == 0
+    assert ga.lib().ga_last_error().decode() != ""
