@@ -211,3 +211,37 @@ def attention_block(X, Wqkv, Wo, H: int, N: int, iters: int, scale: float):
     O = round_bf16_f64(r["O"])
     Y = project_out(O, Wo)
     return dict(Y=Y, Q=Q, K=K, V=V, O=O, belong=r["belong"], count=r["count"], centroid=r["centroid"])
+
+
+def backward(Q, dO, belong, centroid, count, vsum, N: int, scale: float, dtype: str):
+    """Gradient of the group-attention forward (Eq. 3, Algorithm 1) with the
+    grouping held fixed (BELONG / COUNT are piecewise constant in the keys).
+    r_j = round_dt(centroid_j) with the rounding passed straight through, so
+    dr_j reaches every member key as dr_j / c_j (r_j is the member mean);
+    mu_j = vsum_j / c_j reaches every member value as dmu_j / c_j.  fp64.
+    Returns (dQ, dK, dV), each [B, H, n, d]."""
+    Q, G = _f64(Q), _f64(dO)
+    B, H, n, d = Q.shape
+    C = _f64(centroid)
+    R = round_bf16_f64(C) if dtype == "bf16" else C
+    c = np.asarray(count, np.float64)
+    cs = np.where(c > 0, c, 1.0)
+    mu = np.where((c > 0)[..., None], _f64(vsum) / cs[..., None], 0.0)
+    p = scale * np.einsum("bhid,bhjd->bhij", Q, R)
+    live = (c > 0)[:, :, None, :]
+    m = np.max(np.where(live, p, -np.inf), axis=-1, keepdims=True)
+    m = np.where(np.isfinite(m), m, 0.0)
+    e = np.where(live, c[:, :, None, :] * np.exp(p - m), 0.0)
+    S = e.sum(-1, keepdims=True)
+    w = np.where(S > 0, e / np.where(S > 0, S, 1.0), 0.0)
+    dw = np.einsum("bhid,bhjd->bhij", G, mu)
+    D = (w * dw).sum(-1, keepdims=True)
+    dp = w * (dw - D)
+    dQ = scale * np.einsum("bhij,bhjd->bhid", dp, R)
+    dr = scale * np.einsum("bhij,bhid->bhjd", dp, Q)
+    dmu = np.einsum("bhij,bhid->bhjd", w, G)
+    idx = np.asarray(belong, np.int64)[..., None]
+    per_k = np.take_along_axis(cs, idx[..., 0], axis=2)[..., None]
+    dK = np.take_along_axis(dr, idx, axis=2) / per_k
+    dV = np.take_along_axis(dmu, idx, axis=2) / per_k
+    return dQ, dK, dV
