@@ -202,6 +202,26 @@ int ga_merge_plan(ga_shape_t s, const void *Q, const void *K, const int32_t *bel
 int32_t ga_next_group_count(int32_t N, const int32_t *merges, int64_t slices, double alpha);
 
 /*
+ * Backward pass of group attention (bf16; N <= 128), the gradient with the
+ * grouping held fixed (BELONG / COUNT are piecewise constant in the keys; the
+ * paper states no gradient rule).  With w_ij = c_j e^{p_ij} / sum_l c_l e^{p_il}
+ * (the normalised group weights of Eq. 3), mu_j = vsum_j / c_j and G = dO:
+ *   dp_ij = w_ij (G_i . mu_j - G_i . o_i),   dQ_i = scale sum_j dp_ij r_j,
+ *   dK_k = scale sum_i dp_{i a_k} q_i / c_{a_k}   (r_j is the member mean;
+ *          its bf16 rounding is passed straight through),
+ *   dV_k = sum_i w_{i a_k} G_i / c_{a_k}.
+ * Inputs: Q, dO [B,H,n,d] bf16; belong, centroid, count as from ga_cluster;
+ * vsum [B,H,N,d] fp32 (ga_aggregate).  Outputs dQ, dK, dV [B,H,n,d] bf16.
+ * Workspace: ga_backward_workspace_bytes(s, N) (0 if unsupported).
+ * Accuracy versus the fp64 definition: 2e-2 relative (bf16 operands, fp32
+ * accumulation).  Deterministic: every reduction has a fixed order.
+ */
+size_t ga_backward_workspace_bytes(ga_shape_t s, int32_t N);
+int ga_backward(ga_shape_t s, const void *Q, const void *dO, const int32_t *belong, const float *centroid,
+                const int32_t *count, const float *vsum, int32_t N, float scale, void *dQ, void *dK, void *dV,
+                void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Per-kernel timing for measurement tools.  While enabled (per calling
  * thread), every kernel launch of this library is bracketed by a pair of
  * hipEvents recorded on the launch stream.  ga_timing_collect waits for the

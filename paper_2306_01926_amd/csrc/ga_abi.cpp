@@ -446,6 +446,47 @@ int32_t ga_next_group_count(int32_t N, const int32_t* merges, int64_t slices, do
   return r < 1.0 ? 1 : (r > N ? N : (int32_t)r);
 }
 
+size_t ga_backward_workspace_bytes(ga_shape_t s, int32_t N) {
+  bool empty;
+  const std::string keep = g_last_error;
+  const int rc = check_shape(s, N, &empty);
+  g_last_error = keep;
+  if (rc != GA_OK || s.dtype != GA_BF16 || N > ga::backward_max_groups()) return 0;
+  return ga::backward_workspace_layout(dims_of(s, N), nullptr, nullptr);
+}
+
+int ga_backward(ga_shape_t s, const void* Q, const void* dO, const int32_t* belong, const float* centroid,
+                const int32_t* count, const float* vsum, int32_t N, float scale, void* dQ, void* dK, void* dV,
+                void* workspace, size_t workspace_bytes, void* stream) {
+  bool empty;
+  GA_TRY(check_shape(s, N, &empty));
+  if (s.dtype != GA_BF16) return fail(GA_ERR_UNSUPPORTED, "the backward pass is bf16 only");
+  if (N > ga::backward_max_groups())
+    return fail(GA_ERR_UNSUPPORTED, "the backward pass supports N <= %d (got %d)", ga::backward_max_groups(), N);
+  if (!isfinite(scale)) return fail(GA_ERR_INVALID_ARG, "scale must be finite");
+  GA_TRY(check_ptr(Q, "Q", true));
+  GA_TRY(check_ptr(dO, "dO", true));
+  GA_TRY(check_ptr(belong, "belong", true));
+  GA_TRY(check_ptr(centroid, "centroid", true));
+  GA_TRY(check_ptr(count, "count", true));
+  GA_TRY(check_ptr(vsum, "vsum", true));
+  GA_TRY(check_ptr(dQ, "dQ", true));
+  GA_TRY(check_ptr(dK, "dK", true));
+  GA_TRY(check_ptr(dV, "dV", true));
+  if (empty) return GA_OK;
+  const ga::Dims d = dims_of(s, N);
+  const size_t need = ga::backward_workspace_layout(d, nullptr, nullptr);
+  if (!workspace) return fail(GA_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (((uintptr_t)workspace & 255u) != 0) return fail(GA_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(GA_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+  ga::BackwardWorkspace w;
+  ga::backward_workspace_layout(d, &w, workspace);
+  GA_LAUNCH(ga::launch_backward(d, Q, dO, belong, centroid, count, vsum, scale, dQ, dK, dV, w, (hipStream_t)stream),
+            "backward launch");
+  return GA_OK;
+}
+
 const char* ga_status_string(int status) {
   switch (status) {
     case GA_OK: return "GA_OK";

@@ -1,0 +1,470 @@
+// gfx950 (MI355X) backward pass of group attention (bf16 storage, fp32
+// accumulation).
+//
+// Forward (Eq. 3, Algorithm 1) for query i and group j with c_j members,
+// representative r_j and value mean mu_j = vsum_j / c_j:
+//   p_ij = scale q_i . r_j,   w_ij = c_j e^{p_ij} / sum_l c_l e^{p_il},
+//   o_i = sum_j w_ij mu_j.
+// The grouping (BELONG, COUNT) is piecewise constant in the keys, so the
+// gradient treats it as fixed; r_j is the centroid (the mean of the member
+// keys; bf16 rounding passed straight through) and mu_j the mean of the member
+// values.  Given G = dL/dO:
+//   dw_ij = G_i . mu_j,   D_i = sum_j w_ij dw_ij (= G_i . o_i),
+//   dp_ij = w_ij (dw_ij - D_i),
+//   dQ_i = scale sum_j dp_ij r_j,
+//   dr_j = scale sum_i dp_ij q_i  ->  dK_k = dr_{a_k} / c_{a_k},
+//   dmu_j = sum_i w_ij G_i        ->  dV_k = dmu_{a_k} / c_{a_k}.
+//
+// Kernels (N <= 128, padded to Npad = 32 NB groups):
+//   k_bwd_prep    per slice: R = bf16(centroid) rows and transposed, bf16
+//                 value means, log2(count) (-inf for an empty group)
+//   k_bwd_query   per 32-query tile (lane = query): MFMA scores, the group
+//                 softmax, MFMA dw, D, dp, MFMA dQ; stores the softmax shift,
+//                 sum and D of every query
+//   k_bwd_group   per (32-group block, query chunk): the same scores and dw
+//                 in the transposed layout (lane = group), so that the dp and
+//                 w registers are directly the A operand of the MFMA
+//                 reductions dr += dp Q and dmu += w G; the four waves'
+//                 partials are added in a fixed order
+//   k_bwd_finish  per group: the chunk partials added in a fixed order,
+//                 scaled: scale dr / c and dmu / c
+//   k_bwd_keys    per key: the rows of its group to dK, dV (bf16)
+// Every reduction has a fixed order, so repeated calls give identical bits.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include "ga_internal.h"
+
+namespace ga {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kBs = 72;       // LDS row stride (bf16) of group rows and wave tiles
+constexpr int kBwdChunks = 8;  // query chunks per slice in k_bwd_group
+
+__device__ __forceinline__ uint32_t bf16_bits(float x) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x);  // round to nearest even
+}
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) { return bf16_bits(lo) | (bf16_bits(hi) << 16); }
+__device__ __forceinline__ f32x16 mfma(const u32x4& a, const u32x4& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                 0, 0);
+}
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) z[v] = 0.f;
+  return z;
+}
+// MFMA 32x32x16 layouts used below: the A operand of lane l is row l % 32, the
+// B operand column l % 32, each with 8 contraction indices chosen by lane half
+// h = l / 32; accumulator register v of lane l is row 8 (v / 4) + 4 h + v % 4,
+// column l % 32.  Features are contracted in the order 32 h + 8 s .. + 7 at
+// step s (both operands); groups or queries taken from accumulator registers
+// are contracted in the order {16 u + 4 h + j, 16 u + 8 + 4 h + j : j < 4} at
+// step u, the indices those registers hold.
+
+// Padded slice layout of the workspace (all per slice bh):
+//   R   [Npad][64] bf16,  RT [64][rts] bf16 (rts = Npad + 4),
+//   MU  [Npad][64] bf16,  LC [Npad] f32.
+__global__ __launch_bounds__(256) void k_bwd_prep(const float* __restrict__ centroid, const int32_t* __restrict__ count,
+                                                  const float* __restrict__ vsum, int N, int Npad, int rts,
+                                                  uint16_t* __restrict__ R, uint16_t* __restrict__ RT,
+                                                  uint16_t* __restrict__ MU, float* __restrict__ LC) {
+  const int64_t bh = blockIdx.x;
+  for (int x = threadIdx.x; x < Npad * 64; x += 256) {
+    const int g = x >> 6, c = x & 63;
+    const int cnt = g < N ? count[bh * N + g] : 0;
+    const float cv = g < N ? centroid[(bh * N + g) * 64 + c] : 0.f;
+    const float mv = cnt > 0 ? vsum[(bh * N + g) * 64 + c] / (float)cnt : 0.f;
+    const uint16_t rb = (uint16_t)bf16_bits(cv);
+    R[(bh * Npad + g) * 64 + c] = rb;
+    RT[(bh * 64 + c) * rts + g] = rb;
+    MU[(bh * Npad + g) * 64 + c] = (uint16_t)bf16_bits(mv);
+    if (c == 0) LC[bh * Npad + g] = cnt > 0 ? log2f((float)cnt) : -INFINITY;
+  }
+}
+
+// Stage a slice's R rows (A or B operand rows), value-mean rows and the count
+// logarithms in LDS.
+template <int NB>
+__device__ __forceinline__ void stage_groups(const uint16_t* __restrict__ R, const uint16_t* __restrict__ MU,
+                                             const float* __restrict__ LC, int64_t bh, uint16_t* Rs, uint16_t* Ms,
+                                             float* lc) {
+  constexpr int Npad = NB * 32;
+  for (int x = threadIdx.x; x < Npad * 8; x += 256) {
+    const int row = x >> 3, ch = x & 7;
+    *(u32x4*)(Rs + row * kBs + 8 * ch) = *(const u32x4*)(R + (bh * Npad + row) * 64 + 8 * ch);
+    *(u32x4*)(Ms + row * kBs + 8 * ch) = *(const u32x4*)(MU + (bh * Npad + row) * 64 + 8 * ch);
+  }
+  for (int g = threadIdx.x; g < Npad; g += 256) lc[g] = LC[bh * Npad + g];
+}
+
+// lane (row, h) loads features 32 h .. 32 h + 31 of row `row` (clamped): the
+// operand fragments of the 4 feature steps
+__device__ __forceinline__ void load_row_frags(const uint16_t* __restrict__ X, int64_t row, u32x4 (&f)[4]) {
+  const int h = (threadIdx.x & 63) >> 5;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) f[s] = *(const u32x4*)(X + row * 64 + 32 * h + 8 * s);
+}
+
+// grid (ceil(tiles / (4 tpw)), BH), 256 threads: wave tiles of 32 queries.
+template <int NB>
+__global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ G,
+                                                   const uint16_t* __restrict__ R, const uint16_t* __restrict__ RT,
+                                                   const uint16_t* __restrict__ MU, const float* __restrict__ LC,
+                                                   int n, int rts, float scale, float sl2e, int tpw,
+                                                   uint16_t* __restrict__ dQ, float4* __restrict__ stats) {
+  constexpr int Npad = NB * 32;
+  __shared__ __attribute__((aligned(16))) uint16_t Rs[Npad * kBs];
+  __shared__ __attribute__((aligned(16))) uint16_t Ms[Npad * kBs];
+  __shared__ __attribute__((aligned(16))) uint16_t RTs[64 * (Npad + 4)];
+  __shared__ float lc[Npad];
+  __shared__ __attribute__((aligned(16))) uint16_t Ot[4][32 * kBs];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
+  const int64_t bh = blockIdx.y;
+  stage_groups<NB>(R, MU, LC, bh, Rs, Ms, lc);
+  for (int x = tid; x < 64 * (Npad / 4); x += 256) {
+    const int row = x / (Npad / 4), ch = x % (Npad / 4);
+    *(u32x2*)(RTs + row * (Npad + 4) + 4 * ch) = *(const u32x2*)(RT + (bh * 64 + row) * rts + 4 * ch);
+  }
+  __syncthreads();
+  const int64_t ntiles = ((int64_t)n + 31) / 32;
+  const int64_t t0 = ((int64_t)blockIdx.x * 4 + wave) * tpw;
+  const uint16_t* Qb = Q + bh * (int64_t)n * 64;
+  const uint16_t* Gb = G + bh * (int64_t)n * 64;
+  uint16_t* Ow = Ot[wave];
+  for (int64_t t = t0; t < min(t0 + tpw, ntiles); ++t) {
+    const int64_t qi = t * 32 + q;
+    u32x4 qf[4], gf[4];
+    load_row_frags(Qb, min(qi, (int64_t)n - 1), qf);
+    load_row_frags(Gb, min(qi, (int64_t)n - 1), gf);
+    // scores x_gq = sl2e (r_g . q) + log2 c_g and dw_gq = mu_g . G_q (rows g, column q)
+    f32x16 x[NB], dw[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      f32x16 a = zero16(), d = zero16();
+      const uint16_t* rr = Rs + (32 * b + q) * kBs + 32 * h;
+      const uint16_t* mr = Ms + (32 * b + q) * kBs + 32 * h;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        a = mfma(*(const u32x4*)(rr + 8 * s), qf[s], a);
+        d = mfma(*(const u32x4*)(mr + 8 * s), gf[s], d);
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) a[v] = fmaf(a[v], sl2e, lc[32 * b + 8 * (v >> 2) + 4 * h + (v & 3)]);
+      x[b] = a;
+      dw[b] = d;
+    }
+    float M = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) M = fmaxf(M, x[b][v]);
+    M = fmaxf(M, __shfl_xor(M, 32));
+    const bool any = M != -INFINITY;  // some group is non-empty
+    const float Ms_ = any ? M : 0.f;
+    float S = 0.f;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        x[b][v] = __builtin_amdgcn_exp2f(x[b][v] - Ms_);  // e (0 for an empty group)
+        S += x[b][v];
+      }
+    S += __shfl_xor(S, 32);
+    const float inv = any ? 1.0f / S : 0.f;
+    float Dq = 0.f;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        x[b][v] *= inv;  // w
+        Dq = fmaf(x[b][v], dw[b][v], Dq);
+      }
+    Dq += __shfl_xor(Dq, 32);
+    // dQ^T[f][q] = sum_g r_gf dp_gq: A = R^T rows (features), B = dp from the registers
+    f32x16 o0 = zero16(), o1 = zero16();
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      float dp[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) dp[v] = x[b][v] * (dw[b][v] - Dq);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const u32x4 bf = {pack2(dp[8 * u], dp[8 * u + 1]), pack2(dp[8 * u + 2], dp[8 * u + 3]),
+                          pack2(dp[8 * u + 4], dp[8 * u + 5]), pack2(dp[8 * u + 6], dp[8 * u + 7])};
+        const int gcol = 32 * b + 16 * u + 4 * h;
+        const uint16_t* r0 = RTs + q * (Npad + 4) + gcol;
+        const uint16_t* r1 = RTs + (32 + q) * (Npad + 4) + gcol;
+        const u32x2 a0l = *(const u32x2*)r0, a0h = *(const u32x2*)(r0 + 8);
+        const u32x2 a1l = *(const u32x2*)r1, a1h = *(const u32x2*)(r1 + 8);
+        o0 = mfma(u32x4{a0l[0], a0l[1], a0h[0], a0h[1]}, bf, o0);
+        o1 = mfma(u32x4{a1l[0], a1l[1], a1h[0], a1h[1]}, bf, o1);
+      }
+    }
+    // dQ rows through the wave's LDS tile: lane (q, h) holds features 8 k + 4 h + j
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      *(u32x2*)(Ow + q * kBs + 8 * k + 4 * h) = u32x2{pack2(scale * o0[4 * k], scale * o0[4 * k + 1]),
+                                                      pack2(scale * o0[4 * k + 2], scale * o0[4 * k + 3])};
+      *(u32x2*)(Ow + q * kBs + 32 + 8 * k + 4 * h) = u32x2{pack2(scale * o1[4 * k], scale * o1[4 * k + 1]),
+                                                           pack2(scale * o1[4 * k + 2], scale * o1[4 * k + 3])};
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = 8 * k + (lane >> 3), ch = lane & 7;
+      const int64_t qo = t * 32 + row;
+      if (qo < n) *(u32x4*)(dQ + (bh * (int64_t)n + qo) * 64 + 8 * ch) = *(const u32x4*)(Ow + row * kBs + 8 * ch);
+    }
+    if (h == 0 && qi < n) stats[bh * (int64_t)n + qi] = make_float4(Ms_, any ? S : 1.f, Dq, 0.f);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
+// grid (NB, kBwdChunks, BH), 256 threads: group block b of a slice over query
+// chunk c (tiles [c T / chunks, (c + 1) T / chunks), wave w takes every 4th).
+// part[bh][c][0/1][g][f] = this chunk's sum_i dp_gi q_if / sum_i w_gi G_if.
+template <int NB>
+__global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ G,
+                                                   const uint16_t* __restrict__ R, const uint16_t* __restrict__ MU,
+                                                   const float* __restrict__ LC, const float4* __restrict__ stats,
+                                                   int n, float sl2e, float* __restrict__ part) {
+  constexpr int Npad = NB * 32;
+  __shared__ __attribute__((aligned(16))) uint16_t Rs[Npad * kBs];
+  __shared__ __attribute__((aligned(16))) uint16_t Ms[Npad * kBs];
+  __shared__ float lc[Npad];
+  __shared__ __attribute__((aligned(16))) uint16_t Qt[4][32 * kBs], Gt[4][32 * kBs];
+  __shared__ float4 st[4][32];
+  __shared__ float red[4][2][32 * 64];  // per-wave partials, added in wave order
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, gl = lane & 31;
+  const int b = blockIdx.x, chunk = blockIdx.y;
+  const int64_t bh = blockIdx.z;
+  stage_groups<NB>(R, MU, LC, bh, Rs, Ms, lc);
+  __syncthreads();
+  const int64_t ntiles = ((int64_t)n + 31) / 32;
+  const int64_t c0 = chunk * ntiles / gridDim.y, c1 = (chunk + 1) * ntiles / gridDim.y;
+  const uint16_t* Qb = Q + bh * (int64_t)n * 64;
+  const uint16_t* Gb = G + bh * (int64_t)n * 64;
+  const int g = 32 * b + gl;  // this lane's group (MFMA column / A-operand row)
+  const float lcg = lc[g];
+  uint16_t *Qw = Qt[wave], *Gw = Gt[wave];
+  f32x16 dr0 = zero16(), dr1 = zero16(), dm0 = zero16(), dm1 = zero16();
+  for (int64_t t = c0 + wave; t < c1; t += 4) {
+    // lane (row = query gl, h): its query's features as A fragments, also
+    // kept row-major in the wave's tile for the transposed reads below
+    const int64_t qi = t * 32 + gl;
+    u32x4 qf[4], gf[4];
+    load_row_frags(Qb, min(qi, (int64_t)n - 1), qf);
+    load_row_frags(Gb, min(qi, (int64_t)n - 1), gf);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      *(u32x4*)(Qw + gl * kBs + 32 * h + 8 * s) = qf[s];
+      *(u32x4*)(Gw + gl * kBs + 32 * h + 8 * s) = gf[s];
+    }
+    if (h == 0) st[wave][gl] = qi < n ? stats[bh * (int64_t)n + qi] : make_float4(0.f, 1.f, 0.f, 0.f);
+    // scores and dw with queries as rows, groups as columns
+    f32x16 x = zero16(), dw = zero16();
+    const uint16_t* rr = Rs + g * kBs + 32 * h;
+    const uint16_t* mr = Ms + g * kBs + 32 * h;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      x = mfma(qf[s], *(const u32x4*)(rr + 8 * s), x);
+      dw = mfma(gf[s], *(const u32x4*)(mr + 8 * s), dw);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // register v: query 8 (v / 4) + 4 h + v % 4 of the tile; padded queries get w = 0
+    float w[16], dp[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int r = 8 * (v >> 2) + 4 * h + (v & 3);
+      const float4 sq = st[wave][r];
+      const float e = __builtin_amdgcn_exp2f(fmaf(x[v], sl2e, lcg) - sq.x);
+      w[v] = t * 32 + r < n ? e / sq.y : 0.f;
+      dp[v] = w[v] * (dw[v] - sq.z);
+    }
+    // dr[g][f] += sum_q dp[g][q] Q[q][f]; dmu[g][f] += sum_q w[g][q] G[q][f]
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const u32x4 adp = {pack2(dp[8 * u], dp[8 * u + 1]), pack2(dp[8 * u + 2], dp[8 * u + 3]),
+                         pack2(dp[8 * u + 4], dp[8 * u + 5]), pack2(dp[8 * u + 6], dp[8 * u + 7])};
+      const u32x4 aw = {pack2(w[8 * u], w[8 * u + 1]), pack2(w[8 * u + 2], w[8 * u + 3]),
+                        pack2(w[8 * u + 4], w[8 * u + 5]), pack2(w[8 * u + 6], w[8 * u + 7])};
+      const int r0 = 16 * u + 4 * h;  // queries r0 .. r0 + 3 and r0 + 8 .. r0 + 11
+      u32x4 bq[2], bg[2];
+#pragma unroll
+      for (int fb = 0; fb < 2; ++fb) {
+        const int f = 32 * fb + gl;
+        uint32_t vq[8], vg[8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          vq[j] = Qw[(r0 + j) * kBs + f];
+          vq[4 + j] = Qw[(r0 + 8 + j) * kBs + f];
+          vg[j] = Gw[(r0 + j) * kBs + f];
+          vg[4 + j] = Gw[(r0 + 8 + j) * kBs + f];
+        }
+        bq[fb] = u32x4{vq[0] | (vq[1] << 16), vq[2] | (vq[3] << 16), vq[4] | (vq[5] << 16), vq[6] | (vq[7] << 16)};
+        bg[fb] = u32x4{vg[0] | (vg[1] << 16), vg[2] | (vg[3] << 16), vg[4] | (vg[5] << 16), vg[6] | (vg[7] << 16)};
+      }
+      dr0 = mfma(adp, bq[0], dr0);
+      dr1 = mfma(adp, bq[1], dr1);
+      dm0 = mfma(aw, bg[0], dm0);
+      dm1 = mfma(aw, bg[1], dm1);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  // accumulator register v of lane (col = feature gl, h): group row 8 (v / 4) + 4 h + v % 4
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int gr = 8 * (v >> 2) + 4 * h + (v & 3);
+    red[wave][0][gr * 64 + gl] = dr0[v];
+    red[wave][0][gr * 64 + 32 + gl] = dr1[v];
+    red[wave][1][gr * 64 + gl] = dm0[v];
+    red[wave][1][gr * 64 + 32 + gl] = dm1[v];
+  }
+  __syncthreads();
+  float* out = part + ((bh * gridDim.y + chunk) * 2) * (int64_t)Npad * 64;
+  for (int x = tid; x < 2 * 32 * 64; x += 256) {
+    const int k = x / (32 * 64), e = x % (32 * 64);
+    const float s = ((red[0][k][e] + red[1][k][e]) + red[2][k][e]) + red[3][k][e];
+    out[(int64_t)k * Npad * 64 + 32 * b * 64 + e] = s;
+  }
+}
+
+// grid (Npad / 4, BH), 256 threads: thread = (group, feature) of 4 groups.
+// gk = scale sum_chunks dr / c, gv = sum_chunks dmu / c (0 for an empty group).
+__global__ __launch_bounds__(256) void k_bwd_finish(const float* __restrict__ part, const int32_t* __restrict__ count,
+                                                    int N, int Npad, int chunks, float scale, float* __restrict__ gk,
+                                                    float* __restrict__ gv) {
+  const int64_t bh = blockIdx.y;
+  const int g = blockIdx.x * 4 + (threadIdx.x >> 6), f = threadIdx.x & 63;
+  if (g >= N) return;
+  float sr = 0.f, sm = 0.f;
+  for (int c = 0; c < chunks; ++c) {
+    const float* p = part + ((bh * chunks + c) * 2) * (int64_t)Npad * 64;
+    sr += p[g * 64 + f];
+    sm += p[(int64_t)Npad * 64 + g * 64 + f];
+  }
+  const int cnt = count[bh * N + g];
+  gk[(bh * Npad + g) * 64 + f] = cnt > 0 ? scale * sr / (float)cnt : 0.f;
+  gv[(bh * Npad + g) * 64 + f] = cnt > 0 ? sm / (float)cnt : 0.f;
+}
+
+// grid (ceil(n / 32), BH), 256 threads: 8 lanes per key row.
+__global__ __launch_bounds__(256) void k_bwd_keys(const int32_t* __restrict__ belong, const float* __restrict__ gk,
+                                                  const float* __restrict__ gv, int n, int N, int Npad,
+                                                  uint16_t* __restrict__ dK, uint16_t* __restrict__ dV) {
+  const int64_t bh = blockIdx.y;
+  const int k = blockIdx.x * 32 + (threadIdx.x >> 3), ch = threadIdx.x & 7;
+  if (k >= n) return;
+  const int g = belong[bh * n + k];
+  u32x4 ok = {0u, 0u, 0u, 0u}, ov = {0u, 0u, 0u, 0u};
+  if ((unsigned)g < (unsigned)N) {
+    const float* rk = gk + (bh * Npad + g) * 64 + 8 * ch;
+    const float* rv = gv + (bh * Npad + g) * 64 + 8 * ch;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      ok[e] = pack2(rk[2 * e], rk[2 * e + 1]);
+      ov[e] = pack2(rv[2 * e], rv[2 * e + 1]);
+    }
+  }
+  *(u32x4*)(dK + (bh * n + k) * 64 + 8 * ch) = ok;
+  *(u32x4*)(dV + (bh * n + k) * 64 + 8 * ch) = ov;
+}
+
+int bwd_npad(int N) { return (N + 31) / 32 * 32; }
+int bwd_rts(int N) { return bwd_npad(N) + 4; }
+
+}  // namespace
+
+int backward_max_groups() { return 128; }
+
+size_t backward_workspace_layout(const Dims& d, BackwardWorkspace* w, void* base) {
+  const int Npad = bwd_npad(d.N), rts = bwd_rts(d.N);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += (bytes + 255) & ~(size_t)255;
+    return base ? (char*)base + o : nullptr;
+  };
+  void* R = take((size_t)d.BH * Npad * 64 * 2);
+  void* RT = take((size_t)d.BH * 64 * rts * 2);
+  void* MU = take((size_t)d.BH * Npad * 64 * 2);
+  void* LC = take((size_t)d.BH * Npad * 4);
+  void* ST = take((size_t)d.BH * d.n * 16);
+  void* PART = take((size_t)d.BH * kBwdChunks * 2 * Npad * 64 * 4);
+  void* GK = take((size_t)d.BH * Npad * 64 * 4);
+  void* GV = take((size_t)d.BH * Npad * 64 * 4);
+  if (w) *w = BackwardWorkspace{(uint16_t*)R, (uint16_t*)RT, (uint16_t*)MU, (float*)LC, ST, (float*)PART,
+                                (float*)GK, (float*)GV};
+  return off;
+}
+
+hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const int32_t* belong,
+                           const float* centroid, const int32_t* count, const float* vsum, float scale, void* dQ,
+                           void* dK, void* dV, const BackwardWorkspace& w, hipStream_t st) {
+  const int Npad = bwd_npad(d.N), rts = bwd_rts(d.N), NB = Npad / 32;
+  const float sl2e = scale * 1.4426950408889634f;
+  {
+    TimedLaunch tl("bwd_prep", st);
+    hipLaunchKernelGGL(k_bwd_prep, dim3((unsigned)d.BH), dim3(256), 0, st, centroid, count, vsum, d.N, Npad, rts, w.R,
+                       w.RT, w.MU, w.LC);
+  }
+  const int64_t ntiles = ((int64_t)d.n + 31) / 32;
+  const int tpw = (int)((ntiles + 31) / 32);  // about 8 workgroups per slice
+  const unsigned gq = (unsigned)((ntiles + 4 * tpw - 1) / (4 * tpw));
+  {
+    TimedLaunch tl("bwd_query", st);
+#define GA_BWD_Q(NBV)                                                                                              \
+  hipLaunchKernelGGL(k_bwd_query<NBV>, dim3(gq, (unsigned)d.BH), dim3(256), 0, st, (const uint16_t*)Q,            \
+                     (const uint16_t*)dO, w.R, w.RT, w.MU, w.LC, d.n, rts, scale, sl2e, tpw, (uint16_t*)dQ,       \
+                     (float4*)w.stats)
+    switch (NB) {
+      case 1: GA_BWD_Q(1); break;
+      case 2: GA_BWD_Q(2); break;
+      case 3: GA_BWD_Q(3); break;
+      default: GA_BWD_Q(4); break;
+    }
+#undef GA_BWD_Q
+  }
+  {
+    TimedLaunch tl("bwd_group", st);
+#define GA_BWD_G(NBV)                                                                                              \
+  hipLaunchKernelGGL(k_bwd_group<NBV>, dim3(NBV, kBwdChunks, (unsigned)d.BH), dim3(256), 0, st,                   \
+                     (const uint16_t*)Q, (const uint16_t*)dO, w.R, w.MU, w.LC, (const float4*)w.stats, d.n, sl2e, \
+                     w.part)
+    switch (NB) {
+      case 1: GA_BWD_G(1); break;
+      case 2: GA_BWD_G(2); break;
+      case 3: GA_BWD_G(3); break;
+      default: GA_BWD_G(4); break;
+    }
+#undef GA_BWD_G
+  }
+  {
+    TimedLaunch tl("bwd_finish", st);
+    hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 4), (unsigned)d.BH), dim3(256), 0, st, w.part, count, d.N,
+                       Npad, kBwdChunks, scale, w.gk, w.gv);
+  }
+  TimedLaunch tl("bwd_keys", st);
+  hipLaunchKernelGGL(k_bwd_keys, dim3((unsigned)((d.n + 31) / 32), (unsigned)d.BH), dim3(256), 0, st, belong, w.gk,
+                     w.gv, d.n, d.N, Npad, (uint16_t*)dK, (uint16_t*)dV);
+  return hipGetLastError();
+}
+
+}  // namespace ga

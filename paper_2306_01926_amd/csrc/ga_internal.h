@@ -122,4 +122,21 @@ hipError_t launch_merge_plan(const Dims& d, const void* Q, const void* K, const 
                              const float* centroid, const int32_t* count, double abs_scale, double log_eps,
                              double* radius, double* dthr, int32_t* partner, int32_t* merges, hipStream_t st);
 
+// Backward pass (ga_backward.hip), bf16, N <= backward_max_groups().
+struct BackwardWorkspace {
+  uint16_t* R;   // [BH][Npad][64] bf16 representatives
+  uint16_t* RT;  // [BH][64][Npad + 4] the same, transposed
+  uint16_t* MU;  // [BH][Npad][64] bf16 value means
+  float* LC;     // [BH][Npad] log2(count), -inf for an empty group
+  void* stats;   // [BH][n] float4: softmax shift, sum, D = dO . o per query
+  float* part;   // [BH][chunks][2][Npad][64] per-chunk sums of dp q and w dO
+  float* gk;     // [BH][Npad][64] scale dr / count
+  float* gv;     // [BH][Npad][64] dmu / count
+};
+int backward_max_groups();
+size_t backward_workspace_layout(const Dims& d, BackwardWorkspace* w, void* base);  // returns bytes
+hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const int32_t* belong,
+                           const float* centroid, const int32_t* count, const float* vsum, float scale, void* dQ,
+                           void* dK, void* dV, const BackwardWorkspace& w, hipStream_t st);
+
 }  // namespace ga

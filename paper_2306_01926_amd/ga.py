@@ -19,7 +19,7 @@ GA_F32, GA_BF16 = 0, 1
 STATUS = {0: "GA_OK", 1: "GA_ERR_INVALID_ARG", 2: "GA_ERR_UNSUPPORTED", 3: "GA_ERR_WORKSPACE", 4: "GA_ERR_HIP"}
 SYMBOLS = ("ga_workspace_bytes", "ga_cluster", "ga_aggregate", "ga_attend", "ga_forward",
            "ga_block_workspace_bytes", "ga_project_qkv", "ga_project_out", "ga_attention_block",
-           "ga_merge_plan", "ga_next_group_count",
+           "ga_merge_plan", "ga_next_group_count", "ga_backward_workspace_bytes", "ga_backward",
            "ga_timing_enable", "ga_timing_collect", "ga_status_string", "ga_last_error")
 
 
@@ -61,10 +61,13 @@ def lib() -> ctypes.CDLL:
         L.ga_project_out.argtypes = [Shape, P, P, P, P]
         L.ga_attention_block.argtypes = [Shape, P, P, P, i32, i32, ctypes.c_float, P, P, ctypes.c_size_t, P]
         L.ga_merge_plan.argtypes = [Shape, P, P, P, P, P, i32, ctypes.c_float, ctypes.c_double, P, P, P, P, P]
+        L.ga_backward_workspace_bytes.argtypes = [Shape, i32]
+        L.ga_backward_workspace_bytes.restype = ctypes.c_size_t
+        L.ga_backward.argtypes = [Shape, P, P, P, P, P, P, i32, ctypes.c_float, P, P, P, P, ctypes.c_size_t, P]
         L.ga_next_group_count.argtypes = [i32, P, ctypes.c_int64, ctypes.c_double]
         L.ga_next_group_count.restype = i32
         for f in ("ga_cluster", "ga_aggregate", "ga_attend", "ga_forward", "ga_project_qkv", "ga_project_out",
-                  "ga_attention_block", "ga_merge_plan"):
+                  "ga_attention_block", "ga_merge_plan", "ga_backward"):
             getattr(L, f).restype = ctypes.c_int
         L.ga_timing_enable.argtypes = [ctypes.c_int]
         L.ga_timing_enable.restype = ctypes.c_int
@@ -264,6 +267,24 @@ def next_group_count(N: int, merges, alpha: float) -> int:
     if r == 0:
         raise GAError(1, lib().ga_last_error().decode())
     return int(r)
+
+
+def backward_workspace_bytes(shape: Shape, N: int) -> int:
+    return int(lib().ga_backward_workspace_bytes(shape, int(N)))
+
+
+def backward(Q: torch.Tensor, dO: torch.Tensor, belong: torch.Tensor, centroid: torch.Tensor, count: torch.Tensor,
+             vsum: torch.Tensor, N: int, scale: float | None = None, ws=None):
+    """Gradient of the forward with the grouping fixed: (dQ, dK, dV) [B,H,n,d] bf16."""
+    s = shape_of(Q)
+    dev = Q.device
+    scale = 1.0 / math.sqrt(Q.shape[3]) if scale is None else float(scale)
+    dQ, dK, dV = (torch.empty_like(Q) for _ in range(3))
+    if ws is None:
+        ws = torch.empty(max(backward_workspace_bytes(s, N), 256), dtype=torch.uint8, device=dev)
+    _check(lib().ga_backward(s, _p(Q), _p(dO), _p(belong), _p(centroid), _p(count), _p(vsum), int(N), scale, _p(dQ),
+                             _p(dK), _p(dV), _p(ws), ws.numel(), _stream(dev)))
+    return dQ, dK, dV
 
 
 def timing_enable(on: bool = True) -> None:

@@ -171,3 +171,23 @@ def test_next_group_count_matches_the_definition(oracle_mod):
     assert L.ga_next_group_count(10, None, 0, 1.5) == 0
     assert L.ga_next_group_count(10, None, 3, 0.5) == 0
     assert ga.lib().ga_last_error().decode() != ""
+
+
+def test_backward_validates():
+    L = ga.lib()
+    s = shape(B=1, H=2, n=300)
+    nb = L.ga_backward_workspace_bytes(s, 64)
+    assert nb > 0
+    assert L.ga_backward_workspace_bytes(shape(dtype=ga.GA_F32), 8) == 0
+    assert L.ga_backward_workspace_bytes(s, 200) == 0
+    bw = lambda s=s, N=64, scale=0.125, dQ=FAKE, ws=FAKE, nbytes=nb: L.ga_backward(
+        s, P(), P(), P(), P(), P(), P(), N, scale, P(dQ) if dQ else None, P(), P(), P(ws) if ws else None, nbytes,
+        None)
+    assert bw(s=shape(dtype=ga.GA_F32)) == 2
+    assert bw(N=129) == 2
+    assert bw(N=0) == 1
+    assert bw(scale=float("inf")) == 1
+    assert bw(dQ=0) == 1
+    assert bw(ws=0) == 3
+    assert bw(nbytes=nb - 1) == 3
+    assert bw(s=shape(B=0)) == 0
