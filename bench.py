@@ -161,6 +161,36 @@ def main():
                      peak=HBM_PEAK_GBS, unit="GB/s", frac=mbytes / (avg / 1e3) / 1e9 / HBM_PEAK_GBS,
                      merges_min=int(plan["merges"].min()), next_N=ga.next_group_count(N, plan["merges"], 0.5))
 
+    # the backward pass (gradient with the grouping fixed) of the same forward
+    bwd = None
+    if w.dtype == "bf16" and N <= 128:
+        Q0, K0, V0 = sets[0]
+        _, bel0, cnt0, cen0 = ga.forward(Q0, K0, V0, N, w.iters, scale, return_groups=True, ws=ws)
+        vs0 = ga.aggregate(V0, bel0, N, ws=ws)
+        dO = torch.randn(Q0.shape, device=dev).to(torch.bfloat16)
+        bws = torch.empty(ga.backward_workspace_bytes(ga.shape_of(Q0), N), dtype=torch.uint8, device=dev)
+        for _ in range(2):
+            ga.backward(Q0, dO, bel0, cen0, cnt0, vs0, N, scale, ws=bws)
+        torch.cuda.synchronize()
+        t0.record()
+        for _ in range(args.steps):
+            ga.backward(Q0, dO, bel0, cen0, cnt0, vs0, N, scale, ws=bws)
+        t1.record()
+        torch.cuda.synchronize()
+        bms = t0.elapsed_time(t1) / args.steps
+        ga.timing_enable(True)
+        for _ in range(args.steps):
+            ga.backward(Q0, dO, bel0, cen0, cnt0, vs0, N, scale, ws=bws)
+        torch.cuda.synchronize()
+        ga.timing_enable(False)
+        tk = ga.timing_collect()
+        # algorithmic bytes: read q and dO, write dQ (3 rows per query); read
+        # the group and write dK and dV (4 B + 2 rows per key)
+        bbytes = BH * w.n * (3 * w.d * 2 + 4 + 2 * w.d * 2)
+        bwd = dict(ms=bms, launches={k: t / l for k, (l, t) in tk.items()}, bound="hbm",
+                   achieved=bbytes / (bms / 1e3) / 1e9, peak=HBM_PEAK_GBS, unit="GB/s",
+                   frac=bbytes / (bms / 1e3) / 1e9 / HBM_PEAK_GBS, queries_per_s=BH * w.n / (bms / 1e3))
+
     queries = BH * w.n
     es = 2 if w.dtype == "bf16" else 4
     compulsory = 4.0 * queries * w.d * es  # read Q, K, V once, write O once
@@ -230,7 +260,7 @@ def main():
         "pct_hbm_roofline": pct_hbm, "compulsory_bytes": compulsory,
         "roofline": roofline, "cpu_baseline": cpu,
         "kernels": kernels, "ms_per_step_with_kernel_events": ms_timed, "parity_sample": parity,
-        "scheduler": sched,
+        "scheduler": sched, "backward": bwd,
     }
     print(json.dumps(line), flush=True)
 

@@ -20,7 +20,7 @@
 //                 value means, log2(count) (-inf for an empty group)
 //   k_bwd_query   per 32-query tile (lane = query): MFMA scores, the group
 //                 softmax, MFMA dw, D, dp, MFMA dQ; stores the softmax shift,
-//                 sum and D of every query
+//                 1 / sum and D of every query
 //   k_bwd_group   per (32-group block, query chunk): the same scores and dw
 //                 in the transposed layout (lane = group), so that the dp and
 //                 w registers are directly the A operand of the MFMA
@@ -226,7 +226,7 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
       const int64_t qo = t * 32 + row;
       if (qo < n) *(u32x4*)(dQ + (bh * (int64_t)n + qo) * 64 + 8 * ch) = *(const u32x4*)(Ow + row * kBs + 8 * ch);
     }
-    if (h == 0 && qi < n) stats[bh * (int64_t)n + qi] = make_float4(Ms_, any ? S : 1.f, Dq, 0.f);
+    if (h == 0 && qi < n) stats[bh * (int64_t)n + qi] = make_float4(Ms_, inv, Dq, 0.f);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -242,12 +242,17 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
                                                    const float* __restrict__ LC, const float4* __restrict__ stats,
                                                    int n, float sl2e, float* __restrict__ part) {
   constexpr int Npad = NB * 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Rs[Npad * kBs];
-  __shared__ __attribute__((aligned(16))) uint16_t Ms[Npad * kBs];
+  // group rows and the waves' query tiles; after the loop the same bytes hold
+  // the per-wave partials [4][2][32][64] (added in wave order)
+  constexpr int kRows = 2 * Npad * kBs * 2, kTiles = 8 * 32 * kBs * 2, kRed = 4 * 2 * 32 * 64 * 4;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kRows + kTiles > kRed ? kRows + kTiles : kRed];
+  uint16_t* Rs = (uint16_t*)lds;
+  uint16_t* Ms = Rs + Npad * kBs;
+  uint16_t* Qt = Ms + Npad * kBs;  // [4][32][kBs]
+  uint16_t* Gt = Qt + 4 * 32 * kBs;
+  float* red = (float*)lds;
   __shared__ float lc[Npad];
-  __shared__ __attribute__((aligned(16))) uint16_t Qt[4][32 * kBs], Gt[4][32 * kBs];
   __shared__ float4 st[4][32];
-  __shared__ float red[4][2][32 * 64];  // per-wave partials, added in wave order
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, gl = lane & 31;
   const int b = blockIdx.x, chunk = blockIdx.y;
   const int64_t bh = blockIdx.z;
@@ -259,21 +264,33 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
   const uint16_t* Gb = G + bh * (int64_t)n * 64;
   const int g = 32 * b + gl;  // this lane's group (MFMA column / A-operand row)
   const float lcg = lc[g];
-  uint16_t *Qw = Qt[wave], *Gw = Gt[wave];
+  uint16_t *Qw = Qt + wave * 32 * kBs, *Gw = Gt + wave * 32 * kBs;
   f32x16 dr0 = zero16(), dr1 = zero16(), dm0 = zero16(), dm1 = zero16();
+  // the wave's next tile loads while the current one is processed
+  u32x4 qn[4], gn[4];
+  load_row_frags(Qb, min((c0 + wave) * 32 + gl, (int64_t)n - 1), qn);
+  load_row_frags(Gb, min((c0 + wave) * 32 + gl, (int64_t)n - 1), gn);
   for (int64_t t = c0 + wave; t < c1; t += 4) {
     // lane (row = query gl, h): its query's features as A fragments, also
     // kept row-major in the wave's tile for the transposed reads below
     const int64_t qi = t * 32 + gl;
     u32x4 qf[4], gf[4];
-    load_row_frags(Qb, min(qi, (int64_t)n - 1), qf);
-    load_row_frags(Gb, min(qi, (int64_t)n - 1), gf);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      qf[s] = qn[s];
+      gf[s] = gn[s];
+    }
+    if (t + 4 < c1) {
+      load_row_frags(Qb, min(qi + 128, (int64_t)n - 1), qn);
+      load_row_frags(Gb, min(qi + 128, (int64_t)n - 1), gn);
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       *(u32x4*)(Qw + gl * kBs + 32 * h + 8 * s) = qf[s];
       *(u32x4*)(Gw + gl * kBs + 32 * h + 8 * s) = gf[s];
     }
-    if (h == 0) st[wave][gl] = qi < n ? stats[bh * (int64_t)n + qi] : make_float4(0.f, 1.f, 0.f, 0.f);
+    if (h == 0) st[wave][gl] = qi < n ? stats[bh * (int64_t)n + qi] : make_float4(0.f, 0.f, 0.f, 0.f);
     // scores and dw with queries as rows, groups as columns
     f32x16 x = zero16(), dw = zero16();
     const uint16_t* rr = Rs + g * kBs + 32 * h;
@@ -293,7 +310,7 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
       const int r = 8 * (v >> 2) + 4 * h + (v & 3);
       const float4 sq = st[wave][r];
       const float e = __builtin_amdgcn_exp2f(fmaf(x[v], sl2e, lcg) - sq.x);
-      w[v] = t * 32 + r < n ? e / sq.y : 0.f;
+      w[v] = t * 32 + r < n ? e * sq.y : 0.f;
       dp[v] = w[v] * (dw[v] - sq.z);
     }
     // dr[g][f] += sum_q dp[g][q] Q[q][f]; dmu[g][f] += sum_q w[g][q] G[q][f]
@@ -329,19 +346,22 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   // accumulator register v of lane (col = feature gl, h): group row 8 (v / 4) + 4 h + v % 4
+  __syncthreads();  // every wave is done with the group rows and tiles
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int gr = 8 * (v >> 2) + 4 * h + (v & 3);
-    red[wave][0][gr * 64 + gl] = dr0[v];
-    red[wave][0][gr * 64 + 32 + gl] = dr1[v];
-    red[wave][1][gr * 64 + gl] = dm0[v];
-    red[wave][1][gr * 64 + 32 + gl] = dm1[v];
+    float* rw = red + wave * 2 * 32 * 64;
+    rw[gr * 64 + gl] = dr0[v];
+    rw[gr * 64 + 32 + gl] = dr1[v];
+    rw[32 * 64 + gr * 64 + gl] = dm0[v];
+    rw[32 * 64 + gr * 64 + 32 + gl] = dm1[v];
   }
   __syncthreads();
   float* out = part + ((bh * gridDim.y + chunk) * 2) * (int64_t)Npad * 64;
   for (int x = tid; x < 2 * 32 * 64; x += 256) {
     const int k = x / (32 * 64), e = x % (32 * 64);
-    const float s = ((red[0][k][e] + red[1][k][e]) + red[2][k][e]) + red[3][k][e];
+    const float* rk = red + k * 32 * 64 + e;
+    const float s = ((rk[0] + rk[2 * 32 * 64]) + rk[4 * 32 * 64]) + rk[6 * 32 * 64];
     out[(int64_t)k * Npad * 64 + 32 * b * 64 + e] = s;
   }
 }
