@@ -25,9 +25,9 @@
 //                 in the transposed layout (lane = group), so that the dp and
 //                 w registers are directly the A operand of the MFMA
 //                 reductions dr += dp Q and dmu += w G; the four waves'
-//                 partials are added in a fixed order
+//                 partials are added in a fixed order ((w0 + w2) + (w1 + w3))
 //   k_bwd_finish  per group: the chunk partials added in a fixed order,
-//                 scaled: scale dr / c and dmu / c
+//                 scaled: scale dr / c and dmu / c, as bf16 rows
 //   k_bwd_keys    per key: the rows of its group to dK, dV (bf16)
 // Every reduction has a fixed order, so repeated calls give identical bits.
 #include <hip/hip_runtime.h>
@@ -73,21 +73,30 @@ __device__ __forceinline__ f32x16 zero16() {
 // Padded slice layout of the workspace (all per slice bh):
 //   R   [Npad][64] bf16,  RT [64][rts] bf16 (rts = Npad + 4),
 //   MU  [Npad][64] bf16,  LC [Npad] f32.
+// grid (Npad / 32, BH), 256 threads: one 32-group block; its R^T columns go
+// through an LDS tile so that each transposed row segment is stored whole.
 __global__ __launch_bounds__(256) void k_bwd_prep(const float* __restrict__ centroid, const int32_t* __restrict__ count,
                                                   const float* __restrict__ vsum, int N, int Npad, int rts,
                                                   uint16_t* __restrict__ R, uint16_t* __restrict__ RT,
                                                   uint16_t* __restrict__ MU, float* __restrict__ LC) {
-  const int64_t bh = blockIdx.x;
-  for (int x = threadIdx.x; x < Npad * 64; x += 256) {
-    const int g = x >> 6, c = x & 63;
+  __shared__ uint16_t tt[64][32 + 2];
+  const int64_t bh = blockIdx.y;
+  const int g0 = 32 * blockIdx.x;
+  for (int x = threadIdx.x; x < 32 * 64; x += 256) {
+    const int g = g0 + (x >> 6), c = x & 63;
     const int cnt = g < N ? count[bh * N + g] : 0;
     const float cv = g < N ? centroid[(bh * N + g) * 64 + c] : 0.f;
     const float mv = cnt > 0 ? vsum[(bh * N + g) * 64 + c] / (float)cnt : 0.f;
     const uint16_t rb = (uint16_t)bf16_bits(cv);
     R[(bh * Npad + g) * 64 + c] = rb;
-    RT[(bh * 64 + c) * rts + g] = rb;
+    tt[c][x >> 6] = rb;
     MU[(bh * Npad + g) * 64 + c] = (uint16_t)bf16_bits(mv);
     if (c == 0) LC[bh * Npad + g] = cnt > 0 ? log2f((float)cnt) : -INFINITY;
+  }
+  __syncthreads();
+  for (int x = threadIdx.x; x < 64 * 16; x += 256) {
+    const int c = x >> 4, p = x & 15;  // 16 pairs of groups per feature row
+    *(uint32_t*)(RT + (bh * 64 + c) * rts + g0 + 2 * p) = (uint32_t)tt[c][2 * p] | ((uint32_t)tt[c][2 * p + 1] << 16);
   }
 }
 
@@ -242,31 +251,34 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
                                                    const float* __restrict__ LC, const float4* __restrict__ stats,
                                                    int n, float sl2e, float* __restrict__ part) {
   constexpr int Npad = NB * 32;
-  // group rows and the waves' query tiles; after the loop the same bytes hold
-  // the per-wave partials [4][2][32][64] (added in wave order)
-  constexpr int kRows = 2 * Npad * kBs * 2, kTiles = 8 * 32 * kBs * 2, kRed = 4 * 2 * 32 * 64 * 4;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[kRows + kTiles > kRed ? kRows + kTiles : kRed];
-  uint16_t* Rs = (uint16_t*)lds;
-  uint16_t* Ms = Rs + Npad * kBs;
-  uint16_t* Qt = Ms + Npad * kBs;  // [4][32][kBs]
+  // the waves' query tiles; after the loop the same bytes hold two partial
+  // slots [2][2][32][64] (waves 0, 1 write, waves 2, 3 add: fixed order)
+  constexpr int kTiles = 8 * 32 * kBs * 2, kRed = 2 * 2 * 32 * 64 * 4;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kTiles > kRed ? kTiles : kRed];
+  uint16_t* Qt = (uint16_t*)lds;  // [4][32][kBs]
   uint16_t* Gt = Qt + 4 * 32 * kBs;
   float* red = (float*)lds;
-  __shared__ float lc[Npad];
   __shared__ float4 st[4][32];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, gl = lane & 31;
   const int b = blockIdx.x, chunk = blockIdx.y;
   const int64_t bh = blockIdx.z;
-  stage_groups<NB>(R, MU, LC, bh, Rs, Ms, lc);
-  __syncthreads();
   const int64_t ntiles = ((int64_t)n + 31) / 32;
   const int64_t c0 = chunk * ntiles / gridDim.y, c1 = (chunk + 1) * ntiles / gridDim.y;
   const uint16_t* Qb = Q + bh * (int64_t)n * 64;
   const uint16_t* Gb = G + bh * (int64_t)n * 64;
   const int g = 32 * b + gl;  // this lane's group (MFMA column / A-operand row)
-  const float lcg = lc[g];
+  const float lcg = LC[bh * Npad + g];
+  // the lane's group row (features 32 h ..) of R and of the value means: the
+  // B operands of every tile's score and dw MFMAs
+  u32x4 rf[4], mf[4];
+  load_row_frags(R + bh * (int64_t)Npad * 64, g, rf);
+  load_row_frags(MU + bh * (int64_t)Npad * 64, g, mf);
   uint16_t *Qw = Qt + wave * 32 * kBs, *Gw = Gt + wave * 32 * kBs;
   f32x16 dr0 = zero16(), dr1 = zero16(), dm0 = zero16(), dm1 = zero16();
-  // the wave's next tile loads while the current one is processed
+  // the wave's next tile (its query stats, then its rows) loads while the
+  // current one is processed
+  const float4* statb = stats + bh * (int64_t)n;
+  float4 sn = statb[min((c0 + wave) * 32 + gl, (int64_t)n - 1)];
   u32x4 qn[4], gn[4];
   load_row_frags(Qb, min((c0 + wave) * 32 + gl, (int64_t)n - 1), qn);
   load_row_frags(Gb, min((c0 + wave) * 32 + gl, (int64_t)n - 1), gn);
@@ -280,25 +292,25 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
       qf[s] = qn[s];
       gf[s] = gn[s];
     }
-    if (t + 4 < c1) {
-      load_row_frags(Qb, min(qi + 128, (int64_t)n - 1), qn);
-      load_row_frags(Gb, min(qi + 128, (int64_t)n - 1), gn);
-    }
+    const float4 sc = sn;
+    // unconditional (rows clamped; past the chunk it loads a row again), so
+    // the loads stay in this block, ahead of the tile's work
+    sn = statb[min(qi + 128, (int64_t)n - 1)];
+    load_row_frags(Qb, min(qi + 128, (int64_t)n - 1), qn);
+    load_row_frags(Gb, min(qi + 128, (int64_t)n - 1), gn);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       *(u32x4*)(Qw + gl * kBs + 32 * h + 8 * s) = qf[s];
       *(u32x4*)(Gw + gl * kBs + 32 * h + 8 * s) = gf[s];
     }
-    if (h == 0) st[wave][gl] = qi < n ? stats[bh * (int64_t)n + qi] : make_float4(0.f, 0.f, 0.f, 0.f);
+    if (h == 0) st[wave][gl] = qi < n ? sc : make_float4(0.f, 0.f, 0.f, 0.f);
     // scores and dw with queries as rows, groups as columns
     f32x16 x = zero16(), dw = zero16();
-    const uint16_t* rr = Rs + g * kBs + 32 * h;
-    const uint16_t* mr = Ms + g * kBs + 32 * h;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      x = mfma(qf[s], *(const u32x4*)(rr + 8 * s), x);
-      dw = mfma(gf[s], *(const u32x4*)(mr + 8 * s), dw);
+      x = mfma(qf[s], rf[s], x);
+      dw = mfma(gf[s], mf[s], dw);
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -346,31 +358,44 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   // accumulator register v of lane (col = feature gl, h): group row 8 (v / 4) + 4 h + v % 4
-  __syncthreads();  // every wave is done with the group rows and tiles
+  __syncthreads();  // every wave is done with the tiles
+  float* rw = red + (wave & 1) * 2 * 32 * 64;
+  for (int pass = 0; pass < 2; ++pass) {
+    if ((wave >> 1) == pass) {
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int gr = 8 * (v >> 2) + 4 * h + (v & 3);
-    float* rw = red + wave * 2 * 32 * 64;
-    rw[gr * 64 + gl] = dr0[v];
-    rw[gr * 64 + 32 + gl] = dr1[v];
-    rw[32 * 64 + gr * 64 + gl] = dm0[v];
-    rw[32 * 64 + gr * 64 + 32 + gl] = dm1[v];
+      for (int v = 0; v < 16; ++v) {
+        const int gr = 8 * (v >> 2) + 4 * h + (v & 3);
+        float* r0 = rw + gr * 64 + gl;
+        float* r1 = rw + 32 * 64 + gr * 64 + gl;
+        if (pass == 0) {
+          r0[0] = dr0[v];
+          r0[32] = dr1[v];
+          r1[0] = dm0[v];
+          r1[32] = dm1[v];
+        } else {
+          r0[0] += dr0[v];
+          r0[32] += dr1[v];
+          r1[0] += dm0[v];
+          r1[32] += dm1[v];
+        }
+      }
+    }
+    __syncthreads();
   }
-  __syncthreads();
   float* out = part + ((bh * gridDim.y + chunk) * 2) * (int64_t)Npad * 64;
   for (int x = tid; x < 2 * 32 * 64; x += 256) {
     const int k = x / (32 * 64), e = x % (32 * 64);
-    const float* rk = red + k * 32 * 64 + e;
-    const float s = ((rk[0] + rk[2 * 32 * 64]) + rk[4 * 32 * 64]) + rk[6 * 32 * 64];
+    const float s = red[k * 32 * 64 + e] + red[2 * 32 * 64 + k * 32 * 64 + e];  // (w0 + w2) + (w1 + w3)
     out[(int64_t)k * Npad * 64 + 32 * b * 64 + e] = s;
   }
 }
 
 // grid (Npad / 4, BH), 256 threads: thread = (group, feature) of 4 groups.
-// gk = scale sum_chunks dr / c, gv = sum_chunks dmu / c (0 for an empty group).
+// gk = scale sum_chunks dr / c, gv = sum_chunks dmu / c (0 for an empty
+// group), rounded to bf16 once: the rows every member key receives.
 __global__ __launch_bounds__(256) void k_bwd_finish(const float* __restrict__ part, const int32_t* __restrict__ count,
-                                                    int N, int Npad, int chunks, float scale, float* __restrict__ gk,
-                                                    float* __restrict__ gv) {
+                                                    int N, int Npad, int chunks, float scale, uint16_t* __restrict__ gk,
+                                                    uint16_t* __restrict__ gv) {
   const int64_t bh = blockIdx.y;
   const int g = blockIdx.x * 4 + (threadIdx.x >> 6), f = threadIdx.x & 63;
   if (g >= N) return;
@@ -381,13 +406,13 @@ __global__ __launch_bounds__(256) void k_bwd_finish(const float* __restrict__ pa
     sm += p[(int64_t)Npad * 64 + g * 64 + f];
   }
   const int cnt = count[bh * N + g];
-  gk[(bh * Npad + g) * 64 + f] = cnt > 0 ? scale * sr / (float)cnt : 0.f;
-  gv[(bh * Npad + g) * 64 + f] = cnt > 0 ? sm / (float)cnt : 0.f;
+  gk[(bh * Npad + g) * 64 + f] = (uint16_t)bf16_bits(cnt > 0 ? scale * sr / (float)cnt : 0.f);
+  gv[(bh * Npad + g) * 64 + f] = (uint16_t)bf16_bits(cnt > 0 ? sm / (float)cnt : 0.f);
 }
 
-// grid (ceil(n / 32), BH), 256 threads: 8 lanes per key row.
-__global__ __launch_bounds__(256) void k_bwd_keys(const int32_t* __restrict__ belong, const float* __restrict__ gk,
-                                                  const float* __restrict__ gv, int n, int N, int Npad,
+// grid (ceil(n / 32), BH), 256 threads: 8 lanes per key row (16 bytes each).
+__global__ __launch_bounds__(256) void k_bwd_keys(const int32_t* __restrict__ belong, const uint16_t* __restrict__ gk,
+                                                  const uint16_t* __restrict__ gv, int n, int N, int Npad,
                                                   uint16_t* __restrict__ dK, uint16_t* __restrict__ dV) {
   const int64_t bh = blockIdx.y;
   const int k = blockIdx.x * 32 + (threadIdx.x >> 3), ch = threadIdx.x & 7;
@@ -395,13 +420,8 @@ __global__ __launch_bounds__(256) void k_bwd_keys(const int32_t* __restrict__ be
   const int g = belong[bh * n + k];
   u32x4 ok = {0u, 0u, 0u, 0u}, ov = {0u, 0u, 0u, 0u};
   if ((unsigned)g < (unsigned)N) {
-    const float* rk = gk + (bh * Npad + g) * 64 + 8 * ch;
-    const float* rv = gv + (bh * Npad + g) * 64 + 8 * ch;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      ok[e] = pack2(rk[2 * e], rk[2 * e + 1]);
-      ov[e] = pack2(rv[2 * e], rv[2 * e + 1]);
-    }
+    ok = *(const u32x4*)(gk + (bh * Npad + g) * 64 + 8 * ch);
+    ov = *(const u32x4*)(gv + (bh * Npad + g) * 64 + 8 * ch);
   }
   *(u32x4*)(dK + (bh * n + k) * 64 + 8 * ch) = ok;
   *(u32x4*)(dV + (bh * n + k) * 64 + 8 * ch) = ov;
@@ -442,8 +462,8 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
   const float sl2e = scale * 1.4426950408889634f;
   {
     TimedLaunch tl("bwd_prep", st);
-    hipLaunchKernelGGL(k_bwd_prep, dim3((unsigned)d.BH), dim3(256), 0, st, centroid, count, vsum, d.N, Npad, rts, w.R,
-                       w.RT, w.MU, w.LC);
+    hipLaunchKernelGGL(k_bwd_prep, dim3((unsigned)NB, (unsigned)d.BH), dim3(256), 0, st, centroid, count, vsum, d.N,
+                       Npad, rts, w.R, w.RT, w.MU, w.LC);
   }
   const int64_t ntiles = ((int64_t)d.n + 31) / 32;
   const int tpw = (int)((ntiles + 31) / 32);  // about 8 workgroups per slice
@@ -479,11 +499,11 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
   {
     TimedLaunch tl("bwd_finish", st);
     hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 4), (unsigned)d.BH), dim3(256), 0, st, w.part, count, d.N,
-                       Npad, kBwdChunks, scale, w.gk, w.gv);
+                       Npad, kBwdChunks, scale, (uint16_t*)w.gk, (uint16_t*)w.gv);
   }
   TimedLaunch tl("bwd_keys", st);
-  hipLaunchKernelGGL(k_bwd_keys, dim3((unsigned)((d.n + 31) / 32), (unsigned)d.BH), dim3(256), 0, st, belong, w.gk,
-                     w.gv, d.n, d.N, Npad, (uint16_t*)dK, (uint16_t*)dV);
+  hipLaunchKernelGGL(k_bwd_keys, dim3((unsigned)((d.n + 31) / 32), (unsigned)d.BH), dim3(256), 0, st, belong,
+                     (const uint16_t*)w.gk, (const uint16_t*)w.gv, d.n, d.N, Npad, (uint16_t*)dK, (uint16_t*)dV);
   return hipGetLastError();
 }
 
