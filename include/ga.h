@@ -202,7 +202,7 @@ int ga_merge_plan(ga_shape_t s, const void *Q, const void *K, const int32_t *bel
 int32_t ga_next_group_count(int32_t N, const int32_t *merges, int64_t slices, double alpha);
 
 /*
- * Backward pass of group attention (bf16; N <= 128), the gradient with the
+ * Backward pass of group attention (bf16; N <= 256), the gradient with the
  * grouping held fixed (BELONG / COUNT are piecewise constant in the keys; the
  * paper states no gradient rule).  With w_ij = c_j e^{p_ij} / sum_l c_l e^{p_il}
  * (the normalised group weights of Eq. 3), mu_j = vsum_j / c_j and G = dO:

@@ -15,12 +15,13 @@
 //   dr_j = scale sum_i dp_ij q_i  ->  dK_k = dr_{a_k} / c_{a_k},
 //   dmu_j = sum_i w_ij G_i        ->  dV_k = dmu_{a_k} / c_{a_k}.
 //
-// Kernels (N <= 128, padded to Npad = 32 NB groups):
+// Kernels (N <= 256, padded to Npad = 32 NB groups):
 //   k_bwd_prep    per slice: R = bf16(centroid) rows and transposed, bf16
 //                 value means, log2(count) (-inf for an empty group)
 //   k_bwd_query   per 32-query tile (lane = query): MFMA scores, the group
 //                 softmax, MFMA dw, D, dp, MFMA dQ; stores the softmax shift,
-//                 1 / sum and D of every query
+//                 1 / sum and D of every query (N > 128: three passes over the
+//                 32-group blocks instead of all scores in registers)
 //   k_bwd_group   per (32-group block, query chunk): the same scores and dw
 //                 in the transposed layout (lane = group), so that the dp and
 //                 w registers are directly the A operand of the MFMA
@@ -154,11 +155,10 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
     u32x4 qf[4], gf[4];
     load_row_frags(Qb, min(qi, (int64_t)n - 1), qf);
     load_row_frags(Gb, min(qi, (int64_t)n - 1), gf);
-    // scores x_gq = sl2e (r_g . q) + log2 c_g and dw_gq = mu_g . G_q (rows g, column q)
-    f32x16 x[NB], dw[NB];
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      f32x16 a = zero16(), d = zero16();
+    // block b's scores r_g . q and dw_gq = mu_g . G_q (rows g, column q)
+    auto block_mfma = [&](int b, f32x16& a, f32x16& d) __attribute__((always_inline)) {
+      a = zero16();
+      d = zero16();
       const uint16_t* rr = Rs + (32 * b + q) * kBs + 32 * h;
       const uint16_t* mr = Ms + (32 * b + q) * kBs + 32 * h;
 #pragma unroll
@@ -166,45 +166,10 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
         a = mfma(*(const u32x4*)(rr + 8 * s), qf[s], a);
         d = mfma(*(const u32x4*)(mr + 8 * s), gf[s], d);
       }
-#pragma unroll
-      for (int v = 0; v < 16; ++v) a[v] = fmaf(a[v], sl2e, lc[32 * b + 8 * (v >> 2) + 4 * h + (v & 3)]);
-      x[b] = a;
-      dw[b] = d;
-    }
-    float M = -INFINITY;
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) M = fmaxf(M, x[b][v]);
-    M = fmaxf(M, __shfl_xor(M, 32));
-    const bool any = M != -INFINITY;  // some group is non-empty
-    const float Ms_ = any ? M : 0.f;
-    float S = 0.f;
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        x[b][v] = __builtin_amdgcn_exp2f(x[b][v] - Ms_);  // e (0 for an empty group)
-        S += x[b][v];
-      }
-    S += __shfl_xor(S, 32);
-    const float inv = any ? 1.0f / S : 0.f;
-    float Dq = 0.f;
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        x[b][v] *= inv;  // w
-        Dq = fmaf(x[b][v], dw[b][v], Dq);
-      }
-    Dq += __shfl_xor(Dq, 32);
-    // dQ^T[f][q] = sum_g r_gf dp_gq: A = R^T rows (features), B = dp from the registers
+    };
+    // dQ^T[f][q] += sum_g r_gf dp_gq over block b: A = R^T rows (features), B = dp from the registers
     f32x16 o0 = zero16(), o1 = zero16();
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      float dp[16];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) dp[v] = x[b][v] * (dw[b][v] - Dq);
+    auto dq_block = [&](int b, const float (&dp)[16]) __attribute__((always_inline)) {
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const u32x4 bf = {pack2(dp[8 * u], dp[8 * u + 1]), pack2(dp[8 * u + 2], dp[8 * u + 3]),
@@ -216,6 +181,92 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
         const u32x2 a1l = *(const u32x2*)r1, a1h = *(const u32x2*)(r1 + 8);
         o0 = mfma(u32x4{a0l[0], a0l[1], a0h[0], a0h[1]}, bf, o0);
         o1 = mfma(u32x4{a1l[0], a1l[1], a1h[0], a1h[1]}, bf, o1);
+      }
+    };
+    float Ms_, inv, Dq;
+    if constexpr (NB <= 4) {
+      // all blocks' scores and dw held at once
+      f32x16 x[NB], dw[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        block_mfma(b, x[b], dw[b]);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) x[b][v] = fmaf(x[b][v], sl2e, lc[32 * b + 8 * (v >> 2) + 4 * h + (v & 3)]);
+      }
+      float M = -INFINITY;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) M = fmaxf(M, x[b][v]);
+      M = fmaxf(M, __shfl_xor(M, 32));
+      const bool any = M != -INFINITY;  // some group is non-empty
+      Ms_ = any ? M : 0.f;
+      float S = 0.f;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          x[b][v] = __builtin_amdgcn_exp2f(x[b][v] - Ms_);  // e (0 for an empty group)
+          S += x[b][v];
+        }
+      S += __shfl_xor(S, 32);
+      inv = any ? 1.0f / S : 0.f;
+      Dq = 0.f;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          x[b][v] *= inv;  // w
+          Dq = fmaf(x[b][v], dw[b][v], Dq);
+        }
+      Dq += __shfl_xor(Dq, 32);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        float dp[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dp[v] = x[b][v] * (dw[b][v] - Dq);
+        dq_block(b, dp);
+      }
+    } else {
+      // more groups than fit in registers: three passes over the blocks
+      // (shift; sum and D; dp and dQ), the MFMAs recomputed in each
+      float M = -INFINITY;
+      for (int b = 0; b < NB; ++b) {
+        f32x16 a, d;
+        block_mfma(b, a, d);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) M = fmaxf(M, fmaf(a[v], sl2e, lc[32 * b + 8 * (v >> 2) + 4 * h + (v & 3)]));
+      }
+      M = fmaxf(M, __shfl_xor(M, 32));
+      const bool any = M != -INFINITY;
+      Ms_ = any ? M : 0.f;
+      float S = 0.f, SD = 0.f;
+      for (int b = 0; b < NB; ++b) {
+        f32x16 a, d;
+        block_mfma(b, a, d);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float e =
+              __builtin_amdgcn_exp2f(fmaf(a[v], sl2e, lc[32 * b + 8 * (v >> 2) + 4 * h + (v & 3)]) - Ms_);
+          S += e;
+          SD = fmaf(e, d[v], SD);
+        }
+      }
+      S += __shfl_xor(S, 32);
+      SD += __shfl_xor(SD, 32);
+      inv = any ? 1.0f / S : 0.f;
+      Dq = SD * inv;
+      for (int b = 0; b < NB; ++b) {
+        f32x16 a, d;
+        block_mfma(b, a, d);
+        float dp[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float w =
+              __builtin_amdgcn_exp2f(fmaf(a[v], sl2e, lc[32 * b + 8 * (v >> 2) + 4 * h + (v & 3)]) - Ms_) * inv;
+          dp[v] = w * (d[v] - Dq);
+        }
+        dq_block(b, dp);
       }
     }
     // dQ rows through the wave's LDS tile: lane (q, h) holds features 8 k + 4 h + j
@@ -432,7 +483,7 @@ int bwd_rts(int N) { return bwd_npad(N) + 4; }
 
 }  // namespace
 
-int backward_max_groups() { return 128; }
+int backward_max_groups() { return 256; }
 
 size_t backward_workspace_layout(const Dims& d, BackwardWorkspace* w, void* base) {
   const int Npad = bwd_npad(d.N), rts = bwd_rts(d.N);
@@ -478,7 +529,11 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
       case 1: GA_BWD_Q(1); break;
       case 2: GA_BWD_Q(2); break;
       case 3: GA_BWD_Q(3); break;
-      default: GA_BWD_Q(4); break;
+      case 4: GA_BWD_Q(4); break;
+      case 5: GA_BWD_Q(5); break;
+      case 6: GA_BWD_Q(6); break;
+      case 7: GA_BWD_Q(7); break;
+      default: GA_BWD_Q(8); break;
     }
 #undef GA_BWD_Q
   }
@@ -492,7 +547,11 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
       case 1: GA_BWD_G(1); break;
       case 2: GA_BWD_G(2); break;
       case 3: GA_BWD_G(3); break;
-      default: GA_BWD_G(4); break;
+      case 4: GA_BWD_G(4); break;
+      case 5: GA_BWD_G(5); break;
+      case 6: GA_BWD_G(6); break;
+      case 7: GA_BWD_G(7); break;
+      default: GA_BWD_G(8); break;
     }
 #undef GA_BWD_G
   }

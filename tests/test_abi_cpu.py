@@ -179,12 +179,12 @@ def test_backward_validates():
     nb = L.ga_backward_workspace_bytes(s, 64)
     assert nb > 0
     assert L.ga_backward_workspace_bytes(shape(dtype=ga.GA_F32), 8) == 0
-    assert L.ga_backward_workspace_bytes(s, 200) == 0
+    assert L.ga_backward_workspace_bytes(s, 257) == 0
     bw = lambda s=s, N=64, scale=0.125, dQ=FAKE, ws=FAKE, nbytes=nb: L.ga_backward(
         s, P(), P(), P(), P(), P(), P(), N, scale, P(dQ) if dQ else None, P(), P(), P(ws) if ws else None, nbytes,
         None)
     assert bw(s=shape(dtype=ga.GA_F32)) == 2
-    assert bw(N=129) == 2
+    assert bw(N=257) == 2
     assert bw(N=0) == 1
     assert bw(scale=float("inf")) == 1
     assert bw(dQ=0) == 1

@@ -65,6 +65,8 @@ CASES = [
     (1, 2, 700, 100, 3, 100, (0.05, 0.3)),
     (1, 1, 500, 128, 3, 128, (0.05, 0.3)),
     (1, 1, 64, 1, 1, 4, (0.1, 0.1)),      # one group
+    (1, 2, 900, 200, 3, 200, (0.05, 0.3)),  # more groups than the one-pass query kernel holds
+    (1, 1, 1500, 256, 3, 256, (0.05, 0.3)),  # largest N
 ]
 
 
