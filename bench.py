@@ -4,7 +4,9 @@
 One step = one whole group-attention forward (grouping rounds, aggregation,
 group softmax + combine) over one batch of synthetic input already resident in
 HBM.  Two input sets alternate so consecutive steps do not hit in the 256 MB
-last-level cache.  Prints one JSON line (see the contract in the design doc).
+last-level cache.  Prints one JSON line: throughput, the roofline of the dominant
+kernel, the CPU oracle timed on a sample, per-kernel times, and the merge plan
+and backward pass of the same grouping timed on their own.
 """
 import argparse
 import hashlib
@@ -86,8 +88,9 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU: this build runs group attention on a single MI355X "
-              f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}); see DESIGN.md for how it would shard.",
+        print(f"bench.py measures one GPU: group attention runs here on a single MI355X "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}); every (batch, head) slice is independent, "
+              f"so batches and heads shard across GPUs without communication.",
               file=sys.stderr)
         sys.exit(2)
 

@@ -16,7 +16,7 @@
  *     error bound eps into a distance threshold, the simplified rule of Eq. 5
  *     marks mergeable groups).
  *
- * Readings where the paper is silent (each also listed in the design doc):
+ * Readings where the paper is silent:
  *   init     C0_j = k_{floor(j*n/N)} (strided), or a caller-given fp32 init.
  *   iters    T = number of (assign, update) rounds, no convergence test.
  *   R        R = round_dt(C): identity for fp32 inputs, round-to-nearest-even
