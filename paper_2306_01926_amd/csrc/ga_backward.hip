@@ -150,11 +150,23 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
   const uint16_t* Qb = Q + bh * (int64_t)n * 64;
   const uint16_t* Gb = G + bh * (int64_t)n * 64;
   uint16_t* Ow = Ot[wave];
-  for (int64_t t = t0; t < min(t0 + tpw, ntiles); ++t) {
+  const int64_t tend = min(t0 + tpw, ntiles);
+  // the next tile's rows load while the current tile is processed
+  // (unconditional, rows clamped, so the loads stay ahead of the tile's work)
+  u32x4 qn[4], gn[4];
+  load_row_frags(Qb, min(t0 * 32 + q, (int64_t)n - 1), qn);
+  load_row_frags(Gb, min(t0 * 32 + q, (int64_t)n - 1), gn);
+  for (int64_t t = t0; t < tend; ++t) {
     const int64_t qi = t * 32 + q;
     u32x4 qf[4], gf[4];
-    load_row_frags(Qb, min(qi, (int64_t)n - 1), qf);
-    load_row_frags(Gb, min(qi, (int64_t)n - 1), gf);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      qf[s] = qn[s];
+      gf[s] = gn[s];
+    }
+    load_row_frags(Qb, min(qi + 32, (int64_t)n - 1), qn);
+    load_row_frags(Gb, min(qi + 32, (int64_t)n - 1), gn);
+    __builtin_amdgcn_sched_barrier(0);
     // block b's scores r_g . q and dw_gq = mu_g . G_q (rows g, column q)
     auto block_mfma = [&](int b, f32x16& a, f32x16& d) __attribute__((always_inline)) {
       a = zero16();
@@ -185,14 +197,25 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
     };
     float Ms_, inv, Dq;
     if constexpr (NB <= 4) {
-      // all blocks' scores and dw held at once
-      f32x16 x[NB], dw[NB];
+      // all blocks' weights held in registers; each block's dw is formed
+      // twice (for D, then for dp) rather than held
+      f32x16 x[NB];
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        block_mfma(b, x[b], dw[b]);
+        x[b] = zero16();
+        const uint16_t* rr = Rs + (32 * b + q) * kBs + 32 * h;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) x[b] = mfma(*(const u32x4*)(rr + 8 * s), qf[s], x[b]);
 #pragma unroll
         for (int v = 0; v < 16; ++v) x[b][v] = fmaf(x[b][v], sl2e, lc[32 * b + 8 * (v >> 2) + 4 * h + (v & 3)]);
       }
+      auto dw_block = [&](int b) __attribute__((always_inline)) {
+        f32x16 d = zero16();
+        const uint16_t* mr = Ms + (32 * b + q) * kBs + 32 * h;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) d = mfma(*(const u32x4*)(mr + 8 * s), gf[s], d);
+        return d;
+      };
       float M = -INFINITY;
 #pragma unroll
       for (int b = 0; b < NB; ++b)
@@ -213,18 +236,21 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
       inv = any ? 1.0f / S : 0.f;
       Dq = 0.f;
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
+      for (int b = 0; b < NB; ++b) {
+        const f32x16 d = dw_block(b);
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           x[b][v] *= inv;  // w
-          Dq = fmaf(x[b][v], dw[b][v], Dq);
+          Dq = fmaf(x[b][v], d[v], Dq);
         }
+      }
       Dq += __shfl_xor(Dq, 32);
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
+        const f32x16 d = dw_block(b);
         float dp[16];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) dp[v] = x[b][v] * (dw[b][v] - Dq);
+        for (int v = 0; v < 16; ++v) dp[v] = x[b][v] * (d[v] - Dq);
         dq_block(b, dp);
       }
     } else {
