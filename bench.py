@@ -261,6 +261,8 @@ def main():
         "config": {"workload": w.name, "B": w.B, "H": w.H, "n": w.n, "d": w.d, "N": N, "iters": w.iters,
                    "input_sets": 2},
         "pct_hbm_roofline": pct_hbm, "compulsory_bytes": compulsory,
+        # every contraction of the forward (T assign rounds, scores, combine): 2 N d (T + 2) flop per query
+        "mfma_frac_of_step": 2.0 * N * w.d * (w.iters + 2) * queries / (ms / 1e3) / (MFMA_BF16_PEAK_TFS * 1e12),
         "roofline": roofline, "cpu_baseline": cpu,
         "kernels": kernels, "ms_per_step_with_kernel_events": ms_timed, "parity_sample": parity,
         "scheduler": sched, "backward": bwd,
