@@ -43,31 +43,27 @@ constexpr int kCs = 65;  // LDS row stride (floats) of the centroids
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Raw rows (loaded as 16-byte vectors) and their exact fp64 elements.
 struct F32In {
   typedef float T;
-  // 64 features of row p as doubles (exact)
-  __device__ static void row(const float* p, double (&x)[64]) {
+  static constexpr int kVec = 16;  // 16-byte vectors per 64-feature row
+  __device__ static void load(const float* p, u32x4 (&v)[16]) {
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const u32x4 v = *(const u32x4*)(p + 4 * u);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) x[4 * u + e] = (double)__uint_as_float(v[e]);
-    }
+    for (int u = 0; u < 16; ++u) v[u] = *(const u32x4*)(p + 4 * u);
   }
+  __device__ static double at(const u32x4 (&v)[16], int c) { return (double)__uint_as_float(v[c >> 2][c & 3]); }
 };
 
 struct BF16In {
   typedef uint16_t T;
-  __device__ static void row(const uint16_t* p, double (&x)[64]) {
+  static constexpr int kVec = 8;
+  __device__ static void load(const uint16_t* p, u32x4 (&v)[8]) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const u32x4 v = *(const u32x4*)(p + 8 * u);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[8 * u + 2 * e] = (double)__uint_as_float(v[e] << 16);
-        x[8 * u + 2 * e + 1] = (double)__uint_as_float(v[e] & 0xffff0000u);
-      }
-    }
+    for (int u = 0; u < 8; ++u) v[u] = *(const u32x4*)(p + 8 * u);
+  }
+  __device__ static double at(const u32x4 (&v)[8], int c) {
+    const uint32_t w = v[c >> 3][(c >> 1) & 3];
+    return (double)__uint_as_float((c & 1) ? (w & 0xffff0000u) : (w << 16));
   }
 };
 
@@ -91,20 +87,25 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge_norms(
   for (int g = tid; g < N; g += kMergeThreads) rad2[g] = 0ull;  // bits of +0.0
   __syncthreads();
   double qmax2 = 0.0;
+  // per key: its query row, group and key row are requested together (the
+  // key row's address does not depend on the group), then the two chains run
   for (int i = i0 + tid; i < i1; i += kMergeThreads) {
-    double x[64];
-    S::row(Q + (bh * n + i) * 64, x);
+    u32x4 qv[S::kVec], kv[S::kVec];
+    S::load(Q + (bh * n + i) * 64, qv);
+    const int g = belong[bh * n + i];
+    S::load(K + (bh * n + i) * 64, kv);
     double acc = 0.0;
 #pragma unroll
-    for (int c = 0; c < 64; ++c) acc = __builtin_fma(x[c], x[c], acc);
+    for (int c = 0; c < 64; ++c) {
+      const double xq = S::at(qv, c);
+      acc = __builtin_fma(xq, xq, acc);
+    }
     qmax2 = acc > qmax2 ? acc : qmax2;
-    const int g = belong[bh * n + i];
     if ((unsigned)g >= (unsigned)N) continue;
-    S::row(K + (bh * n + i) * 64, x);
     double r2 = 0.0;
 #pragma unroll
     for (int c = 0; c < 64; ++c) {
-      const double t = x[c] - (double)cs[g * kCs + c];
+      const double t = S::at(kv, c) - (double)cs[g * kCs + c];
       r2 = __builtin_fma(t, t, r2);
     }
     atomicMax(&rad2[g], (unsigned long long)__double_as_longlong(r2));
