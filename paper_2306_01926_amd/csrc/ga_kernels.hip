@@ -14,7 +14,7 @@
 //                   re-decided with the exact fp64 definition; then the
 //                   workgroup's fp64 partition of the group sums
 //   k_part_finish   adds the partitions: counts, C, R, |r|^2
-//   k_assign_reg<false, NB, false> + k_gsum<1>   each later round: the same
+//   k_assign_reg<false, NB, false> + k_gdelta   each later round: the same
 //                   assignment, then the member sums of the groups changed by
 //                   the moved keys only
 //   k_gsum<3>       value sums, written as the attention's bf16 value means
@@ -1428,18 +1428,15 @@ __global__ __launch_bounds__(256) void k_segsum(const typename S::T* __restrict_
 // k_gsum: grid (ceil(N / 32), BH), 256 threads.  Workgroup x owns groups
 // g0 = 32 x .. g0 + 31 of slice bh and finishes them itself:
 //   MODE 0 (first round): S = sum of the member key rows, count = members
-//   MODE 1 (later rounds): S += joins - leaves from the round's moved-key
-//           records, count += joins - leaves (groups without either are left
-//           alone)
 //   MODE 2 (value sums):  vsum = (float) sum of the member value rows
 //   MODE 3 (value sums for the attention): the bf16 value means, transposed,
 //           and the log2(count) score bias, as k_attend_prep forms them
-// MODE 0/1 then set C = (float)(S / count) (an empty group keeps C), R =
+// MODE 0 then sets C = (float)(S / count) (an empty group keeps C), R =
 // bf16(C), the canonical fp64 |r|^2 (fma chain over c = 0..63, one lane per
-// group) and its split.
+// group) and its split.  (The later rounds' update is k_gdelta.)
 //
-// Per chunk of keys (or records), all loaded at once:
-// 1. count the entries (key, sign) of every owned group, lay the groups out
+// Per chunk of keys, all loaded at once:
+// 1. count the entries (key) of every owned group, lay the groups out
 //    in LDS padded to multiples of 8 entries, scatter the entries (a local
 //    counting sort; one LDS atomic per entry);
 // 2. each wave takes a run of whole groups and sums 8 rows per instruction
@@ -1452,72 +1449,50 @@ constexpr int kGsumG = 32;
 constexpr int kGsumList = 8448;  // entry capacity of the sorted chunk list
 template <int MODE>
 __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, const int32_t* __restrict__ belong,
-                                              const unsigned long long* __restrict__ mrec,
-                                              const int32_t* __restrict__ mcount_cur,
-                                              int32_t* __restrict__ mcount_next, int n, int N,
-                                              double* __restrict__ S64, int32_t* __restrict__ count,
-                                              float* __restrict__ out, uint16_t* __restrict__ R,
+                                              int n, int N, double* __restrict__ S64,
+                                              int32_t* __restrict__ count, float* __restrict__ out, uint16_t* __restrict__ R,
                                               double* __restrict__ nrm64, uint16_t* __restrict__ nsplit,
                                               float inv_sl2e, int vts) {
-  __shared__ uint32_t ent[kGsumList];  // key | leave << 31; 0xffffffff pads a group to 8k entries
+  __shared__ uint32_t ent[kGsumList];  // key; 0xffffffff pads a group to 8k entries
   __shared__ double acc[kGsumG * 64];  // [g][c] sums of this workgroup's groups
   __shared__ double tws[4][8 * 64];    // per-wave [slot][feature] transpose tile of a finished group
-  __shared__ int ecnt[kGsumG], eoff[kGsumG + 1], ecur[kGsumG], dcnt[kGsumG], hit[kGsumG], wbeg[5], wg0[4];
+  __shared__ int ecnt[kGsumG], eoff[kGsumG + 1], ecur[kGsumG], dcnt[kGsumG], wbeg[5], wg0[4];
   float* rsh = (float*)ent;            // [32][65] bf16 representatives, after the sums
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bh = blockIdx.y;
   const int g0 = blockIdx.x * kGsumG, ng = min(kGsumG, N - g0);
   for (int i = tid; i < kGsumG * 64; i += 256) acc[i] = 0.0;
-  if (tid < kGsumG) {
-    dcnt[tid] = 0;
-    hit[tid] = 0;
-  }
+  if (tid < kGsumG) dcnt[tid] = 0;
 
-  // (a slice records at most n moved keys; the clamp keeps the loads below in
-  // bounds even if the workspace was corrupted, e.g. shared by overlapping calls)
-  const int64_t total = MODE == 1 ? min((int64_t)mcount_cur[bh], (int64_t)n) : (int64_t)n;
-  // entries per chunk: at most 2 per record (join, leave) plus 7 padding per group
-  constexpr int CH = MODE == 1 ? 4096 : 8192;
+  const int64_t total = n;
+  // entries per chunk: one per key plus 7 padding per group
+  constexpr int CH = 8192;
   constexpr int PER = CH / 256;
-  static_assert((MODE == 1 ? 2 : 1) * CH + 7 * kGsumG <= kGsumList, "chunk list overflow");
+  static_assert(CH + 7 * kGsumG <= kGsumList, "chunk list overflow");
   const uint16_t* Xb = X + bh * (int64_t)n * 64;
   for (int64_t c0 = 0; c0 < total; c0 += CH) {
-    int kv[PER], gj[PER], gl[PER];
+    int kv[PER], gj[PER];
     // every lane loads (index clamped into the chunk) so that the loads overlap
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int64_t e = c0 + tid + 256 * u, ec = min(e, total - 1);
-      if (MODE == 1) {
-        const unsigned long long r = mrec[bh * n + ec];
-        kv[u] = min((int)(r >> 32) & 0x7fffffff, n - 1);
-        gj[u] = (int)(r & 0xffffu) - g0;
-        gl[u] = (int)((r >> 16) & 0xffffu) - g0;
-      } else {
-        kv[u] = (int)e;
-        gj[u] = belong[bh * n + ec] - g0;
-        gl[u] = -1;
-      }
+      kv[u] = (int)e;
+      gj[u] = belong[bh * n + ec] - g0;
     }
 #pragma unroll
     for (int u = 0; u < PER; ++u)
-      if (c0 + tid + 256 * u >= total) {
-        gj[u] = -1;
-        gl[u] = -1;
-      }
+      if (c0 + tid + 256 * u >= total) gj[u] = -1;
     if (tid < kGsumG) ecnt[tid] = 0;
     __syncthreads();
     // 1. count, lay out, scatter
 #pragma unroll
-    for (int u = 0; u < PER; ++u)
-#pragma unroll
-      for (int side = 0; side < (MODE == 1 ? 2 : 1); ++side) {
-        const int g = side ? gl[u] : gj[u];
-        if ((unsigned)g < (unsigned)ng) {
-          atomicAdd(&ecnt[g], 1);
-          if (MODE < 2) atomicAdd(&dcnt[g], side ? -1 : 1);
-          hit[g] = 1;
-        }
+    for (int u = 0; u < PER; ++u) {
+      const int g = gj[u];
+      if ((unsigned)g < (unsigned)ng) {
+        atomicAdd(&ecnt[g], 1);
+        if (MODE == 0) atomicAdd(&dcnt[g], 1);
       }
+    }
     __syncthreads();
     if (wave == 0) {
       const int c = lane < kGsumG ? ecnt[lane] : 0;
@@ -1554,12 +1529,10 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
     }
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < PER; ++u)
-#pragma unroll
-      for (int side = 0; side < (MODE == 1 ? 2 : 1); ++side) {
-        const int g = side ? gl[u] : gj[u];
-        if ((unsigned)g < (unsigned)ng) ent[atomicAdd(&ecur[g], 1)] = (uint32_t)kv[u] | ((uint32_t)side << 31);
-      }
+    for (int u = 0; u < PER; ++u) {
+      const int g = gj[u];
+      if ((unsigned)g < (unsigned)ng) ent[atomicAdd(&ecur[g], 1)] = (uint32_t)kv[u];
+    }
     __syncthreads();
     // 2. per-wave register sums over runs of whole groups
     {
@@ -1597,7 +1570,7 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
             while (eoff[g + 1] <= ch * 8) ++g;
             gend = eoff[g + 1] / 8;
           }
-          const double sg = e[u] == 0xffffffffu ? 0.0 : ((e[u] >> 31) ? -1.0 : 1.0);
+          const double sg = e[u] == 0xffffffffu ? 0.0 : 1.0;
 #pragma unroll
           for (int k = 0; k < 8; ++k) {
             const uint32_t bits = (k & 1) ? (w[u][k >> 1] >> 16) : (w[u][k >> 1] & 0xffffu);
@@ -1626,16 +1599,14 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
 
   // 3. finish the owned groups: element (g, c) = (idx / 64, idx % 64), 8 per thread
   constexpr int EPT = kGsumG * 64 / 256;
-  double prev[EPT];
   int pc[EPT];
 #pragma unroll
   for (int u = 0; u < EPT; ++u) {
-    const int idx = tid + 256 * u, g = idx >> 6, c = idx & 63;
+    const int idx = tid + 256 * u, g = idx >> 6;
     const int64_t row = bh * N + g0 + min(g, ng - 1);
-    prev[u] = MODE == 1 ? S64[row * 64 + c] : 0.0;
-    pc[u] = MODE == 1 || MODE == 3 ? count[row] : 0;
+    pc[u] = MODE == 3 ? count[row] : 0;
   }
-  __syncthreads();  // (total == 0: dcnt, hit, acc initialised above)
+  __syncthreads();  // (total == 0: dcnt, acc initialised above)
   if (MODE == 3) {
     // value means mu = (float) sum / count (0 for an empty or padded group)
     // as bf16, transposed through LDS into Vt[feature][group] (R, 8-byte
@@ -1668,9 +1639,8 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
       out[row * 64 + c] = (float)s;
       continue;
     }
-    if (MODE == 1 && !hit[g]) continue;
-    const double S = prev[u] + s;
-    const int cnt = pc[u] + dcnt[g];
+    const double S = s;
+    const int cnt = dcnt[g];
     S64[row * 64 + c] = S;
     if (c == 0) count[row] = cnt;
     float cf;
@@ -1686,7 +1656,7 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
   }
   if (MODE == 2) return;
   __syncthreads();
-  if (tid < ng && (MODE == 0 || hit[tid])) {
+  if (tid < ng) {
     const int64_t row = bh * N + g0 + tid;
     double nrm = 0.0;
 #pragma unroll 8
@@ -1697,7 +1667,210 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
     nrm64[row] = nrm;
     write_nsplit(nrm, nsplit + row * 8);
   }
-  if (MODE == 1 && blockIdx.x == 0 && tid == 0) mcount_next[bh] = 0;
+}
+
+// ------------------------------------------------------------------ later-round update (bf16)
+// k_gdelta: grid (ceil(N / 32), BH), 256 threads: the later rounds' update
+// of workgroup x's groups g0 = 32 x .. g0 + 31 of slice bh from the round's
+// moved-key records (key, group joined, group left): S += joins - leaves,
+// count += joins - leaves, then C, R, |r|^2 and its split as k_gsum forms them
+// for the groups any record touches.  In the later rounds few keys move, so
+// the update is mostly latency:
+//   - the owned groups' previous sums and counts are requested first, so
+//     that their loads overlap the record pass;
+//   - the touched (key, side) entries are sorted by group in LDS (counting
+//     sort, no padding);
+//   - the sorted list is cut into 32 contiguous ranges, one per 8-lane slot
+//     (lane j of a slot holds features 8 j .. 8 j + 7 of the slot's row, one
+//     16-byte load); a slot adds its rows in fp64 registers while the group
+//     stays the same and adds the partial sum into the LDS sums with atomics
+//     when it changes, so the atomics scale with the groups, not the rows.
+//     The member sums are exact in fp64 (see the bf16 group sums), so neither
+//     the cut nor the order of the atomics can change a bit.
+constexpr int kDeltaCh = 4096;  // records per pass (at most 2 entries each)
+constexpr int kDeltaU = 8;      // rows per slot and batch (two batches in flight)
+__global__ __launch_bounds__(256) void k_gdelta(const uint16_t* __restrict__ X,
+                                                const unsigned long long* __restrict__ mrec,
+                                                const int32_t* __restrict__ mcount_cur,
+                                                int32_t* __restrict__ mcount_next, int n, int N,
+                                                double* __restrict__ S64, int32_t* __restrict__ count,
+                                                float* __restrict__ C, uint16_t* __restrict__ R,
+                                                double* __restrict__ nrm64, uint16_t* __restrict__ nsplit) {
+  __shared__ uint32_t ent[2 * kDeltaCh];  // key | leave << 31, sorted by group
+  __shared__ uint8_t eg[2 * kDeltaCh];    // its group, relative to g0
+  __shared__ double acc[kGsumG * 64];
+  __shared__ float rsh[kGsumG * 65];
+  __shared__ int ecnt[kGsumG], ecur[kGsumG], eoff[kGsumG + 1], dcnt[kGsumG], hit[kGsumG];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t bh = blockIdx.y;
+  const int g0 = blockIdx.x * kGsumG, ng = min(kGsumG, N - g0);
+
+  // previous sums and counts: element (g, c) = (idx / 64, idx % 64), 8 per thread
+  constexpr int EPT = kGsumG * 64 / 256;
+  double prev[EPT];
+  int pc[EPT];
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int idx = tid + 256 * u, g = idx >> 6, c = idx & 63;
+    const int64_t row = bh * N + g0 + min(g, ng - 1);
+    prev[u] = S64[row * 64 + c];
+    pc[u] = count[row];
+  }
+  for (int i = tid; i < kGsumG * 64; i += 256) acc[i] = 0.0;
+  if (tid < kGsumG) {
+    ecnt[tid] = 0;
+    dcnt[tid] = 0;
+    hit[tid] = 0;
+  }
+
+  // (a slice records at most n moved keys; the clamp keeps the loads below in
+  // bounds even if the workspace was corrupted, e.g. shared by overlapping calls)
+  const int64_t total = min((int64_t)mcount_cur[bh], (int64_t)n);
+  constexpr int PER = kDeltaCh / 256;
+  const uint16_t* Xb = X + bh * (int64_t)n * 64;
+  const int slot = lane >> 3, j = lane & 7, gsl = 8 * wave + slot;
+  for (int64_t c0 = 0; c0 < total; c0 += kDeltaCh) {
+    uint32_t kv[PER];
+    int gj[PER], gl[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int64_t e = c0 + tid + 256 * u, ec = min(e, total - 1);
+      const unsigned long long r = mrec[bh * n + ec];
+      kv[u] = (uint32_t)min((int)(r >> 32) & 0x7fffffff, n - 1);
+      gj[u] = e < total ? (int)(r & 0xffffu) - g0 : -1;
+      gl[u] = e < total ? (int)((r >> 16) & 0xffffu) - g0 : -1;
+    }
+    __syncthreads();  // zeroed counters; the previous pass is done with the list
+    // 1. count, offsets, scatter (the list keeps the groups in order)
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+#pragma unroll
+      for (int side = 0; side < 2; ++side) {
+        const int g = side ? gl[u] : gj[u];
+        if ((unsigned)g < (unsigned)ng) {
+          atomicAdd(&ecnt[g], 1);
+          atomicAdd(&dcnt[g], side ? -1 : 1);
+          hit[g] = 1;
+        }
+      }
+    __syncthreads();
+    if (wave == 0) {
+      const int c = lane < kGsumG ? ecnt[lane] : 0;
+      int incl = c;
+#pragma unroll
+      for (int off = 1; off < 32; off <<= 1) {
+        const int y = __shfl_up(incl, off);
+        if (lane >= off) incl += y;
+      }
+      if (lane < kGsumG) {
+        eoff[lane] = incl - c;
+        ecur[lane] = incl - c;
+      }
+      if (lane == kGsumG - 1) eoff[kGsumG] = incl;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+#pragma unroll
+      for (int side = 0; side < 2; ++side) {
+        const int g = side ? gl[u] : gj[u];
+        if ((unsigned)g < (unsigned)ng) {
+          const int pos = atomicAdd(&ecur[g], 1);
+          ent[pos] = kv[u] | ((uint32_t)side << 31);
+          eg[pos] = (uint8_t)g;
+        }
+      }
+    __syncthreads();
+    // 2. slot gsl adds entries [b0, b1) (ranges of ne / 32, differing by at most one)
+    const int ne = eoff[kGsumG];
+    if (ne > 0) {
+      const int b0 = (int)((int64_t)gsl * ne / 32), b1 = (int)((int64_t)(gsl + 1) * ne / 32);
+      const int steps = (ne + 31) / 32;
+      double a[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+      int cur = -1;
+      auto load = [&](int k0, uint32_t (&ei)[kDeltaU], int (&gi)[kDeltaU], u32x4 (&w)[kDeltaU]) {
+#pragma unroll
+        for (int u = 0; u < kDeltaU; ++u) {
+          const int e = min(b0 + k0 + u, ne - 1);
+          ei[u] = ent[e];
+          gi[u] = eg[e];
+          w[u] = *(const u32x4*)(Xb + (int64_t)(ei[u] & 0x7fffffffu) * 64 + 8 * j);
+        }
+      };
+      auto flush = [&]() {
+        double* p = acc + cur * 64 + 8 * j;
+#pragma unroll
+        for (int f = 0; f < 8; ++f) {
+          atomicAdd(p + f, a[f]);
+          a[f] = 0.0;
+        }
+      };
+      auto add = [&](int k0, const uint32_t (&ei)[kDeltaU], const int (&gi)[kDeltaU], const u32x4 (&w)[kDeltaU]) {
+#pragma unroll
+        for (int u = 0; u < kDeltaU; ++u) {
+          if (b0 + k0 + u >= b1) break;
+          if (gi[u] != cur) {
+            if (cur >= 0) flush();
+            cur = gi[u];
+          }
+          const double sg = (ei[u] >> 31) ? -1.0 : 1.0;
+#pragma unroll
+          for (int f = 0; f < 8; ++f)
+            a[f] = fma(sg, (double)bf16_to_f32((w[u][f >> 1] >> (16 * (f & 1))) & 0xffffu), a[f]);
+        }
+      };
+      uint32_t eA[kDeltaU], eB[kDeltaU];
+      int gA[kDeltaU], gB[kDeltaU];
+      u32x4 wA[kDeltaU], wB[kDeltaU];
+      load(0, eA, gA, wA);
+      for (int k0 = 0; k0 < steps; k0 += 2 * kDeltaU) {
+        if (k0 + kDeltaU < steps) load(k0 + kDeltaU, eB, gB, wB);
+        add(k0, eA, gA, wA);
+        if (k0 + kDeltaU >= steps) break;
+        if (k0 + 2 * kDeltaU < steps) load(k0 + 2 * kDeltaU, eA, gA, wA);
+        add(k0 + kDeltaU, eB, gB, wB);
+      }
+      if (cur >= 0) flush();
+    }
+    __syncthreads();
+    if (tid < kGsumG) ecnt[tid] = 0;
+  }
+  __syncthreads();
+
+  // the touched groups: S, count, C (an empty group keeps C), R, |r|^2
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int idx = tid + 256 * u, g = idx >> 6, c = idx & 63;
+    if (g >= ng || !hit[g]) continue;
+    const int64_t row = bh * N + g0 + g;
+    const double S = prev[u] + acc[g * 64 + c];
+    const int cnt = pc[u] + dcnt[g];
+    S64[row * 64 + c] = S;
+    if (c == 0) count[row] = cnt;
+    float cf;
+    if (cnt > 0) {
+      cf = (float)(S / (double)cnt);
+      C[row * 64 + c] = cf;
+    } else {
+      cf = C[row * 64 + c];
+    }
+    const float r = BF16::rep(cf);
+    BF16::store(R, row * 64 + c, r);
+    rsh[g * 65 + c] = r;
+  }
+  __syncthreads();
+  if (tid < ng && hit[tid]) {
+    const int64_t row = bh * N + g0 + tid;
+    double nrm = 0.0;
+#pragma unroll 8
+    for (int c = 0; c < 64; ++c) {
+      const double rc = (double)rsh[tid * 65 + c];
+      nrm = fma(rc, rc, nrm);
+    }
+    nrm64[row] = nrm;
+    write_nsplit(nrm, nsplit + row * 8);
+  }
+  if (blockIdx.x == 0 && tid == 0) mcount_next[bh] = 0;
 }
 
 // ------------------------------------------------------------------ attention (bf16)
@@ -2301,14 +2474,14 @@ hipError_t launch_gsum(const Dims& d, int mode, const void* X, const int32_t* be
   const uint16_t* Xb = (const uint16_t*)X;
   uint16_t* Rb = (uint16_t*)R;
   if (mode == 0)
-    hipLaunchKernelGGL(k_gsum<0>, grid, block, lds, st, Xb, belong, mrec, mcount_cur, mcount_next, d.n, d.N, S64,
-                       count, out, Rb, nrm64, nsplit, 0.f, 0);
+    hipLaunchKernelGGL(k_gsum<0>, grid, block, lds, st, Xb, belong, d.n, d.N, S64, count, out, Rb, nrm64, nsplit,
+                       0.f, 0);
   else if (mode == 1)
-    hipLaunchKernelGGL(k_gsum<1>, grid, block, lds, st, Xb, belong, mrec, mcount_cur, mcount_next, d.n, d.N, S64,
-                       count, out, Rb, nrm64, nsplit, 0.f, 0);
+    hipLaunchKernelGGL(k_gdelta, grid, block, 0, st, Xb, mrec, mcount_cur, mcount_next, d.n, d.N, S64, count, out,
+                       Rb, nrm64, nsplit);
   else
-    hipLaunchKernelGGL(k_gsum<2>, grid, block, lds, st, Xb, belong, mrec, mcount_cur, mcount_next, d.n, d.N, S64,
-                       count, out, Rb, nrm64, nsplit, 0.f, 0);
+    hipLaunchKernelGGL(k_gsum<2>, grid, block, lds, st, Xb, belong, d.n, d.N, S64, count, out, Rb, nrm64, nsplit,
+                       0.f, 0);
   return hipGetLastError();
 }
 
@@ -2322,9 +2495,9 @@ hipError_t launch_valuesum_prep(const Dims& d, const void* V, const int32_t* bel
   TimedLaunch timed("valuesum", st);
   if (d.dtype != 1) return hipErrorInvalidValue;
   const dim3 grid(cdiv(d.N, kGsumG), (unsigned)d.BH), block(256);
-  hipLaunchKernelGGL(k_gsum<3>, grid, block, 0, st, (const uint16_t*)V, belong, (const unsigned long long*)nullptr,
-                     (const int32_t*)nullptr, (int32_t*)nullptr, d.n, d.N, (double*)nullptr, (int32_t*)count,
-                     ginit, Vt, (double*)nullptr, (uint16_t*)nullptr, 1.0f / clamp_sl2e(scale), vt_stride(d.N));
+  hipLaunchKernelGGL(k_gsum<3>, grid, block, 0, st, (const uint16_t*)V, belong, d.n, d.N, (double*)nullptr,
+                     (int32_t*)count, ginit, Vt, (double*)nullptr, (uint16_t*)nullptr, 1.0f / clamp_sl2e(scale),
+                     vt_stride(d.N));
   return hipGetLastError();
 }
 
