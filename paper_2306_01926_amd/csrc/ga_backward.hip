@@ -19,9 +19,10 @@
 //   k_bwd_prep    per slice: R = bf16(centroid) rows and transposed, bf16
 //                 value means, log2(count) (-inf for an empty group)
 //   k_bwd_query   per 32-query tile (lane = query): MFMA scores, the group
-//                 softmax, MFMA dw, D, dp, MFMA dQ; stores the softmax shift,
-//                 1 / sum and D of every query (N > 128: three passes over the
-//                 32-group blocks instead of all scores in registers)
+//                 softmax, MFMA dw, D, dp, MFMA dQ; stores each query's
+//                 softmax shift plus log2 of its sum (so that a weight is one
+//                 exp2) and D (N > 128: three passes over the 32-group blocks
+//                 instead of all scores in registers)
 //   k_bwd_group   per (32-group block, query chunk): the same scores and dw
 //                 in the transposed layout (lane = group), so that the dp and
 //                 w registers are directly the A operand of the MFMA
@@ -45,6 +46,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBs = 72;       // LDS row stride (bf16) of group rows and wave tiles
 constexpr int kBwdChunks = 8;  // query chunks per slice in k_bwd_group
@@ -56,6 +58,15 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) { return bf16_bits
 __device__ __forceinline__ f32x16 mfma(const u32x4& a, const u32x4& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
                                                  0, 0);
+}
+// LDS transpose read (ds_read_b64_tr_b16): within each 16-lane block, lane
+// i receives element i % 4 of the 8-byte rows addressed by block lanes
+// 4 j + i / 4, j = 0..3 (element j of the result from row j).  With block
+// lane 4 j + s addressing row j at columns c0 + 4 s .. + 3, lane i gets
+// column c0 + i of the four rows.
+__device__ __forceinline__ u32x2 lds_tr16(const uint16_t* p) {
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
+  return __builtin_bit_cast(u32x2, v);
 }
 __device__ __forceinline__ f32x16 zero16() {
   f32x16 z;
@@ -130,7 +141,7 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
                                                    const uint16_t* __restrict__ R, const uint16_t* __restrict__ RT,
                                                    const uint16_t* __restrict__ MU, const float* __restrict__ LC,
                                                    int n, int rts, float scale, float sl2e, int tpw,
-                                                   uint16_t* __restrict__ dQ, float4* __restrict__ stats) {
+                                                   uint16_t* __restrict__ dQ, float2* __restrict__ stats) {
   constexpr int Npad = NB * 32;
   __shared__ __attribute__((aligned(16))) uint16_t Rs[Npad * kBs];
   __shared__ __attribute__((aligned(16))) uint16_t Ms[Npad * kBs];
@@ -195,7 +206,7 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
         o1 = mfma(u32x4{a1l[0], a1l[1], a1h[0], a1h[1]}, bf, o1);
       }
     };
-    float Ms_, inv, Dq;
+    float Ms_, inv, Dq, Lq;  // Lq: the shift plus log2 of the sum (+inf if every group is empty)
     if constexpr (NB <= 4) {
       // all blocks' weights held in registers; each block's dw is formed
       // twice (for D, then for dp) rather than held
@@ -234,6 +245,7 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
         }
       S += __shfl_xor(S, 32);
       inv = any ? 1.0f / S : 0.f;
+      Lq = any ? Ms_ + log2f(S) : INFINITY;
       Dq = 0.f;
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
@@ -281,6 +293,7 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
       S += __shfl_xor(S, 32);
       SD += __shfl_xor(SD, 32);
       inv = any ? 1.0f / S : 0.f;
+      Lq = any ? Ms_ + log2f(S) : INFINITY;
       Dq = SD * inv;
       for (int b = 0; b < NB; ++b) {
         f32x16 a, d;
@@ -312,21 +325,25 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
       const int64_t qo = t * 32 + row;
       if (qo < n) *(u32x4*)(dQ + (bh * (int64_t)n + qo) * 64 + 8 * ch) = *(const u32x4*)(Ow + row * kBs + 8 * ch);
     }
-    if (h == 0 && qi < n) stats[bh * (int64_t)n + qi] = make_float4(Ms_, inv, Dq, 0.f);
+    if (h == 0 && qi < n) stats[bh * (int64_t)n + qi] = make_float2(Lq, Dq);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 }
 
-// grid (NB, kBwdChunks, BH), 256 threads: group block b of a slice over query
-// chunk c (tiles [c T / chunks, (c + 1) T / chunks), wave w takes every 4th).
+// 1-D grid of ceil(NB kBwdChunks BH / 8) * 8 workgroups, 256 threads: work
+// item (bh, chunk, b) is group block b of slice bh over query chunk c (tiles
+// [c T / chunks, (c + 1) T / chunks), wave w takes every 4th).  Items are
+// handed to the XCDs in contiguous ranges (workgroup x runs on XCD x % 8), so
+// the NB group blocks that read the same query and dO rows run together on
+// one XCD and share its L2.
 // part[bh][c][0/1][g][f] = this chunk's sum_i dp_gi q_if / sum_i w_gi G_if.
 template <int NB>
 __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ G,
                                                    const uint16_t* __restrict__ R, const uint16_t* __restrict__ MU,
-                                                   const float* __restrict__ LC, const float4* __restrict__ stats,
-                                                   int n, float sl2e, float* __restrict__ part) {
+                                                   const float* __restrict__ LC, const float2* __restrict__ stats,
+                                                   int n, int64_t BH, float sl2e, float* __restrict__ part) {
   constexpr int Npad = NB * 32;
   // the waves' query tiles; after the loop the same bytes hold two partial
   // slots [2][2][32][64] (waves 0, 1 write, waves 2, 3 add: fixed order)
@@ -335,12 +352,14 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
   uint16_t* Qt = (uint16_t*)lds;  // [4][32][kBs]
   uint16_t* Gt = Qt + 4 * 32 * kBs;
   float* red = (float*)lds;
-  __shared__ float4 st[4][32];
+  __shared__ __attribute__((aligned(16))) float2 st[4][32];  // (Lq, D) of the wave's tile queries
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, gl = lane & 31;
-  const int b = blockIdx.x, chunk = blockIdx.y;
-  const int64_t bh = blockIdx.z;
+  const int64_t item = (int64_t)(blockIdx.x % 8) * (gridDim.x / 8) + blockIdx.x / 8;
+  if (item >= NB * kBwdChunks * BH) return;  // grid padding (whole workgroup)
+  const int b = (int)(item % NB), chunk = (int)(item / NB % kBwdChunks);
+  const int64_t bh = item / (NB * kBwdChunks);
   const int64_t ntiles = ((int64_t)n + 31) / 32;
-  const int64_t c0 = chunk * ntiles / gridDim.y, c1 = (chunk + 1) * ntiles / gridDim.y;
+  const int64_t c0 = chunk * ntiles / kBwdChunks, c1 = (chunk + 1) * ntiles / kBwdChunks;
   const uint16_t* Qb = Q + bh * (int64_t)n * 64;
   const uint16_t* Gb = G + bh * (int64_t)n * 64;
   const int g = 32 * b + gl;  // this lane's group (MFMA column / A-operand row)
@@ -354,8 +373,8 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
   f32x16 dr0 = zero16(), dr1 = zero16(), dm0 = zero16(), dm1 = zero16();
   // the wave's next tile (its query stats, then its rows) loads while the
   // current one is processed
-  const float4* statb = stats + bh * (int64_t)n;
-  float4 sn = statb[min((c0 + wave) * 32 + gl, (int64_t)n - 1)];
+  const float2* statb = stats + bh * (int64_t)n;
+  float2 sn = statb[min((c0 + wave) * 32 + gl, (int64_t)n - 1)];
   u32x4 qn[4], gn[4];
   load_row_frags(Qb, min((c0 + wave) * 32 + gl, (int64_t)n - 1), qn);
   load_row_frags(Gb, min((c0 + wave) * 32 + gl, (int64_t)n - 1), gn);
@@ -369,7 +388,7 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
       qf[s] = qn[s];
       gf[s] = gn[s];
     }
-    const float4 sc = sn;
+    const float2 sc = sn;
     // unconditional (rows clamped; past the chunk it loads a row again), so
     // the loads stay in this block, ahead of the tile's work
     sn = statb[min(qi + 128, (int64_t)n - 1)];
@@ -381,7 +400,7 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
       *(u32x4*)(Qw + gl * kBs + 32 * h + 8 * s) = qf[s];
       *(u32x4*)(Gw + gl * kBs + 32 * h + 8 * s) = gf[s];
     }
-    if (h == 0) st[wave][gl] = qi < n ? sc : make_float4(0.f, 0.f, 0.f, 0.f);
+    if (h == 0) st[wave][gl] = qi < n ? sc : make_float2(INFINITY, 0.f);  // padded query: w = 0
     // scores and dw with queries as rows, groups as columns
     f32x16 x = zero16(), dw = zero16();
 #pragma unroll
@@ -392,15 +411,21 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // register v: query 8 (v / 4) + 4 h + v % 4 of the tile; padded queries get w = 0
+    // register v: query 8 (v / 4) + 4 h + v % 4 of the tile (two queries'
+    // (Lq, D) per 16-byte read); w = 2^(p log2 e + log2 c - Lq)
     float w[16], dp[16];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int r = 8 * (v >> 2) + 4 * h + (v & 3);
-      const float4 sq = st[wave][r];
-      const float e = __builtin_amdgcn_exp2f(fmaf(x[v], sl2e, lcg) - sq.x);
-      w[v] = t * 32 + r < n ? e * sq.y : 0.f;
-      dp[v] = w[v] * (dw[v] - sq.z);
+    for (int a = 0; a < 4; ++a) {
+#pragma unroll
+      for (int p2 = 0; p2 < 2; ++p2) {
+        const float4 sq = *(const float4*)&st[wave][8 * a + 4 * h + 2 * p2];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const int v = 4 * a + 2 * p2 + k;
+          w[v] = __builtin_amdgcn_exp2f(fmaf(x[v], sl2e, lcg) - (k ? sq.z : sq.x));
+          dp[v] = w[v] * (dw[v] - (k ? sq.w : sq.y));
+        }
+      }
     }
     // dr[g][f] += sum_q dp[g][q] Q[q][f]; dmu[g][f] += sum_q w[g][q] G[q][f]
 #pragma unroll
@@ -409,21 +434,19 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
                          pack2(dp[8 * u + 4], dp[8 * u + 5]), pack2(dp[8 * u + 6], dp[8 * u + 7])};
       const u32x4 aw = {pack2(w[8 * u], w[8 * u + 1]), pack2(w[8 * u + 2], w[8 * u + 3]),
                         pack2(w[8 * u + 4], w[8 * u + 5]), pack2(w[8 * u + 6], w[8 * u + 7])};
-      const int r0 = 16 * u + 4 * h;  // queries r0 .. r0 + 3 and r0 + 8 .. r0 + 11
+      // B operands: lane (feature 32 fb + gl, h) takes queries r0 .. r0 + 3,
+      // r0 + 8 .. r0 + 11 of the tile (the k order of the A operand), two
+      // transpose reads each: block lane 4 j + s addresses query row r0 + j
+      // (then r0 + 8 + j) at features 32 fb + 16 (lane / 16 % 2) + 4 s
+      const int r0 = 16 * u + 4 * h;
+      const int tro = (r0 + ((lane & 15) >> 2)) * kBs + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
       u32x4 bq[2], bg[2];
 #pragma unroll
       for (int fb = 0; fb < 2; ++fb) {
-        const int f = 32 * fb + gl;
-        uint32_t vq[8], vg[8];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          vq[j] = Qw[(r0 + j) * kBs + f];
-          vq[4 + j] = Qw[(r0 + 8 + j) * kBs + f];
-          vg[j] = Gw[(r0 + j) * kBs + f];
-          vg[4 + j] = Gw[(r0 + 8 + j) * kBs + f];
-        }
-        bq[fb] = u32x4{vq[0] | (vq[1] << 16), vq[2] | (vq[3] << 16), vq[4] | (vq[5] << 16), vq[6] | (vq[7] << 16)};
-        bg[fb] = u32x4{vg[0] | (vg[1] << 16), vg[2] | (vg[3] << 16), vg[4] | (vg[5] << 16), vg[6] | (vg[7] << 16)};
+        const u32x2 q0 = lds_tr16(Qw + tro + 32 * fb), q1 = lds_tr16(Qw + tro + 8 * kBs + 32 * fb);
+        const u32x2 g0 = lds_tr16(Gw + tro + 32 * fb), g1 = lds_tr16(Gw + tro + 8 * kBs + 32 * fb);
+        bq[fb] = u32x4{q0[0], q0[1], q1[0], q1[1]};
+        bg[fb] = u32x4{g0[0], g0[1], g1[0], g1[1]};
       }
       dr0 = mfma(adp, bq[0], dr0);
       dr1 = mfma(adp, bq[1], dr1);
@@ -459,7 +482,7 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
     }
     __syncthreads();
   }
-  float* out = part + ((bh * gridDim.y + chunk) * 2) * (int64_t)Npad * 64;
+  float* out = part + ((bh * kBwdChunks + chunk) * 2) * (int64_t)Npad * 64;
   for (int x = tid; x < 2 * 32 * 64; x += 256) {
     const int k = x / (32 * 64), e = x % (32 * 64);
     const float s = red[k * 32 * 64 + e] + red[2 * 32 * 64 + k * 32 * 64 + e];  // (w0 + w2) + (w1 + w3)
@@ -523,7 +546,7 @@ size_t backward_workspace_layout(const Dims& d, BackwardWorkspace* w, void* base
   void* RT = take((size_t)d.BH * 64 * rts * 2);
   void* MU = take((size_t)d.BH * Npad * 64 * 2);
   void* LC = take((size_t)d.BH * Npad * 4);
-  void* ST = take((size_t)d.BH * d.n * 16);
+  void* ST = take((size_t)d.BH * d.n * 8);
   void* PART = take((size_t)d.BH * kBwdChunks * 2 * Npad * 64 * 4);
   void* GK = take((size_t)d.BH * Npad * 64 * 4);
   void* GV = take((size_t)d.BH * Npad * 64 * 4);
@@ -550,7 +573,7 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
 #define GA_BWD_Q(NBV)                                                                                              \
   hipLaunchKernelGGL(k_bwd_query<NBV>, dim3(gq, (unsigned)d.BH), dim3(256), 0, st, (const uint16_t*)Q,            \
                      (const uint16_t*)dO, w.R, w.RT, w.MU, w.LC, d.n, rts, scale, sl2e, tpw, (uint16_t*)dQ,       \
-                     (float4*)w.stats)
+                     (float2*)w.stats)
     switch (NB) {
       case 1: GA_BWD_Q(1); break;
       case 2: GA_BWD_Q(2); break;
@@ -566,9 +589,9 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
   {
     TimedLaunch tl("bwd_group", st);
 #define GA_BWD_G(NBV)                                                                                              \
-  hipLaunchKernelGGL(k_bwd_group<NBV>, dim3(NBV, kBwdChunks, (unsigned)d.BH), dim3(256), 0, st,                   \
-                     (const uint16_t*)Q, (const uint16_t*)dO, w.R, w.MU, w.LC, (const float4*)w.stats, d.n, sl2e, \
-                     w.part)
+  hipLaunchKernelGGL(k_bwd_group<NBV>, dim3((unsigned)((NBV * kBwdChunks * d.BH + 7) / 8 * 8)), dim3(256), 0, st, \
+                     (const uint16_t*)Q, (const uint16_t*)dO, w.R, w.MU, w.LC, (const float2*)w.stats, d.n, d.BH,  \
+                     sl2e, w.part)
     switch (NB) {
       case 1: GA_BWD_G(1); break;
       case 2: GA_BWD_G(2); break;

@@ -128,7 +128,7 @@ struct BackwardWorkspace {
   uint16_t* RT;  // [BH][64][Npad + 4] the same, transposed
   uint16_t* MU;  // [BH][Npad][64] bf16 value means
   float* LC;     // [BH][Npad] log2(count), -inf for an empty group
-  void* stats;   // [BH][n] float4: softmax shift, 1 / sum, D = dO . o per query
+  void* stats;   // [BH][n] float2: softmax shift + log2(sum) (log2 domain), D = dO . o per query
   float* part;   // [BH][chunks][2][Npad][64] per-chunk sums of dp q and w dO
   float* gk;     // [BH][Npad][64] scale dr / count
   float* gv;     // [BH][Npad][64] dmu / count
