@@ -1422,6 +1422,69 @@ __global__ __launch_bounds__(256) void k_segsum(const typename S::T* __restrict_
 }
 
 // ------------------------------------------------------------------ group sums (bf16)
+// run_sums: the rows of a group-sorted entry list (ent: key | leave << 31;
+// eg: the entry's group within the workgroup's block) added into the LDS sums
+// acc[g][64] by one workgroup of 4 waves.  The list is cut into 32 contiguous
+// ranges, one per 8-lane slot (lane j of a slot holds features 8 j .. 8 j + 7
+// of the slot's row, one 16-byte load); a slot adds its rows in fp64
+// registers while the group stays the same and adds the partial sum into acc
+// with LDS atomics when it changes, so the atomics scale with the groups, not
+// the rows.  The member sums are exact in fp64 (see the bf16 member sums
+// above), so neither the cut nor the order of the atomics can change a bit.
+constexpr int kRunU = 8;  // rows per slot and batch (two batches in flight)
+__device__ __forceinline__ void run_sums(const uint32_t* ent, const uint8_t* eg, int ne,
+                                         const uint16_t* __restrict__ Xb, double* acc, int wave, int lane) {
+  if (ne <= 0) return;
+  const int j = lane & 7, gsl = 8 * wave + (lane >> 3);
+  const int b0 = (int)((int64_t)gsl * ne / 32), b1 = (int)((int64_t)(gsl + 1) * ne / 32);
+  const int steps = (ne + 31) / 32;  // >= every slot's range (they differ by at most one)
+  double a[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+  int cur = -1;
+  auto load = [&](int k0, uint32_t (&ei)[kRunU], int (&gi)[kRunU], u32x4 (&w)[kRunU]) {
+#pragma unroll
+    for (int u = 0; u < kRunU; ++u) {
+      const int e = min(b0 + k0 + u, ne - 1);
+      ei[u] = ent[e];
+      gi[u] = eg[e];
+      w[u] = *(const u32x4*)(Xb + (int64_t)(ei[u] & 0x7fffffffu) * 64 + 8 * j);
+    }
+  };
+  auto flush = [&]() {
+    double* p = acc + cur * 64 + 8 * j;
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      atomicAdd(p + f, a[f]);
+      a[f] = 0.0;
+    }
+  };
+  auto add = [&](int k0, const uint32_t (&ei)[kRunU], const int (&gi)[kRunU], const u32x4 (&w)[kRunU]) {
+#pragma unroll
+    for (int u = 0; u < kRunU; ++u) {
+      if (b0 + k0 + u >= b1) break;
+      if (gi[u] != cur) {
+        if (cur >= 0) flush();
+        cur = gi[u];
+      }
+      const double sg = (ei[u] >> 31) ? -1.0 : 1.0;
+#pragma unroll
+      for (int f = 0; f < 8; ++f)
+        a[f] = fma(sg, (double)bf16_to_f32((w[u][f >> 1] >> (16 * (f & 1))) & 0xffffu), a[f]);
+    }
+  };
+  uint32_t eA[kRunU], eB[kRunU];
+  int gA[kRunU], gB[kRunU];
+  u32x4 wA[kRunU], wB[kRunU];
+  load(0, eA, gA, wA);
+  for (int k0 = 0; k0 < steps; k0 += 2 * kRunU) {
+    if (k0 + kRunU < steps) load(k0 + kRunU, eB, gB, wB);
+    add(k0, eA, gA, wA);
+    if (k0 + kRunU >= steps) break;
+    if (k0 + 2 * kRunU < steps) load(k0 + 2 * kRunU, eA, gA, wA);
+    add(k0 + kRunU, eB, gB, wB);
+  }
+  if (cur >= 0) flush();
+}
+
 // The member sums of the bf16 path are exact in fp64 (see above), so they can
 // be accumulated in any order and split any way: no global bucketing.
 //
@@ -1436,27 +1499,22 @@ __global__ __launch_bounds__(256) void k_segsum(const typename S::T* __restrict_
 // group) and its split.  (The later rounds' update is k_gdelta.)
 //
 // Per chunk of keys, all loaded at once:
-// 1. count the entries (key) of every owned group, lay the groups out
-//    in LDS padded to multiples of 8 entries, scatter the entries (a local
-//    counting sort; one LDS atomic per entry);
-// 2. each wave takes a run of whole groups and sums 8 rows per instruction
-//    (row slot = lane / 8, 16 bytes = features 8 (lane % 8) .. +7 per lane)
-//    into 8 fp64 registers per lane; the next 8 chunks of 8 rows are loaded
-//    while the current 8 are added; at the end of a group the 8 slots are
-//    combined with cross-lane VALU moves and added into the LDS accumulator;
+// 1. count the keys of every owned group and scatter them into an LDS list
+//    sorted by group (a local counting sort; one LDS atomic per key);
+// 2. run_sums adds the rows into the LDS sums;
 // 3. finish the owned groups.
 constexpr int kGsumG = 32;
-constexpr int kGsumList = 8448;  // entry capacity of the sorted chunk list
+constexpr int kGsumList = 8192;  // entry capacity of the sorted chunk list
 template <int MODE>
 __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, const int32_t* __restrict__ belong,
                                               int n, int N, double* __restrict__ S64,
                                               int32_t* __restrict__ count, float* __restrict__ out, uint16_t* __restrict__ R,
                                               double* __restrict__ nrm64, uint16_t* __restrict__ nsplit,
                                               float inv_sl2e, int vts) {
-  __shared__ uint32_t ent[kGsumList];  // key; 0xffffffff pads a group to 8k entries
+  __shared__ uint32_t ent[kGsumList];  // keys sorted by group
+  __shared__ uint8_t eg[kGsumList];    // their groups, relative to g0
   __shared__ double acc[kGsumG * 64];  // [g][c] sums of this workgroup's groups
-  __shared__ double tws[4][8 * 64];    // per-wave [slot][feature] transpose tile of a finished group
-  __shared__ int ecnt[kGsumG], eoff[kGsumG + 1], ecur[kGsumG], dcnt[kGsumG], wbeg[5], wg0[4];
+  __shared__ int ecnt[kGsumG], eoff[kGsumG + 1], ecur[kGsumG], dcnt[kGsumG];
   float* rsh = (float*)ent;            // [32][65] bf16 representatives, after the sums
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bh = blockIdx.y;
@@ -1465,10 +1523,8 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
   if (tid < kGsumG) dcnt[tid] = 0;
 
   const int64_t total = n;
-  // entries per chunk: one per key plus 7 padding per group
-  constexpr int CH = 8192;
+  constexpr int CH = kGsumList;  // keys per chunk
   constexpr int PER = CH / 256;
-  static_assert(CH + 7 * kGsumG <= kGsumList, "chunk list overflow");
   const uint16_t* Xb = X + bh * (int64_t)n * 64;
   for (int64_t c0 = 0; c0 < total; c0 += CH) {
     int kv[PER], gj[PER];
@@ -1496,104 +1552,31 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
     __syncthreads();
     if (wave == 0) {
       const int c = lane < kGsumG ? ecnt[lane] : 0;
-      const int pc = (c + 7) & ~7;
-      int incl = pc;  // inclusive scan over the 32 groups
+      int incl = c;  // inclusive scan over the 32 groups
 #pragma unroll
       for (int off = 1; off < 32; off <<= 1) {
         const int y = __shfl_up(incl, off);
         if (lane >= off) incl += y;
       }
-      const int start = incl - pc, tot = __shfl(incl, kGsumG - 1);
       if (lane < kGsumG) {
-        eoff[lane] = start;
-        ecur[lane] = start;
-        for (int k = c; k < pc; ++k) ent[start + k] = 0xffffffffu;
+        eoff[lane] = incl - c;
+        ecur[lane] = incl - c;
       }
-      if (lane == 0) {
-        eoff[kGsumG] = tot;
-        wbeg[0] = 0;
-        wbeg[4] = tot;
-        wg0[0] = 0;
-      }
-      // wave w starts at the first group beginning at or after w tot / 4
-#pragma unroll
-      for (int w = 1; w < 4; ++w) {
-        const uint64_t m = __ballot(lane < kGsumG && start >= w * tot / 4);
-        const int g = m ? __ffsll((unsigned long long)m) - 1 : kGsumG;
-        const int gs = __shfl(start, g < kGsumG ? g : 0);  // all lanes take part
-        if (lane == 0) {
-          wbeg[w] = g < kGsumG ? gs : tot;
-          wg0[w] = g;
-        }
-      }
+      if (lane == kGsumG - 1) eoff[kGsumG] = incl;
     }
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int g = gj[u];
-      if ((unsigned)g < (unsigned)ng) ent[atomicAdd(&ecur[g], 1)] = (uint32_t)kv[u];
-    }
-    __syncthreads();
-    // 2. per-wave register sums over runs of whole groups
-    {
-      const int slot = lane >> 3, j = lane & 7;
-      const int cb = wbeg[wave] / 8, ce = wbeg[wave + 1] / 8;
-      double a[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
-      int g = wg0[wave], gend = 0;  // current group and its end chunk
-      // a finished group: the 8 slot rows go through the wave's LDS tile,
-      // lane = feature adds them and adds the sum into the group's LDS row
-      // (other waves may add to the same group)
-      double* tw = tws[wave];
-      auto flush = [&]() {
-#pragma unroll
-        for (int k = 0; k < 8; k += 2) *(double2*)(tw + slot * 64 + 8 * j + k) = double2{a[k], a[k + 1]};
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        double v = tw[lane];
-#pragma unroll
-        for (int k = 1; k < 8; ++k) v += tw[k * 64 + lane];
-        atomicAdd(&acc[g * 64 + lane], v);
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-        for (int k = 0; k < 8; ++k) a[k] = 0.0;
-      };
-      auto add = [&](int ch0, const uint32_t (&e)[kGsumU], const u32x4 (&w)[kGsumU]) {
-#pragma unroll
-        for (int u = 0; u < kGsumU; ++u) {
-          const int ch = ch0 + u;
-          if (ch >= ce) break;
-          if (ch >= gend) {  // next non-empty group (uniform)
-            if (ch > cb) flush();
-            while (eoff[g + 1] <= ch * 8) ++g;
-            gend = eoff[g + 1] / 8;
-          }
-          const double sg = e[u] == 0xffffffffu ? 0.0 : 1.0;
-#pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            const uint32_t bits = (k & 1) ? (w[u][k >> 1] >> 16) : (w[u][k >> 1] & 0xffffu);
-            a[k] = fma(sg, (double)bf16_to_f32(bits), a[k]);
-          }
-        }
-      };
-      if (cb < ce) {
-        uint32_t eA[kGsumU], eB[kGsumU];
-        u32x4 wA[kGsumU], wB[kGsumU];
-        gsum_load(ent, Xb, cb, ce, slot, j, eA, wA);
-        for (int ch0 = cb; ch0 < ce; ch0 += 2 * kGsumU) {
-          gsum_load(ent, Xb, ch0 + kGsumU, ce, slot, j, eB, wB);
-          __builtin_amdgcn_sched_barrier(0);
-          add(ch0, eA, wA);
-          if (ch0 + kGsumU >= ce) break;
-          gsum_load(ent, Xb, ch0 + 2 * kGsumU, ce, slot, j, eA, wA);
-          __builtin_amdgcn_sched_barrier(0);
-          add(ch0 + kGsumU, eB, wB);
-        }
-        flush();
+      if ((unsigned)g < (unsigned)ng) {
+        const int pos = atomicAdd(&ecur[g], 1);
+        ent[pos] = (uint32_t)kv[u];
+        eg[pos] = (uint8_t)g;
       }
     }
+    __syncthreads();
+    // 2. the rows, summed per group
+    run_sums(ent, eg, eoff[kGsumG], Xb, acc, wave, lane);
     __syncthreads();
   }
 
@@ -1680,15 +1663,8 @@ __global__ __launch_bounds__(256) void k_gsum(const uint16_t* __restrict__ X, co
 //     that their loads overlap the record pass;
 //   - the touched (key, side) entries are sorted by group in LDS (counting
 //     sort, no padding);
-//   - the sorted list is cut into 32 contiguous ranges, one per 8-lane slot
-//     (lane j of a slot holds features 8 j .. 8 j + 7 of the slot's row, one
-//     16-byte load); a slot adds its rows in fp64 registers while the group
-//     stays the same and adds the partial sum into the LDS sums with atomics
-//     when it changes, so the atomics scale with the groups, not the rows.
-//     The member sums are exact in fp64 (see the bf16 group sums), so neither
-//     the cut nor the order of the atomics can change a bit.
+//   - run_sums adds the rows (joins +, leaves -).
 constexpr int kDeltaCh = 4096;  // records per pass (at most 2 entries each)
-constexpr int kDeltaU = 8;      // rows per slot and batch (two batches in flight)
 __global__ __launch_bounds__(256) void k_gdelta(const uint16_t* __restrict__ X,
                                                 const unsigned long long* __restrict__ mrec,
                                                 const int32_t* __restrict__ mcount_cur,
@@ -1728,7 +1704,6 @@ __global__ __launch_bounds__(256) void k_gdelta(const uint16_t* __restrict__ X,
   const int64_t total = min((int64_t)mcount_cur[bh], (int64_t)n);
   constexpr int PER = kDeltaCh / 256;
   const uint16_t* Xb = X + bh * (int64_t)n * 64;
-  const int slot = lane >> 3, j = lane & 7, gsl = 8 * wave + slot;
   for (int64_t c0 = 0; c0 < total; c0 += kDeltaCh) {
     uint32_t kv[PER];
     int gj[PER], gl[PER];
@@ -1781,57 +1756,8 @@ __global__ __launch_bounds__(256) void k_gdelta(const uint16_t* __restrict__ X,
         }
       }
     __syncthreads();
-    // 2. slot gsl adds entries [b0, b1) (ranges of ne / 32, differing by at most one)
-    const int ne = eoff[kGsumG];
-    if (ne > 0) {
-      const int b0 = (int)((int64_t)gsl * ne / 32), b1 = (int)((int64_t)(gsl + 1) * ne / 32);
-      const int steps = (ne + 31) / 32;
-      double a[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
-      int cur = -1;
-      auto load = [&](int k0, uint32_t (&ei)[kDeltaU], int (&gi)[kDeltaU], u32x4 (&w)[kDeltaU]) {
-#pragma unroll
-        for (int u = 0; u < kDeltaU; ++u) {
-          const int e = min(b0 + k0 + u, ne - 1);
-          ei[u] = ent[e];
-          gi[u] = eg[e];
-          w[u] = *(const u32x4*)(Xb + (int64_t)(ei[u] & 0x7fffffffu) * 64 + 8 * j);
-        }
-      };
-      auto flush = [&]() {
-        double* p = acc + cur * 64 + 8 * j;
-#pragma unroll
-        for (int f = 0; f < 8; ++f) {
-          atomicAdd(p + f, a[f]);
-          a[f] = 0.0;
-        }
-      };
-      auto add = [&](int k0, const uint32_t (&ei)[kDeltaU], const int (&gi)[kDeltaU], const u32x4 (&w)[kDeltaU]) {
-#pragma unroll
-        for (int u = 0; u < kDeltaU; ++u) {
-          if (b0 + k0 + u >= b1) break;
-          if (gi[u] != cur) {
-            if (cur >= 0) flush();
-            cur = gi[u];
-          }
-          const double sg = (ei[u] >> 31) ? -1.0 : 1.0;
-#pragma unroll
-          for (int f = 0; f < 8; ++f)
-            a[f] = fma(sg, (double)bf16_to_f32((w[u][f >> 1] >> (16 * (f & 1))) & 0xffffu), a[f]);
-        }
-      };
-      uint32_t eA[kDeltaU], eB[kDeltaU];
-      int gA[kDeltaU], gB[kDeltaU];
-      u32x4 wA[kDeltaU], wB[kDeltaU];
-      load(0, eA, gA, wA);
-      for (int k0 = 0; k0 < steps; k0 += 2 * kDeltaU) {
-        if (k0 + kDeltaU < steps) load(k0 + kDeltaU, eB, gB, wB);
-        add(k0, eA, gA, wA);
-        if (k0 + kDeltaU >= steps) break;
-        if (k0 + 2 * kDeltaU < steps) load(k0 + 2 * kDeltaU, eA, gA, wA);
-        add(k0 + kDeltaU, eB, gB, wB);
-      }
-      if (cur >= 0) flush();
-    }
+    // 2. the rows, summed per group
+    run_sums(ent, eg, eoff[kGsumG], Xb, acc, wave, lane);
     __syncthreads();
     if (tid < kGsumG) ecnt[tid] = 0;
   }
