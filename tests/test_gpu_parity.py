@@ -100,6 +100,39 @@ def test_cluster_with_caller_init(oracle_mod, dev):
     assert_groups_equal(got, ref)
 
 
+def emptying_group_case(N=3, active=(0, 1, 2)):
+    """Keys on the first axis: -1 x2, -0.5625 x18, -0.375, +0.3125, +0.5625 x18,
+    +1 x2 (exact in bf16); caller init -1, 0, +1 for the groups `active`
+    (any other group starts far away on its own axis and never gets a key).
+    Round 1 gives the middle group the keys at -0.375 and +0.3125 (its
+    centroid becomes -0.03125); the update moves the outer groups to -0.60625
+    and +0.60625, so in round 2 both keys leave and the middle group is empty
+    from then on, keeping -0.03125 (neither its initial value nor zero)."""
+    xs = [-1.0] * 2 + [-0.5625] * 18 + [-0.375, 0.3125] + [0.5625] * 18 + [1.0] * 2
+    K = np.zeros((1, 1, len(xs), 64), np.float32)
+    K[0, 0, :, 0] = xs
+    init = np.zeros((1, 1, N, 64), np.float32)
+    for j in range(N):
+        init[0, 0, j, 1 + j % 63] = 8.0  # far from every key
+    for j, x in zip(active, (-1.0, 0.0, 1.0)):
+        init[0, 0, j] = 0.0
+        init[0, 0, j, 0] = x
+    return inputs.to_storage(K, "bf16"), torch.from_numpy(init)
+
+
+@pytest.mark.parametrize("N,active", [(3, (0, 1, 2)), (40, (0, 33, 39))], ids=["N3", "N40-block1"])
+def test_cluster_group_empties_in_a_later_round(oracle_mod, dev, N, active):
+    say(f"cluster: a group loses every member in round 2 (N={N}, groups {active})")
+    K, init = emptying_group_case(N, active)
+    mid = active[1]
+    ref = oracle_mod.cluster(f64(K), N, 4, "bf16", init=init.numpy(), trace=True)
+    counts = [np.bincount(b.ravel(), minlength=N)[mid] for b in ref["trace_belong"]]
+    assert counts[0] == 2 and all(c == 0 for c in counts[1:]), counts  # the case does what it says
+    got, ref = cluster_both(oracle_mod, K, N, 4, "bf16", dev, init=init)
+    assert_groups_equal(got, ref)
+    assert got[2][0, 0, mid, 0] == np.float32(-0.03125) and got[1][0, 0, mid] == 0
+
+
 def test_cluster_stepwise_against_trace(oracle_mod, dev):
     """Round t fed the oracle's C^(t-1): isolates each round from earlier ones."""
     say("stepwise cluster rounds")
