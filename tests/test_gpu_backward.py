@@ -106,6 +106,33 @@ def test_backward_with_empty_groups_and_determinism(oracle_mod, dev):
         assert torch.equal(x, y)
 
 
+@pytest.mark.parametrize("N", [40, 200])
+def test_backward_slice_with_every_group_empty(oracle_mod, dev, N):
+    """Slice 1 has no member in any group (counts 0): every weight is 0, so its
+    dQ, dK, dV are exactly 0 (no NaN from the empty softmax); slice 0 is an
+    ordinary grouping."""
+    say(f"backward, one slice with every group empty (N={N})")
+    n = 300
+    rng = np.random.default_rng(21)
+    Q, K, V = inputs.make_qkv(1, 2, n, 64, "bf16", 22, 16, 0.05, 0.2)
+    dO = inputs.to_storage(rng.standard_normal((1, 2, n, 64)).astype(np.float32), "bf16")
+    belong = np.zeros((1, 2, n), np.int32)
+    belong[0, 0] = rng.integers(0, N, n)
+    count = np.zeros((1, 2, N), np.int32)
+    count[0, 0] = np.bincount(belong[0, 0], minlength=N)
+    Kd, Vd = f64(K), f64(V)
+    cen = rng.standard_normal((1, 2, N, 64)).astype(np.float32) * 0.1
+    vs = np.zeros((1, 2, N, 64))
+    for j in range(N):
+        m = belong[0, 0] == j
+        if m.any():
+            cen[0, 0, j] = Kd[0, 0][m].mean(0)
+            vs[0, 0, j] = Vd[0, 0][m].sum(0)
+    dQ, dK, dV = run_both(oracle_mod, dev, Q, dO, belong, count, cen, vs, N)
+    for X in (dQ, dK, dV):
+        assert torch.count_nonzero(X[0, 1]) == 0
+
+
 def test_full_size_slices(oracle_mod, dev):
     w = inputs.WORKLOADS["n8000_N128_bf16"]
     say(f"backward on 2 full-size slices of {w.name}")
