@@ -49,7 +49,17 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBs = 72;       // LDS row stride (bf16) of group rows and wave tiles
-constexpr int kBwdChunks = 8;  // query chunks per slice in k_bwd_group
+// Query chunks per slice in k_bwd_group: as few as give about kBwdTargetWgs
+// workgroups (two per CU of a 256-CU MI355X at the kernel's 2 waves per SIMD),
+// at most kBwdMaxChunks.  Each chunk writes its own partial sums, so fewer
+// chunks mean fewer partial bytes and longer runs per workgroup setup.  A
+// function of the shape only (the workspace size depends on it).
+constexpr int kBwdMaxChunks = 8;
+constexpr int64_t kBwdTargetWgs = 512;
+int bwd_chunks(int64_t BH, int NB) {
+  const int64_t c = (kBwdTargetWgs + NB * BH - 1) / (NB * BH);
+  return (int)(c < 1 ? 1 : (c > kBwdMaxChunks ? kBwdMaxChunks : c));
+}
 
 __device__ __forceinline__ uint32_t bf16_bits(float x) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x);  // round to nearest even
@@ -332,7 +342,7 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
   }
 }
 
-// 1-D grid of ceil(NB kBwdChunks BH / 8) * 8 workgroups, 256 threads: work
+// 1-D grid of ceil(NB chunks BH / 8) * 8 workgroups, 256 threads: work
 // item (bh, chunk, b) is group block b of slice bh over query chunk c (tiles
 // [c T / chunks, (c + 1) T / chunks), wave w takes every 4th).  Items are
 // handed to the XCDs in contiguous ranges (workgroup x runs on XCD x % 8), so
@@ -343,7 +353,8 @@ template <int NB>
 __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ G,
                                                    const uint16_t* __restrict__ R, const uint16_t* __restrict__ MU,
                                                    const float* __restrict__ LC, const float2* __restrict__ stats,
-                                                   int n, int64_t BH, float sl2e, float* __restrict__ part) {
+                                                   int n, int64_t BH, int chunks, float sl2e,
+                                                   float* __restrict__ part) {
   constexpr int Npad = NB * 32;
   // the waves' query tiles; after the loop the same bytes hold two partial
   // slots [2][2][32][64] (waves 0, 1 write, waves 2, 3 add: fixed order)
@@ -355,11 +366,11 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
   __shared__ __attribute__((aligned(16))) float2 st[4][32];  // (Lq, D) of the wave's tile queries
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, gl = lane & 31;
   const int64_t item = (int64_t)(blockIdx.x % 8) * (gridDim.x / 8) + blockIdx.x / 8;
-  if (item >= NB * kBwdChunks * BH) return;  // grid padding (whole workgroup)
-  const int b = (int)(item % NB), chunk = (int)(item / NB % kBwdChunks);
-  const int64_t bh = item / (NB * kBwdChunks);
+  if (item >= NB * chunks * BH) return;  // grid padding (whole workgroup)
+  const int b = (int)(item % NB), chunk = (int)(item / NB % chunks);
+  const int64_t bh = item / (NB * chunks);
   const int64_t ntiles = ((int64_t)n + 31) / 32;
-  const int64_t c0 = chunk * ntiles / kBwdChunks, c1 = (chunk + 1) * ntiles / kBwdChunks;
+  const int64_t c0 = chunk * ntiles / chunks, c1 = (chunk + 1) * ntiles / chunks;
   const uint16_t* Qb = Q + bh * (int64_t)n * 64;
   const uint16_t* Gb = G + bh * (int64_t)n * 64;
   const int g = 32 * b + gl;  // this lane's group (MFMA column / A-operand row)
@@ -482,7 +493,7 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
     }
     __syncthreads();
   }
-  float* out = part + ((bh * kBwdChunks + chunk) * 2) * (int64_t)Npad * 64;
+  float* out = part + ((bh * chunks + chunk) * 2) * (int64_t)Npad * 64;
   for (int x = tid; x < 2 * 32 * 64; x += 256) {
     const int k = x / (32 * 64), e = x % (32 * 64);
     const float s = red[k * 32 * 64 + e] + red[2 * 32 * 64 + k * 32 * 64 + e];  // (w0 + w2) + (w1 + w3)
@@ -547,7 +558,7 @@ size_t backward_workspace_layout(const Dims& d, BackwardWorkspace* w, void* base
   void* MU = take((size_t)d.BH * Npad * 64 * 2);
   void* LC = take((size_t)d.BH * Npad * 4);
   void* ST = take((size_t)d.BH * d.n * 8);
-  void* PART = take((size_t)d.BH * kBwdChunks * 2 * Npad * 64 * 4);
+  void* PART = take((size_t)d.BH * bwd_chunks(d.BH, Npad / 32) * 2 * Npad * 64 * 4);
   void* GK = take((size_t)d.BH * Npad * 64 * 4);
   void* GV = take((size_t)d.BH * Npad * 64 * 4);
   if (w) *w = BackwardWorkspace{(uint16_t*)R, (uint16_t*)RT, (uint16_t*)MU, (float*)LC, ST, (float*)PART,
@@ -586,12 +597,13 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
     }
 #undef GA_BWD_Q
   }
+  const int chunks = bwd_chunks(d.BH, NB);
   {
     TimedLaunch tl("bwd_group", st);
 #define GA_BWD_G(NBV)                                                                                              \
-  hipLaunchKernelGGL(k_bwd_group<NBV>, dim3((unsigned)((NBV * kBwdChunks * d.BH + 7) / 8 * 8)), dim3(256), 0, st, \
+  hipLaunchKernelGGL(k_bwd_group<NBV>, dim3((unsigned)((NBV * chunks * d.BH + 7) / 8 * 8)), dim3(256), 0, st,     \
                      (const uint16_t*)Q, (const uint16_t*)dO, w.R, w.MU, w.LC, (const float2*)w.stats, d.n, d.BH,  \
-                     sl2e, w.part)
+                     chunks, sl2e, w.part)
     switch (NB) {
       case 1: GA_BWD_G(1); break;
       case 2: GA_BWD_G(2); break;
@@ -607,7 +619,7 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
   {
     TimedLaunch tl("bwd_finish", st);
     hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 4), (unsigned)d.BH), dim3(256), 0, st, w.part, count, d.N,
-                       Npad, kBwdChunks, scale, (uint16_t*)w.gk, (uint16_t*)w.gv);
+                       Npad, chunks, scale, (uint16_t*)w.gk, (uint16_t*)w.gv);
   }
   TimedLaunch tl("bwd_keys", st);
   hipLaunchKernelGGL(k_bwd_keys, dim3((unsigned)((d.n + 31) / 32), (unsigned)d.BH), dim3(256), 0, st, belong,
