@@ -577,7 +577,9 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
                        Npad, rts, w.R, w.RT, w.MU, w.LC);
   }
   const int64_t ntiles = ((int64_t)d.n + 31) / 32;
-  const int tpw = (int)((ntiles + 31) / 32);  // about 8 workgroups per slice
+  // about one round of kBwdTargetWgs workgroups: the same number per slice
+  const int64_t per_slice = (kBwdTargetWgs + d.BH - 1) / d.BH;
+  const int tpw = (int)((ntiles + 4 * per_slice - 1) / (4 * per_slice));
   const unsigned gq = (unsigned)((ntiles + 4 * tpw - 1) / (4 * tpw));
   {
     TimedLaunch tl("bwd_query", st);

@@ -201,8 +201,12 @@ hipError_t launch_merge_plan(const Dims& d, const void* Q, const void* K, const 
     hipLaunchKernelGGL(k_merge_zero, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, rad2g, qmax2g, d.BH,
                        d.N);
   }
-  // about 1000 keys per workgroup, at most 16 workgroups per slice
-  const int parts = d.n < 1000 ? 1 : (d.n / 1000 > 16 ? 16 : d.n / 1000);
+  // at least about 1000 keys per workgroup, at most 16 workgroups per slice,
+  // and no more than one round of about 512 workgroups (two per CU) in all:
+  // every workgroup stages the slice's centroids
+  const int64_t round_parts = (512 + d.BH - 1) / d.BH;
+  int parts = d.n < 1000 ? 1 : (d.n / 1000 > 16 ? 16 : d.n / 1000);
+  if (parts > round_parts) parts = (int)round_parts;
   {
     TimedLaunch tl("merge_norms", st);
     if (d.dtype == 1)
