@@ -104,16 +104,29 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const float* __restrict__ cent
   __shared__ uint16_t tt[64][32 + 2];
   const int64_t bh = blockIdx.y;
   const int g0 = 32 * blockIdx.x;
-  for (int x = threadIdx.x; x < 32 * 64; x += 256) {
-    const int g = g0 + (x >> 6), c = x & 63;
-    const int cnt = g < N ? count[bh * N + g] : 0;
-    const float cv = g < N ? centroid[(bh * N + g) * 64 + c] : 0.f;
-    const float mv = cnt > 0 ? vsum[(bh * N + g) * 64 + c] / (float)cnt : 0.f;
-    const uint16_t rb = (uint16_t)bf16_bits(cv);
+  // element x = threadIdx.x + 256 i: group g0 + x / 64, feature x % 64; every
+  // load (rows clamped into the slice) is issued before any result is formed
+  int cnt[8];
+  float cv[8], sv[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int x = threadIdx.x + 256 * i, g = g0 + (x >> 6), c = x & 63;
+    const int64_t row = bh * N + min(g, N - 1);
+    cnt[i] = count[row];
+    cv[i] = centroid[row * 64 + c];
+    sv[i] = vsum[row * 64 + c];
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int x = threadIdx.x + 256 * i, g = g0 + (x >> 6), c = x & 63;
+    const bool in = g < N;
+    const int k = in ? cnt[i] : 0;
+    const float mv = k > 0 ? sv[i] / (float)k : 0.f;
+    const uint16_t rb = (uint16_t)bf16_bits(in ? cv[i] : 0.f);
     R[(bh * Npad + g) * 64 + c] = rb;
     tt[c][x >> 6] = rb;
     MU[(bh * Npad + g) * 64 + c] = (uint16_t)bf16_bits(mv);
-    if (c == 0) LC[bh * Npad + g] = cnt > 0 ? log2f((float)cnt) : -INFINITY;
+    if (c == 0) LC[bh * Npad + g] = k > 0 ? log2f((float)k) : -INFINITY;
   }
   __syncthreads();
   for (int x = threadIdx.x; x < 64 * 16; x += 256) {
