@@ -43,6 +43,22 @@ constexpr int kCs = 65;  // LDS row stride (floats) of the centroids
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// The slice's N x 64 fp32 centroids to LDS (row stride kCs), eight loads per
+// thread issued (index clamped) before any of them is stored.
+__device__ __forceinline__ void stage_centroids(const float* __restrict__ cen, int N, float* cs) {
+  const int tid = threadIdx.x, total = N * 64;
+  for (int base = 0; base < total; base += 8 * kMergeThreads) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = cen[min(base + tid + u * kMergeThreads, total - 1)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int x = base + tid + u * kMergeThreads;
+      if (x < total) cs[(x >> 6) * kCs + (x & 63)] = v[u];
+    }
+  }
+}
+
 // Raw rows (loaded as 16-byte vectors) and their exact fp64 elements.
 struct F32In {
   typedef float T;
@@ -83,7 +99,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge_norms(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bh = blockIdx.y;
   const int i0 = (int)((int64_t)blockIdx.x * n / gridDim.x), i1 = (int)((int64_t)(blockIdx.x + 1) * n / gridDim.x);
-  for (int x = tid; x < N * 64; x += kMergeThreads) cs[(x >> 6) * kCs + (x & 63)] = centroid[bh * N * 64 + x];
+  stage_centroids(centroid + bh * N * 64, N, cs);
   for (int g = tid; g < N; g += kMergeThreads) rad2[g] = 0ull;  // bits of +0.0
   __syncthreads();
   double qmax2 = 0.0;
@@ -148,7 +164,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge_pairs(
   __shared__ int nmarked;
   const int tid = threadIdx.x;
   const int64_t bh = blockIdx.x;
-  for (int x = tid; x < N * 64; x += kMergeThreads) cs[(x >> 6) * kCs + (x & 63)] = centroid[bh * N * 64 + x];
+  stage_centroids(centroid + bh * N * 64, N, cs);
   for (int g = tid; g < N; g += kMergeThreads) {
     rad[g] = __builtin_sqrt(radius[bh * N + g]);  // radius holds the squared maximum here
     cnt[g] = count[bh * N + g];
