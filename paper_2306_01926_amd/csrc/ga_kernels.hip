@@ -720,24 +720,6 @@ __device__ __forceinline__ void gsum_load(const uint32_t* ent, const uint16_t* _
   }
 }
 
-// x summed over the 8 lanes l ^ {0, 8, 16, ..., 56} (lane bits 3, 4, 5), in
-// every lane: DPP row rotation by 8 (lane ^ 8 within 16-lane rows), then the
-// 16- and 32-lane half swaps.
-__device__ __forceinline__ double sum_slots8(double x) {
-  const uint32_t lo = (uint32_t)__double2loint(x), hi = (uint32_t)__double2hiint(x);
-  x += __hiloint2double((int)__builtin_amdgcn_update_dpp(0u, hi, 0x128, 0xf, 0xf, false),
-                        (int)__builtin_amdgcn_update_dpp(0u, lo, 0x128, 0xf, 0xf, false));
-  {
-    const auto l16 = __builtin_amdgcn_permlane16_swap((uint32_t)__double2loint(x), (uint32_t)__double2loint(x), false,
-                                                      false);
-    const auto h16 = __builtin_amdgcn_permlane16_swap((uint32_t)__double2hiint(x), (uint32_t)__double2hiint(x), false,
-                                                      false);
-    x = __hiloint2double((int)h16[0], (int)l16[0]) + __hiloint2double((int)h16[1], (int)l16[1]);
-  }
-  const u32x2 l32 = halves((uint32_t)__double2loint(x)), h32 = halves((uint32_t)__double2hiint(x));
-  return __hiloint2double((int)h32[0], (int)l32[0]) + __hiloint2double((int)h32[1], (int)l32[1]);
-}
-
 // ------------------------------------------------------------------ partition sums (bf16, N <= 128)
 // The member sums of the bf16 path are exact in fp64 (see above), so they may
 // be split into per-workgroup partitions and added in any order.  In the first
