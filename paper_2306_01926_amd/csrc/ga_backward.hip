@@ -367,7 +367,9 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
                                                    const uint16_t* __restrict__ R, const uint16_t* __restrict__ MU,
                                                    const float* __restrict__ LC, const float2* __restrict__ stats,
                                                    int n, int64_t BH, int chunks, float sl2e,
-                                                   float* __restrict__ part) {
+                                                   float* __restrict__ part, const int32_t* __restrict__ count,
+                                                   int N, float scale, uint16_t* __restrict__ gk,
+                                                   uint16_t* __restrict__ gv) {
   constexpr int Npad = NB * 32;
   // the waves' query tiles; after the loop the same bytes hold two partial
   // slots [2][2][32][64] (waves 0, 1 write, waves 2, 3 add: fixed order)
@@ -506,6 +508,20 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
     }
     __syncthreads();
   }
+  if (chunks == 1) {
+    // the only chunk: the rows k_bwd_finish would form from it (the same
+    // operations: its sum over one partial is 0 + s = s)
+    for (int e = tid; e < 32 * 64; e += 256) {
+      const int g = 32 * b + (e >> 6);
+      if (g >= N) continue;
+      const float sr = 0.f + (red[e] + red[2 * 32 * 64 + e]);
+      const float sm = 0.f + (red[32 * 64 + e] + red[3 * 32 * 64 + e]);
+      const int cnt = count[bh * N + g];
+      gk[(bh * Npad + g) * 64 + (e & 63)] = (uint16_t)bf16_bits(cnt > 0 ? scale * sr / (float)cnt : 0.f);
+      gv[(bh * Npad + g) * 64 + (e & 63)] = (uint16_t)bf16_bits(cnt > 0 ? sm / (float)cnt : 0.f);
+    }
+    return;
+  }
   float* out = part + ((bh * chunks + chunk) * 2) * (int64_t)Npad * 64;
   for (int x = tid; x < 2 * 32 * 64; x += 256) {
     const int k = x / (32 * 64), e = x % (32 * 64);
@@ -618,7 +634,7 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
 #define GA_BWD_G(NBV)                                                                                              \
   hipLaunchKernelGGL(k_bwd_group<NBV>, dim3((unsigned)((NBV * chunks * d.BH + 7) / 8 * 8)), dim3(256), 0, st,     \
                      (const uint16_t*)Q, (const uint16_t*)dO, w.R, w.MU, w.LC, (const float2*)w.stats, d.n, d.BH,  \
-                     chunks, sl2e, w.part)
+                     chunks, sl2e, w.part, count, d.N, scale, (uint16_t*)w.gk, (uint16_t*)w.gv)
     switch (NB) {
       case 1: GA_BWD_G(1); break;
       case 2: GA_BWD_G(2); break;
@@ -631,7 +647,7 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
     }
 #undef GA_BWD_G
   }
-  {
+  if (chunks > 1) {  // (one chunk: k_bwd_group wrote the rows itself)
     TimedLaunch tl("bwd_finish", st);
     hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 4), (unsigned)d.BH), dim3(256), 0, st, w.part, count, d.N,
                        Npad, chunks, scale, (uint16_t*)w.gk, (uint16_t*)w.gv);

@@ -133,6 +133,22 @@ def test_backward_slice_with_every_group_empty(oracle_mod, dev, N):
         assert torch.count_nonzero(X[0, 1]) == 0
 
 
+def test_backward_one_query_chunk_per_slice(oracle_mod, dev):
+    """128 slices x 4 group blocks fill the GPU with one query chunk per slice,
+    so the group kernel forms the dK / dV rows itself (no separate finish)."""
+    B, H, n, N = 16, 8, 300, 128
+    say(f"backward, one query chunk per slice (B={B}, H={H}, n={n}, N={N})")
+    Q, K, V = inputs.make_qkv(B, H, n, 64, "bf16", 31, 64, 0.05, 0.3)
+    rng = np.random.default_rng(32)
+    dO = inputs.to_storage(rng.standard_normal((B, H, n, 64)).astype(np.float32), "bf16")
+    cl = oracle_mod.cluster(f64(K), N, 2, "bf16")
+    vsum, _ = oracle_mod.aggregate(f64(V), cl["belong"], N)
+    a = run_both(oracle_mod, dev, Q, dO, cl["belong"], cl["count"], cl["centroid"], vsum, N)
+    b = run_both(oracle_mod, dev, Q, dO, cl["belong"], cl["count"], cl["centroid"], vsum, N)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
 def test_full_size_slices(oracle_mod, dev):
     w = inputs.WORKLOADS["n8000_N128_bf16"]
     say(f"backward on 2 full-size slices of {w.name}")
