@@ -135,8 +135,9 @@ def test_backward_slice_with_every_group_empty(oracle_mod, dev, N):
 
 def test_backward_one_query_chunk_per_slice(oracle_mod, dev):
     """128 slices x 4 group blocks fill the GPU with one query chunk per slice,
-    so the group kernel forms the dK / dV rows itself (no separate finish)."""
-    B, H, n, N = 16, 8, 300, 128
+    so the group kernel forms the dK / dV rows itself (no separate finish);
+    n = 2000 also gives the query kernel's waves several tiles each."""
+    B, H, n, N = 16, 8, 2000, 128
     say(f"backward, one query chunk per slice (B={B}, H={H}, n={n}, N={N})")
     Q, K, V = inputs.make_qkv(B, H, n, 64, "bf16", 31, 64, 0.05, 0.3)
     rng = np.random.default_rng(32)
