@@ -104,6 +104,40 @@ def _p(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _expect(t, name: str, device, dtype, shape=None, optional: bool = False):
+    """Check a tensor handed to the C ABI, which cannot check buffer sizes:
+    it must live on `device` (a CUDA device), have `dtype`, be contiguous and
+    (if given) have exactly `shape`.  Raises ValueError otherwise, before any
+    pointer reaches a kernel."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda" or t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _device_of(X: torch.Tensor):
+    if X.device.type != "cuda":
+        raise ValueError(f"tensors must be on a CUDA device (got {X.device})")
+    return X.device
+
+
+def _qkv_like(X: torch.Tensor, name: str):
+    """Shape [B, H, n, d] and the device of the first operand of a call."""
+    if not isinstance(X, torch.Tensor) or X.dim() != 4:
+        raise ValueError(f"{name} must be a [B, H, n, d] tensor")
+    return _device_of(X)
+
+
 def _check(rc: int):
     if rc != 0:
         raise GAError(rc, lib().ga_last_error().decode())
@@ -120,18 +154,23 @@ def workspace_bytes(shape: Shape, N: int) -> int:
     return int(lib().ga_workspace_bytes(shape, int(N)))
 
 
-def workspace(shape: Shape, N: int, device) -> tuple:
+def workspace(shape: Shape, N: int, device, stream=None) -> tuple:
     """A cached device workspace (uint8 tensor) large enough for (shape, N).
 
-    One buffer per device, shared by every call that does not pass ws: calls
-    that may overlap (on different streams) must each pass a workspace of
-    their own (torch.empty(workspace_bytes(shape, N), dtype=torch.uint8)).
+    One buffer per (device, stream): the workspace carries state between the
+    launches of one call, and calls on one stream run one after another, so
+    calls without ws on different streams never share a buffer.  The buffer
+    is allocated on (and its memory ordered by) that stream.
     """
+    device = torch.device(device)
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
     nbytes = max(workspace_bytes(shape, N), 256)
-    key = torch.device(device)
+    key = (device, stream.cuda_stream)
     ws = _ws_cache.get(key)
     if ws is None or ws.numel() < nbytes:
-        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        with torch.cuda.stream(stream):
+            ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
         _ws_cache[key] = ws
     return ws, ws.numel()
 
@@ -140,6 +179,7 @@ def _ws_args(shape, N, device, ws):
     if ws is None:
         ws, nb = workspace(shape, N, device)
     else:
+        _expect(ws, "ws", device, torch.uint8)
         nb = ws.numel() * ws.element_size()
     return _p(ws), nb
 
@@ -147,8 +187,10 @@ def _ws_args(shape, N, device, ws):
 def cluster(K: torch.Tensor, N: int, iters: int, init: torch.Tensor | None = None, ws=None):
     """Grouping of the keys: returns (belong [B,H,n] int32, count [B,H,N] int32,
     centroid [B,H,N,d] fp32)."""
+    dev = _qkv_like(K, "K")
     s = shape_of(K)
-    dev = K.device
+    B, H, n, d = K.shape
+    _expect(init, "init", dev, torch.float32, (B, H, N, d), optional=True)
     belong = torch.empty(K.shape[:3], dtype=torch.int32, device=dev)
     count = torch.empty((*K.shape[:2], N), dtype=torch.int32, device=dev)
     centroid = torch.empty((*K.shape[:2], N, K.shape[3]), dtype=torch.float32, device=dev)
@@ -160,8 +202,9 @@ def cluster(K: torch.Tensor, N: int, iters: int, init: torch.Tensor | None = Non
 
 def aggregate(V: torch.Tensor, belong: torch.Tensor, N: int, ws=None) -> torch.Tensor:
     """Per-group fp32 sums of the values (fp64 accumulation)."""
+    dev = _qkv_like(V, "V")
     s = shape_of(V)
-    dev = V.device
+    _expect(belong, "belong", dev, torch.int32, V.shape[:3])
     vsum = torch.empty((*V.shape[:2], N, V.shape[3]), dtype=torch.float32, device=dev)
     wp, nb = _ws_args(s, N, dev, ws)
     _check(lib().ga_aggregate(s, _p(V), _p(belong), int(N), _p(vsum), wp, nb, _stream(dev)))
@@ -171,8 +214,12 @@ def aggregate(V: torch.Tensor, belong: torch.Tensor, N: int, ws=None) -> torch.T
 def attend(Q: torch.Tensor, centroid: torch.Tensor, count: torch.Tensor, vsum: torch.Tensor, N: int,
            scale: float | None = None, ws=None) -> torch.Tensor:
     """Group softmax and combine; returns O [B,H,n,d] in Q's dtype."""
+    dev = _qkv_like(Q, "Q")
     s = shape_of(Q)
-    dev = Q.device
+    B, H, n, d = Q.shape
+    _expect(centroid, "centroid", dev, torch.float32, (B, H, N, d))
+    _expect(count, "count", dev, torch.int32, (B, H, N))
+    _expect(vsum, "vsum", dev, torch.float32, (B, H, N, d))
     scale = 1.0 / math.sqrt(Q.shape[3]) if scale is None else float(scale)
     O = torch.empty_like(Q)
     wp, nb = _ws_args(s, N, dev, ws)
@@ -185,8 +232,10 @@ def forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, N: int, iters: in
             scale: float | None = None, return_groups: bool = False, out: torch.Tensor | None = None,
             ws=None):
     """Whole group-attention forward; optionally also (belong, count, centroid)."""
+    dev = _qkv_like(Q, "Q")
     s = shape_of(Q)
-    dev = Q.device
+    for t, nm in ((K, "K"), (V, "V"), (out, "out")):
+        _expect(t, nm, dev, Q.dtype, Q.shape, optional=nm == "out")
     scale = 1.0 / math.sqrt(Q.shape[3]) if scale is None else float(scale)
     O = torch.empty_like(Q) if out is None else out
     belong = count = centroid = None
@@ -210,7 +259,9 @@ def block_shape(X: torch.Tensor, H: int) -> Shape:
 def project_qkv(X: torch.Tensor, Wqkv: torch.Tensor, H: int):
     """(Q, K, V) [B, H, n, 64] = per-head slices of X Wqkv^T (Wqkv [3D, D], rows = outputs)."""
     s = block_shape(X, H)
-    B, n, _ = X.shape
+    dev = _device_of(X)
+    B, n, D = X.shape
+    _expect(Wqkv, "Wqkv", dev, X.dtype, (3 * D, D))
     Q, K, V = (torch.empty((B, H, n, 64), dtype=X.dtype, device=X.device) for _ in range(3))
     _check(lib().ga_project_qkv(s, _p(X), _p(Wqkv), _p(Q), _p(K), _p(V), _stream(X.device)))
     return Q, K, V
@@ -218,7 +269,9 @@ def project_qkv(X: torch.Tensor, Wqkv: torch.Tensor, H: int):
 
 def project_out(O: torch.Tensor, Wo: torch.Tensor) -> torch.Tensor:
     """Y [B, n, D] = heads of O [B, H, n, 64] concatenated, times Wo^T (Wo [D, D])."""
+    dev = _qkv_like(O, "O")
     B, H, n, d = O.shape
+    _expect(Wo, "Wo", dev, O.dtype, (H * d, H * d))
     Y = torch.empty((B, n, H * d), dtype=O.dtype, device=O.device)
     _check(lib().ga_project_out(Shape(B, H, n, d, _dtype_code(O)), _p(O), _p(Wo), _p(Y), _stream(O.device)))
     return Y
@@ -233,12 +286,18 @@ def attention_block(X: torch.Tensor, Wqkv: torch.Tensor, Wo: torch.Tensor, H: in
     """Attention block: projections, group-attention forward, output projection.
     ws: a uint8 device tensor of block_workspace_bytes(shape, N) (allocated if None)."""
     s = block_shape(X, H)
+    dev = _device_of(X)
+    D = X.shape[2]
+    _expect(Wqkv, "Wqkv", dev, X.dtype, (3 * D, D))
+    _expect(Wo, "Wo", dev, X.dtype, (D, D))
+    _expect(out, "out", dev, X.dtype, X.shape, optional=True)
     scale = 1.0 / 8.0 if scale is None else float(scale)
     Y = torch.empty_like(X) if out is None else out
     if ws is None:
         ws = torch.empty(max(block_workspace_bytes(s, N), 256), dtype=torch.uint8, device=X.device)
+    _expect(ws, "ws", dev, torch.uint8)
     _check(lib().ga_attention_block(s, _p(X), _p(Wqkv), _p(Wo), int(N), int(iters), scale, _p(Y), _p(ws),
-                                    ws.numel(), _stream(X.device)))
+                                    ws.numel(), _stream(dev)))
     return Y
 
 
@@ -246,9 +305,13 @@ def merge_plan(Q: torch.Tensor, K: torch.Tensor, belong: torch.Tensor, centroid:
                count: torch.Tensor, N: int, scale: float | None = None, eps: float = 2.0) -> dict:
     """Merge plan of the adaptive group count (Lemma 1 threshold, Eq. 5 rule):
     dict(radius [B,H,N] fp64, dthr [B,H] fp64, partner [B,H,N] int32, merges [B,H] int32)."""
+    dev = _qkv_like(K, "K")
     s = shape_of(K)
-    dev = K.device
-    B, H = K.shape[:2]
+    B, H, n, d = K.shape
+    _expect(Q, "Q", dev, K.dtype, K.shape)
+    _expect(belong, "belong", dev, torch.int32, (B, H, n))
+    _expect(centroid, "centroid", dev, torch.float32, (B, H, N, d))
+    _expect(count, "count", dev, torch.int32, (B, H, N))
     scale = 1.0 / math.sqrt(K.shape[3]) if scale is None else float(scale)
     radius = torch.empty((B, H, N), dtype=torch.float64, device=dev)
     dthr = torch.empty((B, H), dtype=torch.float64, device=dev)
@@ -276,12 +339,19 @@ def backward_workspace_bytes(shape: Shape, N: int) -> int:
 def backward(Q: torch.Tensor, dO: torch.Tensor, belong: torch.Tensor, centroid: torch.Tensor, count: torch.Tensor,
              vsum: torch.Tensor, N: int, scale: float | None = None, ws=None):
     """Gradient of the forward with the grouping fixed: (dQ, dK, dV) [B,H,n,d] bf16."""
+    dev = _qkv_like(Q, "Q")
     s = shape_of(Q)
-    dev = Q.device
+    B, H, n, d = Q.shape
+    _expect(dO, "dO", dev, Q.dtype, Q.shape)
+    _expect(belong, "belong", dev, torch.int32, (B, H, n))
+    _expect(centroid, "centroid", dev, torch.float32, (B, H, N, d))
+    _expect(count, "count", dev, torch.int32, (B, H, N))
+    _expect(vsum, "vsum", dev, torch.float32, (B, H, N, d))
     scale = 1.0 / math.sqrt(Q.shape[3]) if scale is None else float(scale)
     dQ, dK, dV = (torch.empty_like(Q) for _ in range(3))
     if ws is None:
         ws = torch.empty(max(backward_workspace_bytes(s, N), 256), dtype=torch.uint8, device=dev)
+    _expect(ws, "ws", dev, torch.uint8)
     _check(lib().ga_backward(s, _p(Q), _p(dO), _p(belong), _p(centroid), _p(count), _p(vsum), int(N), scale, _p(dQ),
                              _p(dK), _p(dV), _p(ws), ws.numel(), _stream(dev)))
     return dQ, dK, dV

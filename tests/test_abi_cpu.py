@@ -191,3 +191,52 @@ def test_backward_validates():
     assert bw(ws=0) == 3
     assert bw(nbytes=nb - 1) == 3
     assert bw(s=shape(B=0)) == 0
+
+
+# ---------------------------------------------------------------- binding checks
+# ga.py refuses tensors the C ABI could not check (a host pointer, a wrong
+# dtype or a short buffer would reach a kernel) before any library call.
+
+def _cpu(shape, dtype=None):
+    import torch
+
+    return torch.zeros(shape, dtype=dtype or torch.bfloat16)
+
+
+@pytest.mark.parametrize("call", ["forward", "cluster", "aggregate", "attend", "backward", "merge_plan",
+                                  "project_qkv", "project_out", "attention_block"])
+def test_binding_rejects_host_tensors(call):
+    import torch
+
+    B, H, n, N = 1, 2, 40, 4
+    X = _cpu((B, H, n, 64))
+    i32, f32 = torch.int32, torch.float32
+    calls = {
+        "forward": lambda: ga.forward(X, X, X, N, 2),
+        "cluster": lambda: ga.cluster(X, N, 2),
+        "aggregate": lambda: ga.aggregate(X, _cpu((B, H, n), i32), N),
+        "attend": lambda: ga.attend(X, _cpu((B, H, N, 64), f32), _cpu((B, H, N), i32), _cpu((B, H, N, 64), f32), N),
+        "backward": lambda: ga.backward(X, X, _cpu((B, H, n), i32), _cpu((B, H, N, 64), f32), _cpu((B, H, N), i32),
+                                        _cpu((B, H, N, 64), f32), N),
+        "merge_plan": lambda: ga.merge_plan(X, X, _cpu((B, H, n), i32), _cpu((B, H, N, 64), f32),
+                                            _cpu((B, H, N), i32), N),
+        "project_qkv": lambda: ga.project_qkv(_cpu((B, n, 128)), _cpu((384, 128)), 2),
+        "project_out": lambda: ga.project_out(X, _cpu((128, 128))),
+        "attention_block": lambda: ga.attention_block(_cpu((B, n, 128)), _cpu((384, 128)), _cpu((128, 128)), 2, N, 2),
+    }
+    with pytest.raises(ValueError, match="CUDA|cuda"):
+        calls[call]()
+
+
+def test_expect_checks_dtype_shape_and_device():
+    import torch
+
+    cpu = torch.device("cpu")
+    t = torch.zeros((2, 3), dtype=torch.int32)
+    with pytest.raises(ValueError, match="on cpu"):
+        ga._expect(t, "x", cpu, torch.int32, (2, 3))  # not a CUDA tensor
+    with pytest.raises(ValueError, match="required"):
+        ga._expect(None, "x", cpu, torch.int32)
+    ga._expect(None, "x", cpu, torch.int32, optional=True)
+    with pytest.raises(ValueError, match="\\[B, H, n, d\\]"):
+        ga.forward(torch.zeros((2, 3)), None, None, 2, 1)
