@@ -34,9 +34,19 @@
  *     the bf16 attention (ga_attend, ga_forward) holds N <= 256 groups on
  *     chip (GA_ERR_UNSUPPORTED above).  B*H <= 65535.  B = 0 or H = 0 is an
  *     empty batch: GA_OK, nothing enqueued.  n must be >= 1.
- *   - Inputs must be finite with |x| < 2^60 (not checked; results undefined
- *     otherwise).
- *   - Determinism: repeated calls with the same inputs give identical bits.
+ *   - Inputs must be finite, and every nonzero input of magnitude within
+ *     [2^-60, 2^60] (not checked; results undefined otherwise).
+ *   - Exactness and determinism (bf16): the fp64 member sums behind COUNT
+ *     and the centroids are exact, hence independent of the order in which
+ *     the GPU adds them, as long as within every group (e_max - e_min) +
+ *     log2(count) <= 45, with e_max / e_min the largest / smallest binary
+ *     exponent of the group's nonzero member values (for instance at most
+ *     2^15 members whose nonzero magnitudes lie within 2^30 of each other).
+ *     Under that condition belong, count and centroid equal the definition
+ *     below bit for bit and repeated calls give identical bits; outside it a
+ *     centroid can differ in its last bit (and a later assignment with it).
+ *     This condition is not checked on the device.  fp32 sums are formed in
+ *     a fixed order and are deterministic without it.
  *
  * Representatives: R = round_dt(centroid), where round_dt is the identity for
  * GA_F32 and round-to-nearest-even to bfloat16 for GA_BF16.  R is used both
@@ -237,6 +247,17 @@ typedef struct {
 
 int ga_timing_enable(int on);
 int ga_timing_collect(ga_kernel_time_t *out, int32_t max_entries, int32_t *n_entries);
+
+/*
+ * Device status of the last grouping launch that used `workspace` (shape s, N
+ * groups): waits for `stream` (this is the library's only synchronising call)
+ * and returns GA_OK, or GA_ERR_HIP if a cross-workgroup wait of the
+ * persistent grouping kernel gave up (its workgroups were not all resident at
+ * once, e.g. because other work occupied the GPU; the outputs of that call
+ * are then invalid).  Callers that cannot rule that out check after a
+ * forward or cluster call.
+ */
+int ga_workspace_check(ga_shape_t s, int32_t N, const void *workspace, size_t workspace_bytes, void *stream);
 
 /* Static description of a status code. */
 const char *ga_status_string(int status);

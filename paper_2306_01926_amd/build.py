@@ -9,6 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libga.so")
 SOURCES = [os.path.join(HERE, "csrc", "ga_abi.cpp"), os.path.join(HERE, "csrc", "ga_kernels.hip"),
+           os.path.join(HERE, "csrc", "ga_lloyd.hip"),
            os.path.join(HERE, "csrc", "ga_block.hip"),
            os.path.join(HERE, "csrc", "ga_merge.hip"),
            os.path.join(HERE, "csrc", "ga_backward.hip")]

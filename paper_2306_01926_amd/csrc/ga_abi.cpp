@@ -7,6 +7,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <string>
@@ -89,8 +90,22 @@ ga::Dims dims_of(const ga_shape_t& s, int32_t N) {
 // round's assign launch writes per-workgroup partition sums and a small launch
 // adds them.  fp32: every round re-sums the members in ascending key order
 // (fp32 sums need not be exact).
+// The persistent grouping kernel (every round in one launch) serves bf16
+// shapes it supports; GA_GROUPING=rounds in the environment selects the
+// launch-per-round path instead (for comparisons).
+bool use_persistent(const ga::Dims& d) {
+  const char* e = getenv("GA_GROUPING");
+  if (e && strcmp(e, "rounds") == 0) return false;
+  return d.dtype == GA_BF16 && ga::lloyd_usable(d);
+}
+
 int run_cluster(const ga::Dims& d, const void* K, int32_t iters, const float* init, int32_t* belong,
                 int32_t* count, float* C, const ga::Workspace& w, hipStream_t st) {
+  if (use_persistent(d)) {
+    GA_LAUNCH(ga::launch_lloyd(d, K, nullptr, init, iters, belong, count, C, w, nullptr, nullptr, nullptr, 1.0f, st),
+              "grouping launch");
+    return GA_OK;
+  }
   // with the fused first round the assign launch forms the initial centroids itself
   if (ga::fused_first_parts(d) == 0)
     GA_LAUNCH(ga::launch_init(d, K, init, C, w.R, w.nrm64, w.nsplit, w.mcount, st), "init launch");
@@ -133,6 +148,13 @@ int run_forward(const ga::Dims& d, const void* Q, const void* K, const void* V, 
   int32_t* a = belong ? belong : w.belong;
   int32_t* cnt = count ? count : w.count;
   float* C = centroid ? centroid : w.C;
+  if (use_persistent(d)) {
+    // grouping, update and value sums (straight into the attention's inputs) in one launch
+    GA_LAUNCH(ga::launch_lloyd(d, K, V, nullptr, iters, a, cnt, C, w, nullptr, w.Vt, w.ginit, scale, st),
+              "grouping launch");
+    GA_LAUNCH(ga::launch_attend(d, Q, w.R, w.Vt, w.ginit, C, cnt, w.vsum, scale, O, st), "attention launch");
+    return GA_OK;
+  }
   GA_TRY(run_cluster(d, K, iters, nullptr, a, cnt, C, w, st));
   if (d.dtype == GA_BF16) {
     // the value sums go straight into the attention's transposed means and bias
@@ -264,6 +286,23 @@ size_t ga_workspace_bytes(ga_shape_t s, int32_t N) {
     return 0;
   }
   return ga::workspace_layout(dims_of(s, N), nullptr, nullptr);
+}
+
+int ga_workspace_check(ga_shape_t s, int32_t N, const void* workspace, size_t workspace_bytes, void* stream) {
+  bool empty;
+  GA_TRY(check_shape(s, N, &empty));
+  if (empty) return GA_OK;
+  const ga::Dims d = dims_of(s, N);
+  ga::Workspace w;
+  GA_TRY(check_ws(d, (void*)workspace, workspace_bytes, &w));
+  GA_LAUNCH(hipStreamSynchronize((hipStream_t)stream), "stream synchronisation");
+  uint32_t status = 0;
+  GA_LAUNCH(hipMemcpy(&status, w.lstatus, sizeof status, hipMemcpyDeviceToHost), "status read");
+  // a workspace that no persistent grouping launch used holds no status
+  if ((status & 0xffff0000u) == ga::kLloydMark && (status & 1u))
+    return fail(GA_ERR_HIP, "a cross-workgroup wait of the grouping launch gave up (status 0x%x): its outputs are invalid",
+                status);
+  return GA_OK;
 }
 
 int ga_cluster(ga_shape_t s, const void* K, int32_t N, int32_t iters, const float* init, int32_t* belong,

@@ -32,6 +32,10 @@ struct Workspace {
   double* Sp;        // [BH][kFusedP][N][64] per-partition fp64 sums of the fused update
   int32_t* cntp;     // [BH][kFusedP][N] per-partition member counts
   uint32_t* pbits;   // [BH][kFusedP][4] groups with members in each partition (bit g)
+  uint32_t* lrec;    // persistent grouping (ga_lloyd.hip): moved-key records, lloyd_records(d) words
+  int32_t* lrcnt;    // [BH][16] records per rank
+  uint32_t* lsync;   // [BH][32] barrier counters
+  uint32_t* lstatus; // [64] status word (bit 0: a barrier gave up)
 };
 
 // First round of the bf16 path for N <= kFusedG: every assign workgroup (one
@@ -108,6 +112,20 @@ hipError_t launch_attend_prep(const Dims& d, const float* centroid, const int32_
 hipError_t launch_attend(const Dims& d, const void* Q, const void* R, const uint16_t* Vt,
                          const float* ginit, const float* centroid, const int32_t* count,
                          const float* vsum, float scale, void* O, hipStream_t st);
+
+// Persistent grouping (ga_lloyd.hip): every Lloyd round, the update and (if V
+// is given) the value sums in one launch, for bf16, N <= 128 and shapes whose
+// workgroups (P per slice) are all resident at once.  Writes belong, count, C,
+// the final R / nsplit / nrm64 in w, and vsum and/or Vt + ginit if given.
+size_t lloyd_records(const Dims& d);  // words of w.lrec
+// w.lstatus after a persistent grouping launch: kLloydMark, | 1 if a
+// cross-workgroup wait gave up
+constexpr uint32_t kLloydMark = 0x600d0000u;
+bool lloyd_usable(const Dims& d);
+int lloyd_ranks(const Dims& d);       // workgroups per slice, 0 if not usable
+hipError_t launch_lloyd(const Dims& d, const void* K, const void* V, const float* init, int iters, int32_t* belong,
+                        int32_t* count, float* C, const Workspace& w, float* vsum, uint16_t* Vt, float* ginit,
+                        float scale, hipStream_t st);
 
 // Projections of the attention block (ga_block.hip), bf16 with fp32
 // accumulation.  mode 0: X [B][n][64H] x Wqkv[192H][64H]^T -> out0/1/2 = Q, K, V

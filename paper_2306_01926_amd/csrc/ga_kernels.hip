@@ -1995,6 +1995,10 @@ size_t workspace_layout(const Dims& d, Workspace* ws, void* base) {
   w.Sp = (double*)take(BH * fp * N * 64 * 8);
   w.cntp = (int32_t*)take(BH * fp * N * 4);
   w.pbits = (uint32_t*)take(BH * fp * 4 * 4);
+  w.lrec = (uint32_t*)take(lloyd_records(d) * 4);
+  w.lrcnt = (int32_t*)take(BH * 16 * 4);
+  w.lsync = (uint32_t*)take(BH * 32 * 4);
+  w.lstatus = (uint32_t*)take(64 * 4);
   if (ws) *ws = w;
   return off;
 }

@@ -1,0 +1,926 @@
+// gfx950 (MI355X): every Lloyd round of the key grouping (Section 4.4) and
+// the embedding aggregation of Algorithm 1 in one launch (bf16, N <= 128).
+//
+// Slice bh is handled by P workgroups of 8 waves (rank r = 0 .. P-1).  Rank r
+// owns the keys [r kpw, (r + 1) kpw) and the groups g = r, r + P, r + 2P, ...
+// Each round (Section 4.4: assign every key to its nearest representative,
+// then move every representative to the mean of its members):
+//
+//   1. assign: every rank scores its keys against all representatives (MFMA
+//      32x32x16 bf16, packed top-2, certified argmin with the exact fp64
+//      fallback; the same decision procedure as k_assign_reg) and writes one
+//      4-byte record (key, old group, new group) per key whose group changed;
+//   2. barrier A over the slice's P ranks;
+//   3. update: every rank reads all the slice's records, keeps the (key,
+//      side) entries of its own groups, sorts them by group in LDS and adds
+//      the key rows (joins +, leaves -) into its exact fp64 member sums, which
+//      stay in LDS for the whole launch; then C = (float)(S / count) (an
+//      empty group keeps C), R = bf16(C), the canonical |r|^2 and its split,
+//      published for the slice;
+//   4. barrier B; every rank reads the slice's new representatives.
+//
+// The member sums of bf16 keys are exact in fp64 (while (e_max - e_min) +
+// log2 count <= 45, see ga_kernels.hip), so the order in which the ranks, the
+// records and the LDS atomics add them cannot change a bit: groups, counts
+// and centroids are those of the oracle.  In the first round every key is a
+// join (old group "none"), which forms the full sums.  After the last round's
+// update the ranks sum the value rows of their groups' members (Algorithm 1,
+// aggregation) and write the attention's inputs (bf16 value means, transposed,
+// and the log2(count) score bias), so the forward needs no other launch before
+// the attention.
+//
+// Barriers: the ranks of a slice are launched on one XCD (workgroup ids
+// 8 k + x all run on XCD x), all workgroups are co-resident (the host checks
+// the occupancy), and every wait is bounded: past the spin limit a workgroup
+// sets the status word and all workgroups leave.  Data crossing a barrier is
+// written and read with device-scope (sc1) accesses, so it is coherent
+// whichever XCD each rank runs on; a rank arrives only after its own stores
+// have completed (s_waitcnt vmcnt(0)).
+#include <hip/hip_runtime.h>
+
+#include <float.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "ga_internal.h"
+
+namespace ga {
+namespace {
+
+#include "ga_device.h"
+
+constexpr int kLW = 8;            // waves per workgroup
+constexpr int kLT = kLW * 64;     // threads per workgroup
+constexpr int kLCap = 4096;       // keys per rank (LDS state)
+constexpr int kLSort = 4096;      // sorted entries per update pass
+constexpr int kLNone = 255;       // the "no group" of the first round
+constexpr int kLExactB = 4;       // keys decided together by the exact fallback
+constexpr uint32_t kLSpin = 1u << 22;  // polls before a barrier gives up
+
+// ------------------------------------------------------------ device-scope access
+__device__ __forceinline__ void st_dev(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev64(double* p, double v) {
+  __hip_atomic_store((unsigned long long*)p, (unsigned long long)__double_as_longlong(v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int32_t ld_dev(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double ld_dev64(const double* p) {
+  return __longlong_as_double(
+      (long long)__hip_atomic_load((const unsigned long long*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+
+// The thread index through an opaque move: each phase of the round loop forms
+// its addresses from it locally, so the compiler cannot hoist them out of the
+// loop and keep them live across the scoring loop (whose register use would
+// then spill them to scratch, and scratch reloads wait on the same counter as
+// the device-scope stores).
+__device__ __forceinline__ int opaque_tid() {
+  int t;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(t) : "v"((int)threadIdx.x));
+  return t;
+}
+
+// Workgroup barrier that orders LDS only: it waits for this thread's LDS
+// operations (lgkmcnt), not for its global stores, so the device-scope stores
+// of a phase complete in the background; the slice barrier waits for them.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+struct LloydArgs {
+  const uint16_t* K;   // [BH][n][64] bf16
+  const uint16_t* V;   // [BH][n][64] bf16 or null (no aggregation)
+  const float* init;   // [BH][N][64] fp32 initial centroids or null (strided keys)
+  int n, N, BH, P, kpw, T;
+  float cm, cp;        // certification constants (see launch_lloyd)
+  int32_t* belong;     // [BH][n]
+  int32_t* count;      // [BH][N]
+  float* C;            // [BH][N][64]
+  uint16_t* R;         // [BH][N][64] representatives, exchanged every round
+  uint16_t* nsplit;    // [BH][N][8]
+  double* nrm64;       // [BH][N]
+  uint32_t* rec;       // [BH][P][kpw] moved-key records of the round
+  int32_t* rcnt;       // [BH][16] records per rank
+  uint32_t* sync;      // [BH][32] barrier counters (zero at launch)
+  uint32_t* status;    // bit 0: a barrier gave up
+  float* vsum;         // [BH][N][64] fp32 value sums or null
+  uint16_t* Vt;        // [BH][64][vts] bf16 value means, transposed, or null
+  float* ginit;        // [BH][Npad] score bias log2(count) / sl2e
+  int vts;
+  float inv_sl2e;
+};
+
+// LDS layout (dynamic part), in bytes from the base; Go = groups per rank.
+struct LloydLds {
+  double* S;       // [Go][64] exact member sums of the rank's groups
+  uint16_t* Rs;    // [Npad][64] -2R, swizzled (swz)
+  uint16_t* Ns;    // [Npad][8] |r|^2 split
+  double* nrm;     // [Npad] canonical |r|^2
+  float* knorm;    // [kLCap] |k| bounds of the rank's keys
+  uint32_t* ent;   // [kLCap] moved records from the bottom, uncertain keys from the top
+  uint32_t* srt;   // [kLSort] sorted (key | leave << 31) entries; also the exact rows and the finish rows
+  uint8_t* eg;     // [kLSort] the entries' local groups
+  uint8_t* bst;    // [kLCap] the rank's keys' groups
+  int* cnt;        // [Go] member counts of the rank's groups
+  int* dcnt;       // [Go]
+  int* ecnt;       // [Go]
+  int* eoff;       // [Go + 1]
+  int* ecur;       // [Go]
+};
+
+__host__ __device__ constexpr int lloyd_go(int Npad, int P) { return (Npad + P - 1) / P; }
+__host__ __device__ constexpr size_t lloyd_lds_bytes(int Npad, int P) {
+  return (size_t)lloyd_go(Npad, P) * 512 + (size_t)Npad * 128 + (size_t)Npad * 16 + (size_t)Npad * 8 +
+         (size_t)kLCap * 4 + (size_t)kLCap * 4 + (size_t)kLSort * 4 + (size_t)kLSort + (size_t)kLCap +
+         (size_t)(5 * lloyd_go(Npad, P) + 1) * 4 + 64;
+}
+
+__device__ __forceinline__ LloydLds lloyd_layout(unsigned char* base, int Npad, int Go) {
+  LloydLds l;
+  unsigned char* p = base;
+  l.S = (double*)p;          p += (size_t)Go * 512;
+  l.Rs = (uint16_t*)p;       p += (size_t)Npad * 128;
+  l.Ns = (uint16_t*)p;       p += (size_t)Npad * 16;
+  l.nrm = (double*)p;        p += (size_t)Npad * 8;
+  l.knorm = (float*)p;       p += (size_t)kLCap * 4;
+  l.ent = (uint32_t*)p;      p += (size_t)kLCap * 4;
+  l.srt = (uint32_t*)p;      p += (size_t)kLSort * 4;
+  l.eg = p;                  p += kLSort;
+  l.bst = p;                 p += kLCap;
+  l.cnt = (int*)p;           p += (size_t)Go * 4;
+  l.dcnt = (int*)p;          p += (size_t)Go * 4;
+  l.ecnt = (int*)p;          p += (size_t)Go * 4;
+  l.eoff = (int*)p;          p += (size_t)(Go + 1) * 4;
+  l.ecur = (int*)p;
+  return l;
+}
+
+// ------------------------------------------------------------ barrier
+// Arrive at barrier number k (0-based) of the slice and wait for all P ranks.
+// Returns false if the wait gave up (spin limit) or another workgroup did.
+__device__ __forceinline__ bool slice_barrier(uint32_t* ctr, uint32_t* status, int P, int k, int* s_flag) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stores have completed
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t target = (uint32_t)P * (uint32_t)(k + 1);
+    int ok = 1;
+    for (uint32_t spins = 0;; ++spins) {
+      if (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target) break;
+      if ((spins & 255u) == 255u && (__hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 1u)) {
+        ok = 0;
+        break;
+      }
+      if (spins >= kLSpin) {
+        __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    *s_flag = ok;
+  }
+  __syncthreads();
+  return *s_flag != 0;
+}
+
+// ------------------------------------------------------------ representatives
+// -2r of a bf16 pair word (exact), and the swizzled store of 16 bytes of row g.
+__device__ __forceinline__ uint32_t neg2_pair(uint32_t w) {
+  const uint32_t lo = __float_as_uint(bf16_to_f32(w & 0xffffu) * -2.0f) >> 16;
+  const uint32_t hi = __float_as_uint(bf16_to_f32(w >> 16) * -2.0f) >> 16;
+  return lo | (hi << 16);
+}
+
+// Canonical |r|^2 (fp64 fma chain over c = 0..63) of row g from the LDS copy
+// of -2R (x * -0.5 is exact), its split into Ns and the value into nrm.
+__device__ __forceinline__ double lds_row_norm(const LloydLds& L, int g) {
+  double nrm = 0.0;
+#pragma unroll
+  for (int ch = 0; ch < 8; ++ch) {
+    const u32x4 v = *(const u32x4*)(L.Rs + swz(g, ch));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const double lo = (double)(-0.5f * bf16_to_f32(v[e] & 0xffffu));
+      const double hi = (double)(-0.5f * bf16_to_f32(v[e] >> 16));
+      nrm = fma(lo, lo, nrm);
+      nrm = fma(hi, hi, nrm);
+    }
+  }
+  return nrm;
+}
+
+// First round: every rank forms all initial representatives itself, C0_j =
+// k_{floor(j n / N)} (R = C exactly) or the given init (R = bf16(C)); padded
+// groups get zero rows and the largest bf16 as |r|^2 (they never win).  The
+// owners write C for their groups.
+__device__ void lloyd_stage_init(const LloydArgs& a, const LloydLds& L, int Npad, int64_t s, int r) {
+  const int tid = threadIdx.x;
+  const uint16_t* Kbh = a.K + s * (int64_t)a.n * 64;
+  const float* ibh = a.init ? a.init + s * (int64_t)a.N * 64 : nullptr;
+  float* Cbh = a.C + s * (int64_t)a.N * 64;
+  for (int idx = tid; idx < Npad * 8; idx += kLT) {
+    const int row = idx >> 3, ch = idx & 7;
+    u32x4 w = {0u, 0u, 0u, 0u};
+    if (row < a.N) {
+      float c[8];
+      if (ibh) {
+        const float4 x = *(const float4*)(ibh + row * 64 + ch * 8), y = *(const float4*)(ibh + row * 64 + ch * 8 + 4);
+        c[0] = x.x; c[1] = x.y; c[2] = x.z; c[3] = x.w; c[4] = y.x; c[5] = y.y; c[6] = y.z; c[7] = y.w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = f32_to_bf16(c[2 * e]) | (f32_to_bf16(c[2 * e + 1]) << 16);
+      } else {
+        w = *(const u32x4*)(Kbh + ((int64_t)row * a.n / a.N) * 64 + ch * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          c[2 * e] = bf16_to_f32(w[e] & 0xffffu);
+          c[2 * e + 1] = bf16_to_f32(w[e] >> 16);
+        }
+      }
+      if (row % a.P == r) {
+        *(float4*)(Cbh + row * 64 + ch * 8) = float4{c[0], c[1], c[2], c[3]};
+        *(float4*)(Cbh + row * 64 + ch * 8 + 4) = float4{c[4], c[5], c[6], c[7]};
+      }
+    }
+    u32x4 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = neg2_pair(w[e]);
+    *(u32x4*)(L.Rs + swz(row, ch)) = v;
+  }
+  lds_barrier();
+  for (int g = tid; g < Npad; g += kLT) {
+    if (g < a.N) {
+      const double nrm = lds_row_norm(L, g);
+      L.nrm[g] = nrm;
+      write_nsplit(nrm, L.Ns + g * 8);
+    } else {
+      L.nrm[g] = 0.0;
+      *(u32x4*)(L.Ns + g * 8) = u32x4{0x7f7fu, 0u, 0u, 0u};
+    }
+  }
+}
+
+// Later rounds: the slice's representatives published by their owners.
+__device__ void lloyd_read_reps(const LloydArgs& a, const LloydLds& L, int64_t s) {
+  const int tid = opaque_tid();
+  const uint32_t* Rw = (const uint32_t*)(a.R + s * (int64_t)a.N * 64);
+  for (int idx = tid; idx < a.N * 8; idx += kLT) {
+    const int row = idx >> 3, ch = idx & 7;
+    u32x4 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = neg2_pair(ld_dev(Rw + row * 32 + ch * 4 + e));
+    *(u32x4*)(L.Rs + swz(row, ch)) = v;
+  }
+  const uint32_t* Nw = (const uint32_t*)(a.nsplit + s * (int64_t)a.N * 8);
+  for (int g = tid; g < a.N; g += kLT) {
+    *(u32x4*)(L.Ns + g * 8) = u32x4{ld_dev(Nw + g * 4), ld_dev(Nw + g * 4 + 1), 0u, 0u};
+    L.nrm[g] = ld_dev64(a.nrm64 + s * a.N + g);
+  }
+}
+
+// ------------------------------------------------------------ assignment
+// Decision for the keys of two tiles A and B (see decide_pair in
+// ga_kernels.hip for the lane swap and the certification bound E): certain
+// keys get their group in bst and a record if it changed (every key in the
+// first round, whose old group is "none"); uncertain keys are queued from the
+// top of ent for the exact fallback.
+__device__ __forceinline__ void lloyd_decide(float M1a, float M2a, int B1a, float M1b, float M2b, int B1b, float knv,
+                                             int oldv, int lk, bool valid, int N, const Certify& cf, const LloydLds& L,
+                                             int* s_nmov, int* s_nunc) {
+  const auto p1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(M1a), __float_as_uint(M1b), false, false);
+  const auto p2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(M2a), __float_as_uint(M2b), false, false);
+  const auto pb = __builtin_amdgcn_permlane32_swap((uint32_t)B1a, (uint32_t)B1b, false, false);
+  const float a1 = __uint_as_float(p1[0]), b1 = __uint_as_float(p1[1]);
+  const bool hi_wins = b1 < a1;
+  const uint32_t vw = __float_as_uint(hi_wins ? b1 : a1) & kPackMask;
+  const int jstar = 32 * (int)(hi_wins ? pb[1] : pb[0]) + 8 * (int)(vw >> 2) + (hi_wins ? 4 : 0) + (int)(vw & 3);
+  const float best = min2(a1, b1);
+  const float second = min2(max2(a1, b1), min2(__uint_as_float(p2[0]), __uint_as_float(p2[1])));
+  const float Mk = cf.nmaxf + 2.0f * knv * cf.rmaxf;
+  const float aM1 = fabsf(best);
+  const float E = (cf.cm * Mk + cf.cp * (aM1 + 3.0f * cf.cm * Mk)) * (1.0f + 0x1p-20f) + 0x1p-22f * aM1 + 1e-30f;
+  const bool certain = (second > best + 2.0f * E) && (jstar < N);
+  if (valid && certain) L.bst[lk] = (uint8_t)jstar;
+  const bool mv = valid && certain && jstar != oldv;
+  const bool un = valid && !certain;
+  const uint64_t mm = __ballot(mv), mu = __ballot(un);
+  const int lane = threadIdx.x & 63;
+  int bm = 0, bu = 0;
+  if (lane == 0) {
+    if (mm) bm = atomicAdd(s_nmov, (int)__popcll(mm));
+    if (mu) bu = atomicAdd(s_nunc, (int)__popcll(mu));
+  }
+  bm = __shfl(bm, 0);
+  bu = __shfl(bu, 0);
+  const uint64_t below = (1ull << lane) - 1ull;
+  if (mv) L.ent[bm + (int)__popcll(mm & below)] = (uint32_t)lk | ((uint32_t)oldv << 12) | ((uint32_t)jstar << 20);
+  if (un) L.ent[kLCap - 1 - (bu + (int)__popcll(mu & below))] = (uint32_t)lk | ((uint32_t)oldv << 12);
+}
+
+// Scores and decisions of the rank's keys (tiles w, w + 8, ... of wave w),
+// the key fragments of the next tile loaded while the current one is scored.
+template <int NB>
+__device__ __forceinline__ void lloyd_assign(const LloydArgs& a, const LloydLds& L, int64_t s, int k0, int nk,
+                                             bool first, const Certify& cf, int* s_nmov, int* s_nunc) {
+  const int tid = opaque_tid();
+  const int lane = tid & 63, h = lane >> 5, q = lane & 31;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ntl = (nk + 31) >> 5;
+  const int tc = wv < ntl ? (ntl - wv + kLW - 1) / kLW : 0;
+  const uint16_t* Kbh = a.K + s * (int64_t)a.n * 64;
+  u32x4 af[NB][4], an[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    an[b] = *(const u32x4*)(L.Ns + (b * 32 + q) * 8);
+#pragma unroll
+    for (int s2 = 0; s2 < 4; ++s2) af[b][s2] = *(const u32x4*)(L.Rs + swz(b * 32 + q, 4 * h + s2));
+  }
+  const u32x4 ones = h == 0 ? u32x4{0x3f803f80u, 0x3f80u, 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
+  f32x16 nacc[NB];
+  norm_terms<NB>(an, ones, nacc);
+  if (tc == 0) return;
+  // key row of tile j (wave-local index) for this lane: clamped into the slice
+  auto load = [&](int j, u32x4 (&f)[4]) __attribute__((always_inline)) {
+    const int key = min(k0 + (wv + kLW * j) * 32 + q, a.n - 1);
+    const uint16_t* krow = Kbh + (int64_t)key * 64 + h * 32;
+#pragma unroll
+    for (int s2 = 0; s2 < 4; ++s2) f[s2] = *(const u32x4*)(krow + s2 * 8);
+  };
+  auto state = [&](int j, const u32x4 (&f)[4], float& knv, int& oldv) __attribute__((always_inline)) {
+    const int lk = (wv + kLW * j) * 32 + q;
+    if (first) {
+      knv = key_norm_bound(f);
+      if (h == 0 && lk < kLCap) L.knorm[lk] = knv;
+      oldv = kLNone;
+    } else {
+      const int lkc = min(lk, kLCap - 1);
+      knv = L.knorm[lkc];
+      oldv = L.bst[lkc];
+    }
+  };
+  u32x4 kb[2][4];
+  load(0, kb[0]);
+  for (int j = 0; j < tc; j += 2) {
+    float M1a, M2a, M1b, M2b, kna, knb;
+    int B1a, B1b, olda, oldb;
+    load(min(j + 1, tc - 1), kb[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    state(j, kb[0], kna, olda);
+    score_tile<NB, true>(af, an, ones, nacc, kb[0], M1a, M2a, B1a);
+    load(min(j + 2, tc - 1), kb[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    const int jb = min(j + 1, tc - 1);  // past the last tile: a repeat, not decided
+    state(jb, kb[1], knb, oldb);
+    score_tile<NB, true>(af, an, ones, nacc, kb[1], M1b, M2b, B1b);
+    // lanes h = 0 decide key q of tile j, lanes h = 1 key q of tile j + 1
+    const int lk = (wv + kLW * (j + h)) * 32 + q;
+    const bool valid = (j + h < tc) && lk < nk;
+    lloyd_decide(M1a, M2a, B1a, M1b, M2b, B1b, h ? knb : kna, h ? oldb : olda, lk, valid, a.N, cf, L, s_nmov, s_nunc);
+  }
+}
+
+// Exact fp64 decisions of the queued keys (exact_argmin_keys), the waves
+// taking consecutive eighths of the queue.  Each result is written over its
+// queue entry (lk | old << 12 | new << 20); lloyd_exact_records then appends
+// the moved ones to the records (the queue is read into registers before any
+// append, so the two ends of ent never overlap while in use).
+__device__ void lloyd_exact(const LloydArgs& a, const LloydLds& L, int64_t s, int k0, int nunc) {
+  const int otid = opaque_tid(), lane = otid & 63, wave = __builtin_amdgcn_readfirstlane(otid >> 6);
+  const uint16_t* Kbh = a.K + s * (int64_t)a.n * 64;
+  double* kd = (double*)L.srt + wave * kLExactB * 64;
+  const int per = (nunc + kLW - 1) / kLW;
+  const int u_end = min(nunc, (wave + 1) * per);
+  for (int u0 = wave * per; u0 < u_end; u0 += kLExactB) {
+    const int nb = min(kLExactB, u_end - u0);
+    uint32_t e[kLExactB];
+#pragma unroll
+    for (int b = 0; b < kLExactB; ++b) {
+      e[b] = b < nb ? L.ent[kLCap - 1 - (u0 + b)] : 0u;
+      if (b < nb) kd[b * 64 + lane] = (double)bf16_to_f32(Kbh[(int64_t)(k0 + (e[b] & 4095u)) * 64 + lane]);
+    }
+    int jb[kLExactB];
+    switch (nb) {
+      case 1: exact_argmin_keys<1>(kd, L.Rs, L.nrm, a.N, jb); break;
+      case 2: exact_argmin_keys<2>(kd, L.Rs, L.nrm, a.N, jb); break;
+      case 3: exact_argmin_keys<3>(kd, L.Rs, L.nrm, a.N, jb); break;
+      default: exact_argmin_keys<4>(kd, L.Rs, L.nrm, a.N, jb); break;
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int b = 0; b < kLExactB; ++b) {
+        if (b >= nb) break;
+        const int lk = (int)(e[b] & 4095u);
+        L.bst[lk] = (uint8_t)jb[b];
+        L.ent[kLCap - 1 - (u0 + b)] = (e[b] & 0xfffffu) | ((uint32_t)jb[b] << 20);
+      }
+    }
+  }
+}
+
+__device__ void lloyd_exact_records(const LloydLds& L, int nunc, int* s_nmov) {
+  const int tid = opaque_tid();
+  constexpr int PER = kLCap / kLT;
+  uint32_t e[PER];
+#pragma unroll
+  for (int v = 0; v < PER; ++v) {
+    const int u = tid + kLT * v;
+    e[v] = u < nunc ? L.ent[kLCap - 1 - u] : 0u;
+  }
+  lds_barrier();
+#pragma unroll
+  for (int v = 0; v < PER; ++v) {
+    const int u = tid + kLT * v;
+    if (u < nunc && ((e[v] >> 12) & 255u) != (e[v] >> 20)) L.ent[atomicAdd(s_nmov, 1)] = e[v];
+  }
+}
+
+// ------------------------------------------------------------ sums
+// The rows of a group-sorted entry list (srt: key | leave << 31, eg: local
+// group) added into acc[g][64] by the workgroup's 64 slots of 8 lanes: a
+// slot's contiguous range is summed in fp64 registers while the group stays
+// the same and flushed into acc with LDS atomics when it changes (the sums
+// are exact, so neither the cut nor the order matters).
+constexpr int kLRunU = 8;
+__device__ __forceinline__ void lloyd_run_sums(const uint32_t* srt, const uint8_t* eg, int ne,
+                                               const uint16_t* __restrict__ Xb, double* acc) {
+  if (ne <= 0) return;
+  const int otid = opaque_tid(), lane = otid & 63, wave = __builtin_amdgcn_readfirstlane(otid >> 6);
+  const int j = lane & 7, gsl = 8 * wave + (lane >> 3);
+  constexpr int kSlots = 8 * kLW;
+  const int b0 = (int)((int64_t)gsl * ne / kSlots), b1 = (int)((int64_t)(gsl + 1) * ne / kSlots);
+  const int steps = (ne + kSlots - 1) / kSlots;
+  double x[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+  int cur = -1;
+  auto load = [&](int k0, uint32_t (&ei)[kLRunU], int (&gi)[kLRunU], u32x4 (&w)[kLRunU]) {
+#pragma unroll
+    for (int u = 0; u < kLRunU; ++u) {
+      const int e = min(b0 + k0 + u, ne - 1);
+      ei[u] = srt[e];
+      gi[u] = eg[e];
+      w[u] = *(const u32x4*)(Xb + (int64_t)(ei[u] & 0x7fffffffu) * 64 + 8 * j);
+    }
+  };
+  auto flush = [&]() {
+    double* p = acc + cur * 64 + 8 * j;
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      atomicAdd(p + f, x[f]);
+      x[f] = 0.0;
+    }
+  };
+  auto add = [&](int k0, const uint32_t (&ei)[kLRunU], const int (&gi)[kLRunU], const u32x4 (&w)[kLRunU]) {
+#pragma unroll
+    for (int u = 0; u < kLRunU; ++u) {
+      if (b0 + k0 + u >= b1) break;
+      if (gi[u] != cur) {
+        if (cur >= 0) flush();
+        cur = gi[u];
+      }
+      const double sg = (ei[u] >> 31) ? -1.0 : 1.0;
+#pragma unroll
+      for (int f = 0; f < 8; ++f)
+        x[f] = fma(sg, (double)bf16_to_f32((w[u][f >> 1] >> (16 * (f & 1))) & 0xffffu), x[f]);
+    }
+  };
+  uint32_t eA[kLRunU], eB[kLRunU];
+  int gA[kLRunU], gB[kLRunU];
+  u32x4 wA[kLRunU], wB[kLRunU];
+  load(0, eA, gA, wA);
+  for (int k0 = 0; k0 < steps; k0 += 2 * kLRunU) {
+    if (k0 + kLRunU < steps) load(k0 + kLRunU, eB, gB, wB);
+    add(k0, eA, gA, wA);
+    if (k0 + kLRunU >= steps) break;
+    if (k0 + 2 * kLRunU < steps) load(k0 + 2 * kLRunU, eA, gA, wA);
+    add(k0 + kLRunU, eB, gB, wB);
+  }
+  if (cur >= 0) flush();
+}
+
+// Counting sort of up to kLSort entries into srt/eg by local group (the
+// counters ecnt must be zero), given each thread's candidate entries.
+template <int PER>
+__device__ __forceinline__ int lloyd_sort(const LloydLds& L, int Go, const uint32_t (&ev)[PER], const int (&gv)[PER]) {
+  const int tid = opaque_tid(), lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+#pragma unroll
+  for (int u = 0; u < PER; ++u)
+    if (gv[u] >= 0) atomicAdd(&L.ecnt[gv[u]], 1);
+  lds_barrier();
+  if (wave == 0) {  // exclusive scan over Go <= 128 groups, two per lane
+    const int ga = 2 * lane, gb = ga + 1;
+    const int ca = ga < Go ? L.ecnt[ga] : 0, cb = gb < Go ? L.ecnt[gb] : 0;
+    int incl = ca + cb;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(incl, off);
+      if (lane >= off) incl += y;
+    }
+    const int sa = incl - ca - cb;
+    if (ga < Go) L.eoff[ga] = L.ecur[ga] = sa;
+    if (gb < Go) L.eoff[gb] = L.ecur[gb] = sa + ca;
+    if (lane == 63) L.eoff[Go] = incl;
+  }
+  lds_barrier();
+#pragma unroll
+  for (int u = 0; u < PER; ++u)
+    if (gv[u] >= 0) {
+      const int pos = atomicAdd(&L.ecur[gv[u]], 1);
+      L.srt[pos] = ev[u];
+      L.eg[pos] = (uint8_t)gv[u];
+    }
+  lds_barrier();
+  const int ne = L.eoff[Go];
+  if (tid < Go) L.ecnt[tid] = 0;
+  return ne;
+}
+
+// Owner update of one round: the slice's records (from every rank) touching
+// this rank's groups, summed into S with count deltas in dcnt.
+__device__ void lloyd_apply_records(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go) {
+  const int tid = opaque_tid();
+  __shared__ int pre[17];
+  if (tid < 64) {  // the P record counts at once, then their prefix sums
+    const int c = tid < a.P ? min(max(ld_dev(a.rcnt + s * 16 + tid), 0), a.kpw) : 0;
+    int incl = c;
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const int y = __shfl_up(incl, off);
+      if ((tid & 63) >= off) incl += y;
+    }
+    if (tid < a.P) pre[tid] = incl - c;
+    if (tid == a.P - 1) pre[a.P] = incl;
+  }
+  lds_barrier();
+  const int total = pre[a.P];
+  const uint16_t* Kbh = a.K + s * (int64_t)a.n * 64;
+  constexpr int PER = kLSort / 2 / kLT;  // records per thread and pass (two entries each)
+  for (int c0 = 0; c0 < total; c0 += kLSort / 2) {
+    uint32_t ev[2 * PER];
+    int gv[2 * PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = c0 + tid + kLT * u;
+      gv[2 * u] = gv[2 * u + 1] = -1;
+      ev[2 * u] = ev[2 * u + 1] = 0u;
+      if (e < total) {
+        int q = 0;
+        while (q + 1 < a.P && e >= pre[q + 1]) ++q;
+        const uint32_t rc = ld_dev(a.rec + (s * a.P + q) * (int64_t)a.kpw + (e - pre[q]));
+        const uint32_t key = min(rc & 0xffffu, (uint32_t)a.n - 1u);
+        const int o = (int)((rc >> 16) & 255u), nw = (int)(rc >> 24);
+        if (nw < a.N && nw % a.P == r) {
+          gv[2 * u] = nw / a.P;
+          ev[2 * u] = key;
+        }
+        if (o < a.N && o % a.P == r) {
+          gv[2 * u + 1] = o / a.P;
+          ev[2 * u + 1] = key | 0x80000000u;
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2 * PER; ++u)
+      if (gv[u] >= 0) atomicAdd(&L.dcnt[gv[u]], (ev[u] >> 31) ? -1 : 1);
+    const int ne = lloyd_sort<2 * PER>(L, Go, ev, gv);
+    lloyd_run_sums(L.srt, L.eg, ne, Kbh, L.S);
+    lds_barrier();
+  }
+}
+
+// Finish the rank's groups after an update: counts, C (an empty group keeps
+// C), R = bf16(C), |r|^2 and its split, published for the slice.  Every
+// global load (the previous C, needed for empty groups) is issued before any
+// store: loads and stores share one counter (vmcnt), so a load waited for
+// after the device-scope stores would also wait for those to complete.
+constexpr int kLFinU = 128 * 32 / kLT;  // (group, feature pair) items per thread, Go <= 128
+__device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go, bool last) {
+  const int tid = opaque_tid();
+  float* Cbh = a.C + s * (int64_t)a.N * 64;
+  uint32_t* Rw = (uint32_t*)(a.R + s * (int64_t)a.N * 64);
+  uint32_t* rows = L.srt;  // [Go][33] bf16 pairs for the norms (srt and eg are contiguous)
+  for (int lg = tid; lg < Go; lg += kLT) {
+    L.cnt[lg] += L.dcnt[lg];
+    L.dcnt[lg] = 0;
+  }
+  lds_barrier();
+  // the previous C of the empty groups (no global store is outstanding here:
+  // the slice barrier before the update waited for them)
+  float2 prev[kLFinU];
+#pragma unroll
+  for (int u = 0; u < kLFinU; ++u) {
+    const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31, g = r + a.P * lg;
+    prev[u] = (lg < Go && g < a.N && L.cnt[lg] == 0) ? *(const float2*)(Cbh + g * 64 + 2 * c2) : float2{0.f, 0.f};
+  }
+#pragma unroll
+  for (int u = 0; u < kLFinU; ++u) {
+    const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31, g = r + a.P * lg;
+    if (lg >= Go || g >= a.N) continue;
+    const int cnt = L.cnt[lg];
+    float c0 = prev[u].x, c1 = prev[u].y;
+    if (cnt > 0) {
+      c0 = (float)(L.S[lg * 64 + 2 * c2] / (double)cnt);
+      c1 = (float)(L.S[lg * 64 + 2 * c2 + 1] / (double)cnt);
+    }
+    prev[u] = float2{c0, c1};
+    rows[lg * 33 + c2] = f32_to_bf16(c0) | (f32_to_bf16(c1) << 16);
+  }
+#pragma unroll
+  for (int u = 0; u < kLFinU; ++u) {
+    const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31, g = r + a.P * lg;
+    if (lg >= Go || g >= a.N) continue;
+    if (L.cnt[lg] > 0) *(float2*)(Cbh + g * 64 + 2 * c2) = prev[u];
+    st_dev(Rw + g * 32 + c2, f32_to_bf16(prev[u].x) | (f32_to_bf16(prev[u].y) << 16));
+  }
+  lds_barrier();
+  for (int lg = tid; lg < Go; lg += kLT) {
+    const int g = r + a.P * lg;
+    if (g >= a.N) continue;
+    double nrm = 0.0;
+#pragma unroll 8
+    for (int c = 0; c < 64; ++c) {
+      const uint32_t w = rows[lg * 33 + (c >> 1)];
+      const double rc = (double)bf16_to_f32((c & 1) ? (w >> 16) : (w & 0xffffu));
+      nrm = fma(rc, rc, nrm);
+    }
+    uint16_t sp[8];
+    write_nsplit(nrm, sp);
+    uint32_t* Nw = (uint32_t*)(a.nsplit + (s * a.N + g) * 8);
+    st_dev(Nw, (uint32_t)sp[0] | ((uint32_t)sp[1] << 16));
+    st_dev(Nw + 1, (uint32_t)sp[2] | ((uint32_t)sp[3] << 16));
+    st_dev64(a.nrm64 + s * a.N + g, nrm);
+    if (last) a.count[s * a.N + g] = L.cnt[lg];
+  }
+  lds_barrier();
+}
+
+// Value sums of the rank's groups after the last round (Algorithm 1,
+// aggregation): every key of the slice whose final group the rank owns adds
+// its value row into S (reused, zeroed first); then the outputs.
+__device__ void lloyd_values(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go) {
+  const int tid = opaque_tid();
+  for (int i = tid; i < Go * 64; i += kLT) L.S[i] = 0.0;
+  lds_barrier();
+  const uint16_t* Vbh = a.V + s * (int64_t)a.n * 64;
+  const int32_t* bel = a.belong + s * (int64_t)a.n;
+  constexpr int PER = kLSort / kLT;
+  for (int c0 = 0; c0 < a.n; c0 += kLSort) {
+    uint32_t ev[PER];
+    int gv[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = c0 + tid + kLT * u;
+      gv[u] = -1;
+      ev[u] = (uint32_t)e;
+      if (e < a.n) {
+        const int g = ld_dev(bel + e);
+        if ((unsigned)g < (unsigned)a.N && g % a.P == r) gv[u] = g / a.P;
+      }
+    }
+    const int ne = lloyd_sort<PER>(L, Go, ev, gv);
+    lloyd_run_sums(L.srt, L.eg, ne, Vbh, L.S);
+    lds_barrier();
+  }
+  const int NpA = (a.N + 31) & ~31;  // the attention's padded group count
+  for (int idx = tid; idx < Go * 64; idx += kLT) {
+    const int lg = idx >> 6, c = idx & 63, g = r + a.P * lg;
+    if (g >= NpA) continue;
+    const bool real = g < a.N;
+    const float vs = real ? (float)L.S[lg * 64 + c] : 0.f;
+    const int cnt = real ? L.cnt[lg] : 0;
+    if (a.vsum && real) a.vsum[(s * a.N + g) * 64 + c] = vs;
+    if (a.Vt) {
+      a.Vt[(s * 64 + c) * (int64_t)a.vts + g] = (uint16_t)f32_to_bf16(cnt > 0 ? vs / (float)cnt : 0.f);
+      if (c == 0) a.ginit[s * NpA + g] = cnt > 0 ? log2f((float)cnt) * a.inv_sl2e : -INFINITY;
+    }
+  }
+}
+
+// ------------------------------------------------------------ the kernel
+template <int NB>
+__global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int s_nmov, s_nunc, s_flag;
+  __shared__ double s_red[kLW];
+  constexpr int Npad = NB * 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int bx = blockIdx.x, idx = bx >> 3;
+  const int64_t s = (int64_t)(idx / a.P) * 8 + (bx & 7);
+  const int r = idx % a.P;
+  if (s >= a.BH) return;
+  const int Go = lloyd_go(Npad, a.P);
+  const LloydLds L = lloyd_layout(smem, Npad, Go);
+  const int k0 = r * a.kpw, nk = max(0, min(a.kpw, a.n - k0));
+  uint32_t* ctr = a.sync + s * 32;
+  int bar = 0;
+
+  lloyd_stage_init(a, L, Npad, s, r);
+  for (int i = tid; i < Go * 64; i += kLT) L.S[i] = 0.0;
+  for (int i = tid; i < Go; i += kLT) {
+    L.cnt[i] = 0;
+    L.dcnt[i] = 0;
+    L.ecnt[i] = 0;
+  }
+  lds_barrier();
+
+  for (int t = 0; t < a.T; ++t) {
+    const bool first = t == 0, last = t == a.T - 1;
+    // certification constants from the largest |r|^2 of the slice
+    double mx = 0.0;
+    for (int g = tid; g < a.N; g += kLT) mx = fmax(mx, L.nrm[g]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
+    if (lane == 0) s_red[wave] = mx;
+    if (tid == 0) {
+      s_nmov = 0;
+      s_nunc = 0;
+    }
+    lds_barrier();
+    double nmax = s_red[0];
+#pragma unroll
+    for (int w = 1; w < kLW; ++w) nmax = fmax(nmax, s_red[w]);
+    const float nmaxf = (float)nmax * (1.0f + 0x1p-20f);
+    const Certify cf = {nmaxf, sqrtf(nmaxf) * (1.0f + 0x1p-20f), a.cm, a.cp};
+
+    // 1. assignment of the rank's keys
+    lloyd_assign<NB>(a, L, s, k0, nk, first, cf, &s_nmov, &s_nunc);
+    lds_barrier();
+    const int nunc = s_nunc;
+    if (nunc) {
+      lloyd_exact(a, L, s, k0, nunc);
+      lds_barrier();
+      lloyd_exact_records(L, nunc, &s_nmov);
+      lds_barrier();
+    }
+    // records of the keys whose group changed (every key in the first round)
+    const int nmov = s_nmov;
+    uint32_t* recr = a.rec + (s * a.P + r) * (int64_t)a.kpw;
+    for (int i = tid; i < nmov; i += kLT) {
+      const uint32_t e = L.ent[i];
+      st_dev(recr + i, (uint32_t)(k0 + (int)(e & 4095u)) | (((e >> 12) & 255u) << 16) | ((e >> 20) << 24));
+    }
+    if (tid == 0) st_dev(a.rcnt + s * 16 + r, nmov);
+    if (last)
+      for (int i = tid; i < nk; i += kLT) st_dev(a.belong + s * (int64_t)a.n + k0 + i, (int32_t)L.bst[i]);
+    // 2. barrier A
+    if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
+    // 3. update of the rank's groups
+    lloyd_apply_records(a, L, s, r, Go);
+    lloyd_finish(a, L, s, r, Go, last);
+    if (last) {
+      if (a.V) lloyd_values(a, L, s, r, Go);
+      break;
+    }
+    // 4. barrier B, then the slice's new representatives
+    if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
+    lloyd_read_reps(a, L, s);
+    lds_barrier();
+  }
+}
+
+// Clears the barrier counters and marks the status word as belonging to a
+// persistent grouping launch (kLloydMark, failure bit 0 clear).
+__global__ void k_lloyd_reset(uint32_t* sync, int words, uint32_t* status) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < words; i += gridDim.x * blockDim.x) sync[i] = 0u;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *status = kLloydMark;
+}
+
+}  // namespace
+}  // namespace ga
+
+// ------------------------------------------------------------ host side
+#include <map>
+#include <mutex>
+#include <tuple>
+
+namespace ga {
+namespace {
+
+using LloydFn = void (*)(LloydArgs);
+const LloydFn kLloydFns[4] = {k_lloyd<1>, k_lloyd<2>, k_lloyd<3>, k_lloyd<4>};
+
+// Compute units of the current device and the workgroups of `fn` (512
+// threads, `lds` bytes of dynamic LDS) each holds at once; cached.
+std::pair<int, int> lloyd_capacity(int nb, size_t lds) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, int, size_t>, std::pair<int, int>> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return {0, 0};
+  std::lock_guard<std::mutex> lock(mu);
+  const auto key = std::make_tuple(dev, nb, lds);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int cus = 0, occ = 0;
+  const void* fn = (const void*)kLloydFns[nb - 1];
+  (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lloyd_lds_bytes(32 * nb, 1));
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, kLT, lds) != hipSuccess) {
+    (void)hipGetLastError();
+    cus = occ = 0;
+  }
+  return cache[key] = {cus, occ};
+}
+
+struct LloydPlan {
+  bool ok = false;
+  int nb = 0, P = 0, kpw = 0;
+  unsigned grid = 0;
+  size_t lds = 0;
+};
+
+LloydPlan plan_lloyd(const Dims& d) {
+  LloydPlan p;
+  if (d.dtype != 1 || d.N > 128 || d.n > 65536 || d.BH < 1 || d.BH > 4096) return p;
+  p.nb = (d.N + 31) / 32;
+  const int Npad = 32 * p.nb;
+  const int64_t bh8 = (d.BH + 7) / 8;
+  // ranks per slice: about one per 256 keys, at most 16, and every workgroup
+  // of the launch resident at once
+  int P = (int)std::min<int64_t>(16, std::max<int64_t>(1, ((int64_t)d.n + 255) / 256));
+  for (; P >= 1; --P) {
+    const size_t lds = lloyd_lds_bytes(Npad, P);
+    const auto cap = lloyd_capacity(p.nb, lds);
+    if ((int64_t)bh8 * 8 * P <= (int64_t)cap.first * cap.second) {
+      p.lds = lds;
+      break;
+    }
+  }
+  if (P < 1) return p;
+  p.P = P;
+  p.kpw = (int)(((int64_t)d.n + 32 * P - 1) / (32 * P)) * 32;
+  if (p.kpw > kLCap) return p;
+  p.grid = (unsigned)(bh8 * 8 * P);
+  p.ok = true;
+  return p;
+}
+
+}  // namespace
+
+size_t lloyd_records(const Dims& d) { return (size_t)d.BH * ((size_t)d.n + 32 * 16); }
+
+bool lloyd_usable(const Dims& d) { return plan_lloyd(d).ok; }
+
+int lloyd_ranks(const Dims& d) {
+  const LloydPlan p = plan_lloyd(d);
+  return p.ok ? p.P : 0;
+}
+
+hipError_t launch_lloyd(const Dims& d, const void* K, const void* V, const float* init, int iters, int32_t* belong,
+                        int32_t* count, float* C, const Workspace& w, float* vsum, uint16_t* Vt, float* ginit,
+                        float scale, hipStream_t st) {
+  const LloydPlan p = plan_lloyd(d);
+  if (!p.ok) return hipErrorInvalidValue;
+  {
+    TimedLaunch timed("lloyd_reset", st);
+    const int words = (int)(d.BH * 32);
+    hipLaunchKernelGGL(k_lloyd_reset, dim3((unsigned)std::min(64, (words + 255) / 256)), dim3(256), 0, st, w.lsync,
+                       words, w.lstatus);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  TimedLaunch timed("lloyd", st);
+  LloydArgs a{};
+  a.K = (const uint16_t*)K;
+  a.V = (const uint16_t*)V;
+  a.init = init;
+  a.n = d.n;
+  a.N = d.N;
+  a.BH = (int)d.BH;
+  a.P = p.P;
+  a.kpw = p.kpw;
+  a.T = iters;
+  // certification constants: see launch_assign (MFMA accumulation error and
+  // the 4 packed index bits)
+  a.cm = (float)(kD + 4) * 0x1p-23f * (1.0f + 0x1p-10f);
+  a.cp = 0x1p-19f * (1.0f + 0x1p-10f);
+  a.belong = belong;
+  a.count = count;
+  a.C = C;
+  a.R = (uint16_t*)w.R;
+  a.nsplit = w.nsplit;
+  a.nrm64 = w.nrm64;
+  a.rec = w.lrec;
+  a.rcnt = w.lrcnt;
+  a.sync = w.lsync;
+  a.status = w.lstatus;
+  a.vsum = vsum;
+  a.Vt = Vt;
+  a.ginit = ginit;
+  a.vts = vt_stride(d.N);
+  const float sl2e = std::max(fabsf(scale) * 1.4426950408889634f, 1e-30f);
+  a.inv_sl2e = 1.0f / sl2e;
+  hipLaunchKernelGGL(kLloydFns[p.nb - 1], dim3(p.grid), dim3(kLT), p.lds, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace ga

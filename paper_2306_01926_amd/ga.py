@@ -20,7 +20,7 @@ STATUS = {0: "GA_OK", 1: "GA_ERR_INVALID_ARG", 2: "GA_ERR_UNSUPPORTED", 3: "GA_E
 SYMBOLS = ("ga_workspace_bytes", "ga_cluster", "ga_aggregate", "ga_attend", "ga_forward",
            "ga_block_workspace_bytes", "ga_project_qkv", "ga_project_out", "ga_attention_block",
            "ga_merge_plan", "ga_next_group_count", "ga_backward_workspace_bytes", "ga_backward",
-           "ga_timing_enable", "ga_timing_collect", "ga_status_string", "ga_last_error")
+           "ga_timing_enable", "ga_timing_collect", "ga_status_string", "ga_last_error", "ga_workspace_check")
 
 
 class Shape(ctypes.Structure):
@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
         for f in ("ga_cluster", "ga_aggregate", "ga_attend", "ga_forward", "ga_project_qkv", "ga_project_out",
                   "ga_attention_block", "ga_merge_plan", "ga_backward"):
             getattr(L, f).restype = ctypes.c_int
+        L.ga_workspace_check.argtypes = [Shape, i32, P, ctypes.c_size_t, P]
+        L.ga_workspace_check.restype = ctypes.c_int
         L.ga_timing_enable.argtypes = [ctypes.c_int]
         L.ga_timing_enable.restype = ctypes.c_int
         L.ga_timing_collect.argtypes = [ctypes.POINTER(KernelTime), i32, ctypes.POINTER(i32)]
@@ -355,6 +357,16 @@ def backward(Q: torch.Tensor, dO: torch.Tensor, belong: torch.Tensor, centroid: 
     _check(lib().ga_backward(s, _p(Q), _p(dO), _p(belong), _p(centroid), _p(count), _p(vsum), int(N), scale, _p(dQ),
                              _p(dK), _p(dV), _p(ws), ws.numel(), _stream(dev)))
     return dQ, dK, dV
+
+
+def workspace_check(X: torch.Tensor, N: int, ws=None) -> None:
+    """Wait for the current stream and raise GAError if the last grouping
+    launch that used this workspace (the cached one if ws is None) gave up a
+    cross-workgroup wait."""
+    dev = _qkv_like(X, "X")
+    s = shape_of(X)
+    wp, nb = _ws_args(s, N, dev, ws)
+    _check(lib().ga_workspace_check(s, int(N), wp, nb, _stream(dev)))
 
 
 def timing_enable(on: bool = True) -> None:

@@ -24,6 +24,22 @@ def dev():
     return torch.device("cuda:0")
 
 
+@pytest.fixture(params=["persistent", "rounds"])
+def path(request, monkeypatch):
+    """The grouping path under test: the persistent kernel (every round in one
+    launch; the default where it applies) or one launch per round (the
+    GA_GROUPING=rounds switch of the library)."""
+    if request.param == "rounds":
+        monkeypatch.setenv("GA_GROUPING", "rounds")
+    else:
+        monkeypatch.delenv("GA_GROUPING", raising=False)
+    return request.param
+
+
+def uses_persistent(path, dtype, N):
+    return path == "persistent" and dtype == "bf16" and N <= 128
+
+
 def say(msg):
     print(f"\n[case] {msg}", flush=True)
 
@@ -52,8 +68,10 @@ def check_close(O_gpu, O_ref, tol):
 
 
 def cluster_both(oracle_mod, K, N, iters, dtype, dev, init=None, trace=False):
-    bel, cnt, cen = ga.cluster(K.to(dev), N, iters, init=None if init is None else init.to(dev))
+    Kd = K.to(dev)
+    bel, cnt, cen = ga.cluster(Kd, N, iters, init=None if init is None else init.to(dev))
     torch.cuda.synchronize()
+    ga.workspace_check(Kd, N)
     ref = oracle_mod.cluster(f64(K), N, iters, dtype, init=None if init is None else init.numpy(), trace=trace)
     return (bel.cpu().numpy(), cnt.cpu().numpy(), cen.cpu().numpy()), ref
 
@@ -84,7 +102,7 @@ CLUSTER_CASES = [
 
 
 @pytest.mark.parametrize("case", CLUSTER_CASES, ids=lambda c: "-".join(map(str, c[:6])))
-def test_cluster_bit_exact(oracle_mod, dev, case):
+def test_cluster_bit_exact(oracle_mod, dev, case, path):
     dtype, B, H, n, N, iters, M, (slo, shi) = case
     say(f"cluster {case}")
     _, K, _ = inputs.make_qkv(B, H, n, 64, dtype, 1000 + n + N, M, slo, shi)
@@ -161,8 +179,9 @@ PARTITION_CASES = [
 
 
 @pytest.mark.parametrize("case", PARTITION_CASES, ids=lambda c: "-".join(map(str, c)))
-def test_first_round_partitions(oracle_mod, dev, case):
+def test_first_round_partitions(oracle_mod, dev, case, monkeypatch):
     n, N, parts = case
+    monkeypatch.setenv("GA_GROUPING", "rounds")  # the launch-per-round path's first round
     say(f"first-round partitions n={n} N={N} parts={parts}")
     _, K, _ = inputs.make_qkv(1, 1, n, 64, "bf16", 40 + n, max(4, N // 2), 0.05, 0.3)
     ga.timing_enable(True)
@@ -258,13 +277,19 @@ FORWARD_CASES = [
 
 
 @pytest.mark.parametrize("case", FORWARD_CASES, ids=lambda c: "-".join(map(str, c)))
-def test_forward_end_to_end(oracle_mod, dev, case):
+def test_forward_end_to_end(oracle_mod, dev, case, path):
     dtype, B, H, n, N, iters = case
-    say(f"forward {case}")
+    say(f"forward {case} ({path})")
     M = max(4, N // 2)
     Q, K, V = inputs.make_qkv(B, H, n, 64, dtype, 21 + n, M, 0.05, 0.3)
-    O, bel, cnt, cen = ga.forward(Q.to(dev), K.to(dev), V.to(dev), N, iters, return_groups=True)
+    Qd = Q.to(dev)
+    ga.timing_enable(True)
+    O, bel, cnt, cen = ga.forward(Qd, K.to(dev), V.to(dev), N, iters, return_groups=True)
     torch.cuda.synchronize()
+    ga.timing_enable(False)
+    launches = ga.timing_collect()
+    ga.workspace_check(Qd, N)
+    assert ("lloyd" in launches) == uses_persistent(path, dtype, N), sorted(launches)
     ref = oracle_mod.forward(f64(Q), f64(K), f64(V), N, iters, 1 / 8, dtype)
     assert_groups_equal((bel.cpu().numpy(), cnt.cpu().numpy(), cen.cpu().numpy()), ref)
     check_close(O, ref["O"], TOL[dtype])
