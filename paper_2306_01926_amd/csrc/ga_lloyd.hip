@@ -599,29 +599,42 @@ __device__ void lloyd_apply_records(const LloydArgs& a, const LloydLds& L, int64
 }
 
 // Finish the rank's groups after an update: counts, C (an empty group keeps
-// C), R = bf16(C), |r|^2 and its split, published for the slice.  Every
-// global load (the previous C, needed for empty groups) is issued before any
-// store: loads and stores share one counter (vmcnt), so a load waited for
-// after the device-scope stores would also wait for those to complete.
+// C), R = bf16(C), |r|^2 and its split, published for the slice.
+//
+// The previous C of every item is loaded first, unconditionally: loads and
+// stores share one counter (vmcnt), and a load the compiler cannot track
+// (e.g. a conditional one) makes it wait for every earlier store, including
+// the slow device-scope ones, before each later use.
+//
+// |r|^2: the canonical value is the fp64 fma chain over c = 0..63.  Each
+// square of a bf16 component is exact in fp64 (16 significant bits); if the
+// nonzero squares of a row span at most 31 binades, every partial sum in any
+// order is a multiple of the smallest square's last bit and below 2^53 of it,
+// so every partial sum is exact and any summation order gives the chain's
+// bits (one thread per row sums with 8 accumulators).  Rows outside that
+// range take the chain itself.
 constexpr int kLFinU = 128 * 32 / kLT;  // (group, feature pair) items per thread, Go <= 128
+constexpr int kLRowS = 36;              // LDS row stride (words) of the finished bf16 rows
+__device__ __forceinline__ int sq_exp(double x) {  // biased exponent of a square (0 for 0)
+  return (int)((__double_as_longlong(x) >> 52) & 0x7ff);
+}
 __device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go, bool last) {
   const int tid = opaque_tid();
   float* Cbh = a.C + s * (int64_t)a.N * 64;
   uint32_t* Rw = (uint32_t*)(a.R + s * (int64_t)a.N * 64);
-  uint32_t* rows = L.srt;  // [Go][33] bf16 pairs for the norms (srt and eg are contiguous)
+  uint32_t* rows = L.srt;  // [Go][kLRowS] bf16 pairs (srt and eg are contiguous: 20 KB)
+  float2 prev[kLFinU];
+#pragma unroll
+  for (int u = 0; u < kLFinU; ++u) {
+    const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31;
+    const int g = min(r + a.P * min(lg, Go - 1), a.N - 1);
+    prev[u] = *(const float2*)(Cbh + g * 64 + 2 * c2);
+  }
   for (int lg = tid; lg < Go; lg += kLT) {
     L.cnt[lg] += L.dcnt[lg];
     L.dcnt[lg] = 0;
   }
   lds_barrier();
-  // the previous C of the empty groups (no global store is outstanding here:
-  // the slice barrier before the update waited for them)
-  float2 prev[kLFinU];
-#pragma unroll
-  for (int u = 0; u < kLFinU; ++u) {
-    const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31, g = r + a.P * lg;
-    prev[u] = (lg < Go && g < a.N && L.cnt[lg] == 0) ? *(const float2*)(Cbh + g * 64 + 2 * c2) : float2{0.f, 0.f};
-  }
 #pragma unroll
   for (int u = 0; u < kLFinU; ++u) {
     const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31, g = r + a.P * lg;
@@ -633,25 +646,43 @@ __device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, i
       c1 = (float)(L.S[lg * 64 + 2 * c2 + 1] / (double)cnt);
     }
     prev[u] = float2{c0, c1};
-    rows[lg * 33 + c2] = f32_to_bf16(c0) | (f32_to_bf16(c1) << 16);
-  }
-#pragma unroll
-  for (int u = 0; u < kLFinU; ++u) {
-    const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31, g = r + a.P * lg;
-    if (lg >= Go || g >= a.N) continue;
-    if (L.cnt[lg] > 0) *(float2*)(Cbh + g * 64 + 2 * c2) = prev[u];
-    st_dev(Rw + g * 32 + c2, f32_to_bf16(prev[u].x) | (f32_to_bf16(prev[u].y) << 16));
+    rows[lg * kLRowS + c2] = f32_to_bf16(c0) | (f32_to_bf16(c1) << 16);
   }
   lds_barrier();
+  // per group (one thread): |r|^2, its split, the count
   for (int lg = tid; lg < Go; lg += kLT) {
     const int g = r + a.P * lg;
     if (g >= a.N) continue;
-    double nrm = 0.0;
-#pragma unroll 8
-    for (int c = 0; c < 64; ++c) {
-      const uint32_t w = rows[lg * 33 + (c >> 1)];
-      const double rc = (double)bf16_to_f32((c & 1) ? (w >> 16) : (w & 0xffffu));
-      nrm = fma(rc, rc, nrm);
+    u32x4 w[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) w[k] = *(const u32x4*)(rows + lg * kLRowS + 4 * k);
+    double acc[8];
+    int emax = 0, emin = 4096;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      acc[k] = 0.0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t bits = (e & 1) ? (w[k][e >> 1] >> 16) : (w[k][e >> 1] & 0xffffu);
+        const double rc = (double)bf16_to_f32(bits);
+        const double q = rc * rc;  // exact
+        acc[k] += q;
+        if (q != 0.0) {
+          emax = max(emax, sq_exp(q));
+          emin = min(emin, sq_exp(q));
+        }
+      }
+    }
+    double nrm = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
+    if (emin != 4096 && emax - emin > 31) {  // not provably exact: the chain itself
+      nrm = 0.0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const double rc = (double)bf16_to_f32((e & 1) ? (w[k][e >> 1] >> 16) : (w[k][e >> 1] & 0xffffu));
+          nrm = fma(rc, rc, nrm);
+        }
     }
     uint16_t sp[8];
     write_nsplit(nrm, sp);
@@ -660,6 +691,14 @@ __device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, i
     st_dev(Nw + 1, (uint32_t)sp[2] | ((uint32_t)sp[3] << 16));
     st_dev64(a.nrm64 + s * a.N + g, nrm);
     if (last) a.count[s * a.N + g] = L.cnt[lg];
+  }
+  // C (non-empty groups) and R
+#pragma unroll
+  for (int u = 0; u < kLFinU; ++u) {
+    const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31, g = r + a.P * lg;
+    if (lg >= Go || g >= a.N) continue;
+    if (L.cnt[lg] > 0) *(float2*)(Cbh + g * 64 + 2 * c2) = prev[u];
+    st_dev(Rw + g * 32 + c2, f32_to_bf16(prev[u].x) | (f32_to_bf16(prev[u].y) << 16));
   }
   lds_barrier();
 }
