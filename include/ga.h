@@ -139,6 +139,33 @@ int ga_forward(ga_shape_t s, const void *Q, const void *K, const void *V, int32_
                float *centroid, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * ga_forward without a workspace and without allocating, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments and results as
+ * ga_forward (the same kernels), minus the workspace: the scratch lives in a
+ * static device array of GA_NOALLOC_SCRATCH_BYTES (32 MiB) that each GPU the
+ * library runs on holds until the process ends.  No hipMalloc / hipFree or
+ * other allocating call is made.
+ *   - bf16 only, and only the shapes the one-launch grouping serves
+ *     (N <= 128, n <= 65536, every workgroup of that launch resident at
+ *     once): GA_ERR_UNSUPPORTED otherwise.
+ *   - Shapes whose scratch exceeds the array (about 8 n + 420 N + 19 KB
+ *     per (b, h) slice: B*H = 128 at n = 8000, N = 128 takes 17 MiB)
+ *     are rejected with GA_ERR_WORKSPACE.
+ *   - Every call on one GPU shares that GPU's array and leaves its contents
+ *     behind: calls that overlap in time on one GPU (two streams, two host
+ *     threads) race and must be serialised by the caller.
+ *   - `stream` must belong to the current device.
+ *   - A cross-workgroup wait of the grouping launch that gives up (it does
+ *     not while every workgroup is resident) is not reported here; use
+ *     ga_forward with ga_workspace_check where that report is wanted.
+ */
+#define GA_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int ga_forward_noalloc(ga_shape_t s, const void *Q, const void *K, const void *V, int32_t N,
+                       int32_t iters, float scale, void *O, int32_t *belong, int32_t *count,
+                       float *centroid, void *stream);
+
+/*
  * Attention block of the RITA encoder (bf16 only): the encoder is a
  * Transformer encoder whose self-attention is replaced by group attention
  * (Section 3), with the bias-free projections Q = X W_Q, K = X W_K,

@@ -10,6 +10,7 @@ ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libga.so")
 SOURCES = [os.path.join(HERE, "csrc", "ga_abi.cpp"), os.path.join(HERE, "csrc", "ga_kernels.hip"),
            os.path.join(HERE, "csrc", "ga_lloyd.hip"),
+           os.path.join(HERE, "csrc", "ga_noalloc.hip"),
            os.path.join(HERE, "csrc", "ga_block.hip"),
            os.path.join(HERE, "csrc", "ga_merge.hip"),
            os.path.join(HERE, "csrc", "ga_backward.hip")]

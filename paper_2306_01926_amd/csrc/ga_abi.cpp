@@ -142,19 +142,25 @@ int run_valuesum(const ga::Dims& d, const void* V, const int32_t* belong, int32_
   return GA_OK;
 }
 
+// Whole forward through the persistent grouping kernel: grouping, update and
+// value sums (straight into the attention's inputs) in one launch, then the
+// attention.  Uses w.R, nrm64, nsplit, Vt, ginit, lrec, lrcnt, lsync, lstatus.
+int run_forward_persistent(const ga::Dims& d, const void* Q, const void* K, const void* V, int32_t iters,
+                           float scale, void* O, int32_t* belong, int32_t* count, float* C, const ga::Workspace& w,
+                           hipStream_t st) {
+  GA_LAUNCH(ga::launch_lloyd(d, K, V, nullptr, iters, belong, count, C, w, nullptr, w.Vt, w.ginit, scale, st),
+            "grouping launch");
+  GA_LAUNCH(ga::launch_attend(d, Q, w.R, w.Vt, w.ginit, C, count, nullptr, scale, O, st), "attention launch");
+  return GA_OK;
+}
+
 // Whole forward on validated arguments (belong / count / centroid may be NULL).
 int run_forward(const ga::Dims& d, const void* Q, const void* K, const void* V, int32_t iters, float scale, void* O,
                 int32_t* belong, int32_t* count, float* centroid, const ga::Workspace& w, hipStream_t st) {
   int32_t* a = belong ? belong : w.belong;
   int32_t* cnt = count ? count : w.count;
   float* C = centroid ? centroid : w.C;
-  if (use_persistent(d)) {
-    // grouping, update and value sums (straight into the attention's inputs) in one launch
-    GA_LAUNCH(ga::launch_lloyd(d, K, V, nullptr, iters, a, cnt, C, w, nullptr, w.Vt, w.ginit, scale, st),
-              "grouping launch");
-    GA_LAUNCH(ga::launch_attend(d, Q, w.R, w.Vt, w.ginit, C, cnt, w.vsum, scale, O, st), "attention launch");
-    return GA_OK;
-  }
+  if (use_persistent(d)) return run_forward_persistent(d, Q, K, V, iters, scale, O, a, cnt, C, w, st);
   GA_TRY(run_cluster(d, K, iters, nullptr, a, cnt, C, w, st));
   if (d.dtype == GA_BF16) {
     // the value sums go straight into the attention's transposed means and bias
@@ -386,6 +392,41 @@ int ga_forward(ga_shape_t s, const void* Q, const void* K, const void* V, int32_
   ga::Workspace w;
   GA_TRY(check_ws(d, workspace, workspace_bytes, &w));
   return run_forward(d, Q, K, V, iters, scale, O, belong, count, centroid, w, (hipStream_t)stream);
+}
+
+static_assert(GA_NOALLOC_SCRATCH_BYTES == ga::kStaticScratchBytes, "static scratch size");
+
+int ga_forward_noalloc(ga_shape_t s, const void* Q, const void* K, const void* V, int32_t N, int32_t iters,
+                       float scale, void* O, int32_t* belong, int32_t* count, float* centroid, void* stream) {
+  bool empty;
+  GA_TRY(check_shape(s, N, &empty));
+  if (iters < 1) return fail(GA_ERR_INVALID_ARG, "iters must be >= 1 (got %d)", iters);
+  if (!isfinite(scale)) return fail(GA_ERR_INVALID_ARG, "scale must be finite");
+  GA_TRY(check_ptr(Q, "Q", true));
+  GA_TRY(check_ptr(K, "K", true));
+  GA_TRY(check_ptr(V, "V", true));
+  GA_TRY(check_ptr(O, "O", true));
+  GA_TRY(check_ptr(belong, "belong", false));
+  GA_TRY(check_ptr(count, "count", false));
+  GA_TRY(check_ptr(centroid, "centroid", false));
+  if (s.dtype != GA_BF16) return fail(GA_ERR_UNSUPPORTED, "ga_forward_noalloc supports bf16 only");
+  if (empty) return GA_OK;
+  const ga::Dims d = dims_of(s, N);
+  const size_t need = ga::noalloc_layout(d, nullptr, nullptr);
+  if (need > ga::kStaticScratchBytes)
+    return fail(GA_ERR_WORKSPACE, "this shape needs %zu bytes of scratch, the static scratch holds %zu", need,
+                ga::kStaticScratchBytes);
+  if (!ga::lloyd_usable(d))
+    return fail(GA_ERR_UNSUPPORTED,
+                "ga_forward_noalloc serves the one-launch grouping only: N <= 128, n <= 65536 and every workgroup "
+                "of the launch resident at once (B*H=%lld, n=%d, N=%d)", (long long)d.BH, d.n, d.N);
+  void* base = nullptr;
+  const hipError_t e = ga::static_scratch(&base);
+  if (e != hipSuccess) return hip_fail(e, "static scratch lookup");
+  ga::Workspace w;
+  ga::noalloc_layout(d, &w, base);
+  return run_forward_persistent(d, Q, K, V, iters, scale, O, belong ? belong : w.belong, count ? count : w.count,
+                                centroid ? centroid : w.C, w, (hipStream_t)stream);
 }
 
 size_t ga_block_workspace_bytes(ga_shape_t s, int32_t N) {

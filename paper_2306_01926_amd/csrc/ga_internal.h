@@ -72,6 +72,17 @@ class TimedLaunch {
 
 int vt_stride(int N);  // row stride (elements) of Vt
 size_t workspace_layout(const Dims& d, Workspace* ws, void* base);  // returns bytes
+// Layout of the allocation-free forward (persistent grouping + bf16 attention):
+// only C, R, nrm64, nsplit, belong, count, Vt, ginit and the grouping kernel's
+// lrec / lrcnt / lsync / lstatus are set, the rest are null.  Returns bytes.
+size_t noalloc_layout(const Dims& d, Workspace* ws, void* base);
+
+// Static scratch of the allocation-free forward (ga_noalloc.hip): a file-scope
+// device array of kStaticScratchBytes per GPU, held until the process ends.
+// static_scratch returns its device address on the current device (looked up
+// once per device).
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+hipError_t static_scratch(void** out);
 
 hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C, void* R,
                        double* nrm64, uint16_t* nsplit, int32_t* mcount, hipStream_t st);

@@ -2003,6 +2003,33 @@ size_t workspace_layout(const Dims& d, Workspace* ws, void* base) {
   return off;
 }
 
+size_t noalloc_layout(const Dims& d, Workspace* ws, void* base) {
+  const int64_t BH = d.BH, n = d.n, N = d.N;
+  const int64_t Npad = (N + 31) & ~31;
+  size_t off = 0;
+  char* b = (char*)base;
+  auto take = [&](size_t bytes) -> void* {
+    void* p = b ? (void*)(b + off) : nullptr;
+    off += align256(bytes);
+    return p;
+  };
+  Workspace w{};
+  w.C = (float*)take(BH * N * 64 * 4);
+  w.R = take(BH * N * 64 * 2);
+  w.nrm64 = (double*)take(BH * N * 8);
+  w.nsplit = (uint16_t*)take(BH * N * 16);
+  w.belong = (int32_t*)take(BH * n * 4);
+  w.count = (int32_t*)take(BH * N * 4);
+  w.Vt = (uint16_t*)take(BH * 64 * (int64_t)vt_stride((int)N) * 2);
+  w.ginit = (float*)take(BH * Npad * 4);
+  w.lrec = (uint32_t*)take(lloyd_records(d) * 4);
+  w.lrcnt = (int32_t*)take(BH * 16 * 4);
+  w.lsync = (uint32_t*)take(BH * 32 * 4);
+  w.lstatus = (uint32_t*)take(64 * 4);
+  if (ws) *ws = w;
+  return off;
+}
+
 hipError_t launch_init(const Dims& d, const void* K, const float* init, float* C, void* R,
                        double* nrm64, uint16_t* nsplit, int32_t* mcount, hipStream_t st) {
   TimedLaunch timed("init", st);

@@ -20,7 +20,8 @@ STATUS = {0: "GA_OK", 1: "GA_ERR_INVALID_ARG", 2: "GA_ERR_UNSUPPORTED", 3: "GA_E
 SYMBOLS = ("ga_workspace_bytes", "ga_cluster", "ga_aggregate", "ga_attend", "ga_forward",
            "ga_block_workspace_bytes", "ga_project_qkv", "ga_project_out", "ga_attention_block",
            "ga_merge_plan", "ga_next_group_count", "ga_backward_workspace_bytes", "ga_backward",
-           "ga_timing_enable", "ga_timing_collect", "ga_status_string", "ga_last_error", "ga_workspace_check")
+           "ga_timing_enable", "ga_timing_collect", "ga_status_string", "ga_last_error", "ga_workspace_check",
+           "ga_forward_noalloc")
 
 
 class Shape(ctypes.Structure):
@@ -55,6 +56,7 @@ def lib() -> ctypes.CDLL:
         L.ga_aggregate.argtypes = [Shape, P, P, i32, P, P, ctypes.c_size_t, P]
         L.ga_attend.argtypes = [Shape, P, P, P, P, i32, ctypes.c_float, P, P, ctypes.c_size_t, P]
         L.ga_forward.argtypes = [Shape, P, P, P, i32, i32, ctypes.c_float, P, P, P, P, P, ctypes.c_size_t, P]
+        L.ga_forward_noalloc.argtypes = [Shape, P, P, P, i32, i32, ctypes.c_float, P, P, P, P, P]
         L.ga_block_workspace_bytes.argtypes = [Shape, i32]
         L.ga_block_workspace_bytes.restype = ctypes.c_size_t
         L.ga_project_qkv.argtypes = [Shape, P, P, P, P, P, P]
@@ -66,7 +68,8 @@ def lib() -> ctypes.CDLL:
         L.ga_backward.argtypes = [Shape, P, P, P, P, P, P, i32, ctypes.c_float, P, P, P, P, ctypes.c_size_t, P]
         L.ga_next_group_count.argtypes = [i32, P, ctypes.c_int64, ctypes.c_double]
         L.ga_next_group_count.restype = i32
-        for f in ("ga_cluster", "ga_aggregate", "ga_attend", "ga_forward", "ga_project_qkv", "ga_project_out",
+        for f in ("ga_cluster", "ga_aggregate", "ga_attend", "ga_forward", "ga_forward_noalloc", "ga_project_qkv",
+                  "ga_project_out",
                   "ga_attention_block", "ga_merge_plan", "ga_backward"):
             getattr(L, f).restype = ctypes.c_int
         L.ga_workspace_check.argtypes = [Shape, i32, P, ctypes.c_size_t, P]
@@ -248,6 +251,27 @@ def forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, N: int, iters: in
     wp, nb = _ws_args(s, N, dev, ws)
     _check(lib().ga_forward(s, _p(Q), _p(K), _p(V), int(N), int(iters), scale, _p(O), _p(belong), _p(count),
                             _p(centroid), wp, nb, _stream(dev)))
+    return (O, belong, count, centroid) if return_groups else O
+
+
+def forward_noalloc(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, N: int, iters: int,
+                    scale: float | None = None, return_groups: bool = False, out: torch.Tensor | None = None):
+    """forward() through ga_forward_noalloc: no workspace, the library's static
+    scratch instead (bf16, shapes of the one-launch grouping only).  Calls that
+    overlap in time on one GPU share that scratch and race."""
+    dev = _qkv_like(Q, "Q")
+    s = shape_of(Q)
+    for t, nm in ((K, "K"), (V, "V"), (out, "out")):
+        _expect(t, nm, dev, Q.dtype, Q.shape, optional=nm == "out")
+    scale = 1.0 / math.sqrt(Q.shape[3]) if scale is None else float(scale)
+    O = torch.empty_like(Q) if out is None else out
+    belong = count = centroid = None
+    if return_groups:
+        belong = torch.empty(K.shape[:3], dtype=torch.int32, device=dev)
+        count = torch.empty((*K.shape[:2], N), dtype=torch.int32, device=dev)
+        centroid = torch.empty((*K.shape[:2], N, K.shape[3]), dtype=torch.float32, device=dev)
+    _check(lib().ga_forward_noalloc(s, _p(Q), _p(K), _p(V), int(N), int(iters), scale, _p(O), _p(belong),
+                                    _p(count), _p(centroid), _stream(dev)))
     return (O, belong, count, centroid) if return_groups else O
 
 

@@ -74,6 +74,35 @@ def test_forward_argument_errors(kw, status):
     assert ga.lib().ga_status_string(rc).decode() == ga.STATUS[status]
 
 
+def call_forward_noalloc(s, N=8, iters=2, scale=0.125, Q=FAKE, K=FAKE, V=FAKE, O=FAKE, belong=None):
+    return ga.lib().ga_forward_noalloc(s, P(Q), P(K), P(V), N, iters, scale, P(O),
+                                       None if belong is None else P(belong), None, None, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(s=shape(dtype=7)), 1, "dtype"),
+    (dict(s=shape(n=10), N=11), 1, "N"),
+    (dict(s=shape(), iters=0), 1, "iters"),
+    (dict(s=shape(), scale=float("nan")), 1, "scale"),
+    (dict(s=shape(), Q=0), 1, "Q"),
+    (dict(s=shape(), belong=FAKE + 8), 1, "belong"),
+    (dict(s=shape(d=32)), 2, ""),
+    (dict(s=shape(dtype=ga.GA_F32)), 2, "bf16 only"),
+    # 300 slices of 60000 keys need about 150 MB of scratch, beyond the 32 MiB array
+    (dict(s=shape(B=300, H=1, n=60000), N=128), 3, "static scratch"),
+])
+def test_forward_noalloc_argument_errors(kw, status, msg):
+    """ga_forward_noalloc checks everything it can on the host, before any HIP call."""
+    rc = call_forward_noalloc(**kw)
+    err = ga.lib().ga_last_error().decode()
+    assert rc == status, err
+    assert msg in err
+
+
+def test_forward_noalloc_empty_batch_is_a_no_op():
+    assert call_forward_noalloc(shape(B=0)) == 0
+
+
 def test_empty_batch_is_a_no_op():
     assert call_forward(shape(B=0)) == 0
     assert call_forward(shape(H=0), ws=0) == 0
