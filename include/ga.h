@@ -149,9 +149,11 @@ int ga_forward(ga_shape_t s, const void *Q, const void *K, const void *V, int32_
  *   - bf16 only, and only the shapes the one-launch grouping serves
  *     (N <= 128, n <= 65536, every workgroup of that launch resident at
  *     once): GA_ERR_UNSUPPORTED otherwise.
- *   - Shapes whose scratch exceeds the array (about 8 n + 420 N + 19 KB
- *     per (b, h) slice: B*H = 128 at n = 8000, N = 128 takes 17 MiB)
- *     are rejected with GA_ERR_WORKSPACE.
+ *   - Shapes whose scratch exceeds the array are rejected with
+ *     GA_ERR_WORKSPACE.  Per (b, h) slice the scratch is about
+ *     4 n + 420 N + 17 KB plus the grouping's exchange rows, 516 bytes per
+ *     group and workgroup of the slice (B*H = 128 at n = 8000, N = 128 takes
+ *     29 MiB).
  *   - Every call on one GPU shares that GPU's array and leaves its contents
  *     behind: calls that overlap in time on one GPU (two streams, two host
  *     threads) race and must be serialised by the caller.

@@ -144,7 +144,7 @@ int run_valuesum(const ga::Dims& d, const void* V, const int32_t* belong, int32_
 
 // Whole forward through the persistent grouping kernel: grouping, update and
 // value sums (straight into the attention's inputs) in one launch, then the
-// attention.  Uses w.R, nrm64, nsplit, Vt, ginit, lrec, lrcnt, lsync, lstatus.
+// attention.  Uses w.R, nrm64, nsplit, Vt, ginit, lxs, lxc, lxm, lsync, lstatus.
 int run_forward_persistent(const ga::Dims& d, const void* Q, const void* K, const void* V, int32_t iters,
                            float scale, void* O, int32_t* belong, int32_t* count, float* C, const ga::Workspace& w,
                            hipStream_t st) {

@@ -32,8 +32,9 @@ struct Workspace {
   double* Sp;        // [BH][kFusedP][N][64] per-partition fp64 sums of the fused update
   int32_t* cntp;     // [BH][kFusedP][N] per-partition member counts
   uint32_t* pbits;   // [BH][kFusedP][4] groups with members in each partition (bit g)
-  uint32_t* lrec;    // persistent grouping (ga_lloyd.hip): moved-key records, lloyd_records(d) words
-  int32_t* lrcnt;    // [BH][16] records per rank
+  double* lxs;       // persistent grouping (ga_lloyd.hip): [lloyd_exchange_rows(d)][64] exchanged group sums
+  int32_t* lxc;      // [lloyd_exchange_rows(d)] exchanged member-count deltas
+  int32_t* lxm;      // [BH][16] keys of each rank that changed group in a round
   uint32_t* lsync;   // [BH][32] barrier counters
   uint32_t* lstatus; // [64] status word (bit 0: a barrier gave up)
 };
@@ -74,7 +75,7 @@ int vt_stride(int N);  // row stride (elements) of Vt
 size_t workspace_layout(const Dims& d, Workspace* ws, void* base);  // returns bytes
 // Layout of the allocation-free forward (persistent grouping + bf16 attention):
 // only C, R, nrm64, nsplit, belong, count, Vt, ginit and the grouping kernel's
-// lrec / lrcnt / lsync / lstatus are set, the rest are null.  Returns bytes.
+// lxs / lxc / lxm / lsync / lstatus are set, the rest are null.  Returns bytes.
 size_t noalloc_layout(const Dims& d, Workspace* ws, void* base);
 
 // Static scratch of the allocation-free forward (ga_noalloc.hip): a file-scope
@@ -128,7 +129,7 @@ hipError_t launch_attend(const Dims& d, const void* Q, const void* R, const uint
 // is given) the value sums in one launch, for bf16, N <= 128 and shapes whose
 // workgroups (P per slice) are all resident at once.  Writes belong, count, C,
 // the final R / nsplit / nrm64 in w, and vsum and/or Vt + ginit if given.
-size_t lloyd_records(const Dims& d);  // words of w.lrec
+size_t lloyd_exchange_rows(const Dims& d);  // rows (of 64 fp64) of w.lxs: B*H * (most ranks per slice) * Npad
 // w.lstatus after a persistent grouping launch: kLloydMark, | 1 if a
 // cross-workgroup wait gave up
 constexpr uint32_t kLloydMark = 0x600d0000u;

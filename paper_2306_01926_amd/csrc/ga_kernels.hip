@@ -1995,8 +1995,9 @@ size_t workspace_layout(const Dims& d, Workspace* ws, void* base) {
   w.Sp = (double*)take(BH * fp * N * 64 * 8);
   w.cntp = (int32_t*)take(BH * fp * N * 4);
   w.pbits = (uint32_t*)take(BH * fp * 4 * 4);
-  w.lrec = (uint32_t*)take(lloyd_records(d) * 4);
-  w.lrcnt = (int32_t*)take(BH * 16 * 4);
+  w.lxs = (double*)take(lloyd_exchange_rows(d) * 64 * 8);
+  w.lxc = (int32_t*)take(lloyd_exchange_rows(d) * 4);
+  w.lxm = (int32_t*)take(BH * 16 * 4);
   w.lsync = (uint32_t*)take(BH * 32 * 4);
   w.lstatus = (uint32_t*)take(64 * 4);
   if (ws) *ws = w;
@@ -2022,8 +2023,9 @@ size_t noalloc_layout(const Dims& d, Workspace* ws, void* base) {
   w.count = (int32_t*)take(BH * N * 4);
   w.Vt = (uint16_t*)take(BH * 64 * (int64_t)vt_stride((int)N) * 2);
   w.ginit = (float*)take(BH * Npad * 4);
-  w.lrec = (uint32_t*)take(lloyd_records(d) * 4);
-  w.lrcnt = (int32_t*)take(BH * 16 * 4);
+  w.lxs = (double*)take(lloyd_exchange_rows(d) * 64 * 8);
+  w.lxc = (int32_t*)take(lloyd_exchange_rows(d) * 4);
+  w.lxm = (int32_t*)take(BH * 16 * 4);
   w.lsync = (uint32_t*)take(BH * 32 * 4);
   w.lstatus = (uint32_t*)take(64 * 4);
   if (ws) *ws = w;

@@ -8,26 +8,29 @@
 //
 //   1. assign: every rank scores its keys against all representatives (MFMA
 //      32x32x16 bf16, packed top-2, certified argmin with the exact fp64
-//      fallback; the same decision procedure as k_assign_reg) and writes one
-//      4-byte record (key, old group, new group) per key whose group changed;
-//   2. barrier A over the slice's P ranks;
-//   3. update: every rank reads all the slice's records, keeps the (key,
-//      side) entries of its own groups, sorts them by group in LDS and adds
-//      the key rows (joins +, leaves -) into its exact fp64 member sums, which
-//      stay in LDS for the whole launch; then C = (float)(S / count) (an
-//      empty group keeps C), R = bf16(C), the canonical |r|^2 and its split,
-//      published for the slice;
+//      fallback; the same decision procedure as k_assign_reg) and adds the
+//      rows of its keys that changed group into per-group fp64 sums in LDS
+//      (joins +, leaves -): in the first round, where every key joins, straight
+//      from the registers that hold the key tiles; later, in a pass over the
+//      few moved keys;
+//   2. every rank publishes its sums for the groups it does not own (deltas
+//      of this round) and zeroes them; barrier A over the slice's P ranks;
+//   3. update: every rank adds the other ranks' deltas for its groups into its
+//      exact fp64 member sums, which stay in LDS for the whole launch; then
+//      C = (float)(S / count) (an empty group keeps C), R = bf16(C), the
+//      canonical |r|^2 and its split, published for the slice;
 //   4. barrier B; every rank reads the slice's new representatives.
 //
 // The member sums of bf16 keys are exact in fp64 (while (e_max - e_min) +
-// log2 count <= 45, see ga_kernels.hip), so the order in which the ranks, the
-// records and the LDS atomics add them cannot change a bit: groups, counts
-// and centroids are those of the oracle.  In the first round every key is a
-// join (old group "none"), which forms the full sums.  After the last round's
-// update the ranks sum the value rows of their groups' members (Algorithm 1,
-// aggregation) and write the attention's inputs (bf16 value means, transposed,
-// and the log2(count) score bias), so the forward needs no other launch before
-// the attention.
+// log2 count <= 45, see ga_kernels.hip), so the order in which the ranks and
+// the LDS atomics add them cannot change a bit: groups, counts and centroids
+// are those of the oracle.  A round in which no key of the slice changes group
+// is a fixed point: every later round would repeat it, so the slice stops
+// there with the same result.  After the last round every rank sums the value
+// rows of its keys per group the same way (Algorithm 1, aggregation), the
+// owners add the other ranks' parts and write the attention's inputs (bf16
+// value means, transposed, and the log2(count) score bias), so the forward
+// needs no other launch before the attention.
 //
 // Barriers: the ranks of a slice are launched on one XCD (workgroup ids
 // 8 k + x all run on XCD x), all workgroups are co-resident (the host checks
@@ -52,7 +55,14 @@ namespace {
 constexpr int kLW = 8;            // waves per workgroup
 constexpr int kLT = kLW * 64;     // threads per workgroup
 constexpr int kLCap = 4096;       // keys per rank (LDS state)
-constexpr int kLSort = 4096;      // sorted entries per update pass
+constexpr int kLSort = 4096;      // sorted entries per pass of the sums
+constexpr int kLSA = 65;          // row stride (fp64) of the LDS sums: rows of distinct groups start in distinct banks
+constexpr int kLMaxWG = 256;      // workgroups of one launch at most (one per MI355X compute unit)
+
+// The LDS sums keep feature d of a row at position pi(d) (the 8 x 8 transpose
+// of the row): the eight lanes that add one 16-byte chunk of a row (features
+// 8 j + f, f fixed per instruction) then hit eight distinct banks.
+__host__ __device__ constexpr int lloyd_pi(int d) { return ((d & 7) << 3) | (d >> 3); }
 constexpr int kLNone = 255;       // the "no group" of the first round
 constexpr int kLExactB = 4;       // keys decided together by the exact fallback
 constexpr uint32_t kLSpin = 1u << 22;  // polls before a barrier gives up
@@ -111,8 +121,9 @@ struct LloydArgs {
   uint16_t* R;         // [BH][N][64] representatives, exchanged every round
   uint16_t* nsplit;    // [BH][N][8]
   double* nrm64;       // [BH][N]
-  uint32_t* rec;       // [BH][P][kpw] moved-key records of the round
-  int32_t* rcnt;       // [BH][16] records per rank
+  double* xs;          // [BH][P][Npad][64] each rank's sums for the groups it does not own
+  int32_t* xc;         // [BH][P][Npad] and the member-count deltas
+  int32_t* xm;         // [BH][16] keys of each rank that changed group in the round
   uint32_t* sync;      // [BH][32] barrier counters (zero at launch)
   uint32_t* status;    // bit 0: a barrier gave up
   float* vsum;         // [BH][N][64] fp32 value sums or null
@@ -124,46 +135,53 @@ struct LloydArgs {
 
 // LDS layout (dynamic part), in bytes from the base; Go = groups per rank.
 struct LloydLds {
-  double* S;       // [Go][64] exact member sums of the rank's groups
+  double* SA;      // [Npad][kLSA] the rank's groups: exact member sums; other groups: this round's deltas
+  int* dcA;        // [Npad] member-count deltas of the rank's keys
   uint16_t* Rs;    // [Npad][64] -2R, swizzled (swz)
   uint16_t* Ns;    // [Npad][8] |r|^2 split
   double* nrm;     // [Npad] canonical |r|^2
   float* knorm;    // [kLCap] |k| bounds of the rank's keys
-  uint32_t* ent;   // [kLCap] moved records from the bottom, uncertain keys from the top
-  uint32_t* srt;   // [kLSort] sorted (key | leave << 31) entries; also the exact rows and the finish rows
-  uint8_t* eg;     // [kLSort] the entries' local groups
+  uint32_t* ent;   // [kLCap] moved keys from the bottom, uncertain keys from the top
+  uint32_t* X;     // scratch: the exact fallback's key rows, the finished bf16 rows, the sorted entries
+  uint32_t* srt;   // [kLSort] (in X) entries sorted by group: key | leave << 31
+  uint8_t* eg;     // [kLSort] (in X) the entries' groups
   uint8_t* bst;    // [kLCap] the rank's keys' groups
+  int* ecnt;       // [Npad] entries per group (zero between sorts)
+  int* eoff;       // [Npad + 1]
+  int* ecur;       // [Npad]
   int* cnt;        // [Go] member counts of the rank's groups
-  int* dcnt;       // [Go]
-  int* ecnt;       // [Go]
-  int* eoff;       // [Go + 1]
-  int* ecur;       // [Go]
 };
 
+constexpr int kLRowS = 36;  // LDS row stride (words) of the finished bf16 rows
 __host__ __device__ constexpr int lloyd_go(int Npad, int P) { return (Npad + P - 1) / P; }
+__host__ __device__ constexpr size_t cmax(size_t x, size_t y) { return x > y ? x : y; }
+__host__ __device__ constexpr size_t lloyd_x_bytes(int Npad, int P) {
+  return cmax(cmax((size_t)kLW * kLExactB * 64 * 8, (size_t)lloyd_go(Npad, P) * kLRowS * 4), (size_t)kLSort * 5);
+}
 __host__ __device__ constexpr size_t lloyd_lds_bytes(int Npad, int P) {
-  return (size_t)lloyd_go(Npad, P) * 512 + (size_t)Npad * 128 + (size_t)Npad * 16 + (size_t)Npad * 8 +
-         (size_t)kLCap * 4 + (size_t)kLCap * 4 + (size_t)kLSort * 4 + (size_t)kLSort + (size_t)kLCap +
-         (size_t)(5 * lloyd_go(Npad, P) + 1) * 4 + 64;
+  return (size_t)Npad * kLSA * 8 + (size_t)Npad * 4 + (size_t)Npad * 128 + (size_t)Npad * 16 + (size_t)Npad * 8 +
+         (size_t)kLCap * 4 + (size_t)kLCap * 4 + lloyd_x_bytes(Npad, P) + (size_t)kLCap +
+         (size_t)(3 * Npad + 1) * 4 + (size_t)lloyd_go(Npad, P) * 4 + 64;
 }
 
-__device__ __forceinline__ LloydLds lloyd_layout(unsigned char* base, int Npad, int Go) {
+__device__ __forceinline__ LloydLds lloyd_layout(unsigned char* base, int Npad, int P) {
   LloydLds l;
   unsigned char* p = base;
-  l.S = (double*)p;          p += (size_t)Go * 512;
+  l.SA = (double*)p;         p += (size_t)Npad * kLSA * 8;
+  l.dcA = (int*)p;           p += (size_t)Npad * 4;
   l.Rs = (uint16_t*)p;       p += (size_t)Npad * 128;
   l.Ns = (uint16_t*)p;       p += (size_t)Npad * 16;
   l.nrm = (double*)p;        p += (size_t)Npad * 8;
   l.knorm = (float*)p;       p += (size_t)kLCap * 4;
   l.ent = (uint32_t*)p;      p += (size_t)kLCap * 4;
-  l.srt = (uint32_t*)p;      p += (size_t)kLSort * 4;
-  l.eg = p;                  p += kLSort;
+  l.X = (uint32_t*)p;        p += lloyd_x_bytes(Npad, P);
+  l.srt = l.X;
+  l.eg = (uint8_t*)(l.X + kLSort);
   l.bst = p;                 p += kLCap;
-  l.cnt = (int*)p;           p += (size_t)Go * 4;
-  l.dcnt = (int*)p;          p += (size_t)Go * 4;
-  l.ecnt = (int*)p;          p += (size_t)Go * 4;
-  l.eoff = (int*)p;          p += (size_t)(Go + 1) * 4;
-  l.ecur = (int*)p;
+  l.ecnt = (int*)p;          p += (size_t)Npad * 4;
+  l.eoff = (int*)p;          p += (size_t)(Npad + 1) * 4;
+  l.ecur = (int*)p;          p += (size_t)Npad * 4;
+  l.cnt = (int*)p;
   return l;
 }
 
@@ -274,31 +292,63 @@ __device__ void lloyd_stage_init(const LloydArgs& a, const LloydLds& L, int Npad
 
 // Later rounds: the slice's representatives published by their owners.
 __device__ void lloyd_read_reps(const LloydArgs& a, const LloydLds& L, int64_t s) {
+  constexpr int kU = 128 * 8 / kLT;  // 16-byte chunks of R per thread, N <= 128
   const int tid = opaque_tid();
   const uint32_t* Rw = (const uint32_t*)(a.R + s * (int64_t)a.N * 64);
-  for (int idx = tid; idx < a.N * 8; idx += kLT) {
-    const int row = idx >> 3, ch = idx & 7;
-    u32x4 v;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = neg2_pair(ld_dev(Rw + row * 32 + ch * 4 + e));
-    *(u32x4*)(L.Rs + swz(row, ch)) = v;
-  }
   const uint32_t* Nw = (const uint32_t*)(a.nsplit + s * (int64_t)a.N * 8);
-  for (int g = tid; g < a.N; g += kLT) {
-    *(u32x4*)(L.Ns + g * 8) = u32x4{ld_dev(Nw + g * 4), ld_dev(Nw + g * 4 + 1), 0u, 0u};
-    L.nrm[g] = ld_dev64(a.nrm64 + s * a.N + g);
+  // every load first (one round trip), clamped into the slice's rows
+  u32x4 v[kU];
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const int idx = min(tid + kLT * u, a.N * 8 - 1), row = idx >> 3, ch = idx & 7;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[u][e] = ld_dev(Rw + row * 32 + ch * 4 + e);
+  }
+  const int gq = min(tid, a.N - 1);
+  const uint32_t n0 = ld_dev(Nw + gq * 4), n1 = ld_dev(Nw + gq * 4 + 1);
+  const double nr = ld_dev64(a.nrm64 + s * a.N + gq);
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const int idx = tid + kLT * u, row = idx >> 3, ch = idx & 7;
+    if (idx >= a.N * 8) continue;
+    u32x4 w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = neg2_pair(v[u][e]);
+    *(u32x4*)(L.Rs + swz(row, ch)) = w;
+  }
+  if (tid < a.N) {
+    *(u32x4*)(L.Ns + tid * 8) = u32x4{n0, n1, 0u, 0u};
+    L.nrm[tid] = nr;
   }
 }
 
 // ------------------------------------------------------------ assignment
+// The certification bound of ga_kernels.hip,
+//   E = (cm Mk + cp (|M1| + 3 cm Mk)) (1 + 2^-20) + 2^-22 |M1| + 1e-30,
+//   Mk = nmax + 2 |k| rmax,
+// regrouped as eA + eB |k| + eC |M1| with the per-round uniform terms formed
+// once (equal in real arithmetic; the few extra fp32 roundings are far inside
+// the 2^-20 margin).
+struct LloydCert {
+  float eA, eB, eC;
+};
+__device__ __forceinline__ LloydCert lloyd_cert(float nmaxf, float rmaxf, float cm, float cp) {
+  const float f = 1.0f + 0x1p-20f, cmm = cm * (1.0f + 3.0f * cp);
+  LloydCert c;
+  c.eA = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(cmm * nmaxf * f + 1e-30f)));
+  c.eB = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(2.0f * cmm * rmaxf * f)));
+  c.eC = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(cp * f + 0x1p-22f)));
+  return c;
+}
+
 // Decision for the keys of two tiles A and B (see decide_pair in
-// ga_kernels.hip for the lane swap and the certification bound E): certain
-// keys get their group in bst and a record if it changed (every key in the
-// first round, whose old group is "none"); uncertain keys are queued from the
-// top of ent for the exact fallback.
+// ga_kernels.hip for the lane swap): certain keys get their group in bst and,
+// after the first round, a moved-key entry from the bottom of ent if it
+// changed; uncertain keys are queued from the top of ent for the exact
+// fallback.
 __device__ __forceinline__ void lloyd_decide(float M1a, float M2a, int B1a, float M1b, float M2b, int B1b, float knv,
-                                             int oldv, int lk, bool valid, int N, const Certify& cf, const LloydLds& L,
-                                             int* s_nmov, int* s_nunc) {
+                                             int oldv, int lk, bool valid, bool first, int N, const LloydCert& cf,
+                                             const LloydLds& L, int* s_nmov, int* s_nunc) {
   const auto p1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(M1a), __float_as_uint(M1b), false, false);
   const auto p2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(M2a), __float_as_uint(M2b), false, false);
   const auto pb = __builtin_amdgcn_permlane32_swap((uint32_t)B1a, (uint32_t)B1b, false, false);
@@ -308,12 +358,10 @@ __device__ __forceinline__ void lloyd_decide(float M1a, float M2a, int B1a, floa
   const int jstar = 32 * (int)(hi_wins ? pb[1] : pb[0]) + 8 * (int)(vw >> 2) + (hi_wins ? 4 : 0) + (int)(vw & 3);
   const float best = min2(a1, b1);
   const float second = min2(max2(a1, b1), min2(__uint_as_float(p2[0]), __uint_as_float(p2[1])));
-  const float Mk = cf.nmaxf + 2.0f * knv * cf.rmaxf;
-  const float aM1 = fabsf(best);
-  const float E = (cf.cm * Mk + cf.cp * (aM1 + 3.0f * cf.cm * Mk)) * (1.0f + 0x1p-20f) + 0x1p-22f * aM1 + 1e-30f;
-  const bool certain = (second > best + 2.0f * E) && (jstar < N);
+  const float E = fmaf(fabsf(best), cf.eC, knv * cf.eB) + cf.eA;
+  const bool certain = (second > fmaf(2.0f, E, best)) && (jstar < N);
   if (valid && certain) L.bst[lk] = (uint8_t)jstar;
-  const bool mv = valid && certain && jstar != oldv;
+  const bool mv = valid && certain && !first && jstar != oldv;
   const bool un = valid && !certain;
   const uint64_t mm = __ballot(mv), mu = __ballot(un);
   const int lane = threadIdx.x & 63;
@@ -322,18 +370,16 @@ __device__ __forceinline__ void lloyd_decide(float M1a, float M2a, int B1a, floa
     if (mm) bm = atomicAdd(s_nmov, (int)__popcll(mm));
     if (mu) bu = atomicAdd(s_nunc, (int)__popcll(mu));
   }
-  bm = __shfl(bm, 0);
-  bu = __shfl(bu, 0);
+  bm = __builtin_amdgcn_readlane(bm, 0);
+  bu = __builtin_amdgcn_readlane(bu, 0);
   const uint64_t below = (1ull << lane) - 1ull;
   if (mv) L.ent[bm + (int)__popcll(mm & below)] = (uint32_t)lk | ((uint32_t)oldv << 12) | ((uint32_t)jstar << 20);
   if (un) L.ent[kLCap - 1 - (bu + (int)__popcll(mu & below))] = (uint32_t)lk | ((uint32_t)oldv << 12);
 }
 
-// Scores and decisions of the rank's keys (tiles w, w + 8, ... of wave w),
-// the key fragments of the next tile loaded while the current one is scored.
 template <int NB>
 __device__ __forceinline__ void lloyd_assign(const LloydArgs& a, const LloydLds& L, int64_t s, int k0, int nk,
-                                             bool first, const Certify& cf, int* s_nmov, int* s_nunc) {
+                                             bool first, bool rev, const LloydCert& cf, int* s_nmov, int* s_nunc) {
   const int tid = opaque_tid();
   const int lane = tid & 63, h = lane >> 5, q = lane & 31;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -351,15 +397,19 @@ __device__ __forceinline__ void lloyd_assign(const LloydArgs& a, const LloydLds&
   f32x16 nacc[NB];
   norm_terms<NB>(an, ones, nacc);
   if (tc == 0) return;
+  // tile of the wave's j-th step: waves take every kLW-th tile, in ascending
+  // order or (rev) descending, so that a round starts on the keys the previous
+  // round read last
+  auto tile = [&](int j) __attribute__((always_inline)) { return rev ? ntl - 1 - wv - kLW * j : wv + kLW * j; };
   // key row of tile j (wave-local index) for this lane: clamped into the slice
   auto load = [&](int j, u32x4 (&f)[4]) __attribute__((always_inline)) {
-    const int key = min(k0 + (wv + kLW * j) * 32 + q, a.n - 1);
+    const int key = min(k0 + tile(j) * 32 + q, a.n - 1);
     const uint16_t* krow = Kbh + (int64_t)key * 64 + h * 32;
 #pragma unroll
     for (int s2 = 0; s2 < 4; ++s2) f[s2] = *(const u32x4*)(krow + s2 * 8);
   };
   auto state = [&](int j, const u32x4 (&f)[4], float& knv, int& oldv) __attribute__((always_inline)) {
-    const int lk = (wv + kLW * j) * 32 + q;
+    const int lk = tile(j) * 32 + q;
     if (first) {
       knv = key_norm_bound(f);
       if (h == 0 && lk < kLCap) L.knorm[lk] = knv;
@@ -385,23 +435,25 @@ __device__ __forceinline__ void lloyd_assign(const LloydArgs& a, const LloydLds&
     state(jb, kb[1], knb, oldb);
     score_tile<NB, true>(af, an, ones, nacc, kb[1], M1b, M2b, B1b);
     // lanes h = 0 decide key q of tile j, lanes h = 1 key q of tile j + 1
-    const int lk = (wv + kLW * (j + h)) * 32 + q;
-    const bool valid = (j + h < tc) && lk < nk;
-    lloyd_decide(M1a, M2a, B1a, M1b, M2b, B1b, h ? knb : kna, h ? oldb : olda, lk, valid, a.N, cf, L, s_nmov, s_nunc);
+    const bool valid = j + h < tc && tile(j + h) * 32 + q < nk;
+    const int lk = valid ? tile(j + h) * 32 + q : 0;
+    lloyd_decide(M1a, M2a, B1a, M1b, M2b, B1b, h ? knb : kna, h ? oldb : olda, lk, valid, first, a.N, cf, L, s_nmov,
+                 s_nunc);
   }
 }
 
-// Exact fp64 decisions of the queued keys (exact_argmin_keys), the waves
-// taking consecutive eighths of the queue.  Each result is written over its
-// queue entry (lk | old << 12 | new << 20); lloyd_exact_records then appends
-// the moved ones to the records (the queue is read into registers before any
-// append, so the two ends of ent never overlap while in use).
-__device__ void lloyd_exact(const LloydArgs& a, const LloydLds& L, int64_t s, int k0, int nunc) {
+// Exact fallback for the uncertain keys (queued from the top of ent): the
+// wave takes kLExactB keys at a time and decides them in fp64; after the
+// first round it adds the rows of those that changed group (fp64, from the
+// LDS copy) into the sums.
+__device__ void lloyd_exact(const LloydArgs& a, const LloydLds& L, int64_t s, int k0, int nunc, bool first,
+                            int* s_xmov) {
   const int otid = opaque_tid(), lane = otid & 63, wave = __builtin_amdgcn_readfirstlane(otid >> 6);
   const uint16_t* Kbh = a.K + s * (int64_t)a.n * 64;
-  double* kd = (double*)L.srt + wave * kLExactB * 64;
+  double* kd = (double*)L.X + wave * kLExactB * 64;
   const int per = (nunc + kLW - 1) / kLW;
   const int u_end = min(nunc, (wave + 1) * per);
+  int moved = 0;
   for (int u0 = wave * per; u0 < u_end; u0 += kLExactB) {
     const int nb = min(kLExactB, u_end - u0);
     uint32_t e[kLExactB];
@@ -417,44 +469,35 @@ __device__ void lloyd_exact(const LloydArgs& a, const LloydLds& L, int64_t s, in
       case 3: exact_argmin_keys<3>(kd, L.Rs, L.nrm, a.N, jb); break;
       default: exact_argmin_keys<4>(kd, L.Rs, L.nrm, a.N, jb); break;
     }
-    if (lane == 0) {
 #pragma unroll
-      for (int b = 0; b < kLExactB; ++b) {
-        if (b >= nb) break;
-        const int lk = (int)(e[b] & 4095u);
-        L.bst[lk] = (uint8_t)jb[b];
-        L.ent[kLCap - 1 - (u0 + b)] = (e[b] & 0xfffffu) | ((uint32_t)jb[b] << 20);
+    for (int b = 0; b < kLExactB; ++b) {
+      if (b >= nb) break;
+      const int lk = (int)(e[b] & 4095u), old = (int)((e[b] >> 12) & 255u), nw = jb[b];
+      if (nw == old) continue;
+      if (lane == 0) L.bst[lk] = (uint8_t)nw;
+      if (first) continue;  // the first round's sums are formed from every key afterwards
+      const double x = kd[b * 64 + lane];
+      atomicAdd(L.SA + nw * kLSA + lloyd_pi(lane), x);
+      atomicAdd(L.SA + old * kLSA + lloyd_pi(lane), -x);
+      if (lane == 0) {
+        atomicAdd(&L.dcA[nw], 1);
+        atomicAdd(&L.dcA[old], -1);
       }
+      ++moved;
     }
   }
-}
-
-__device__ void lloyd_exact_records(const LloydLds& L, int nunc, int* s_nmov) {
-  const int tid = opaque_tid();
-  constexpr int PER = kLCap / kLT;
-  uint32_t e[PER];
-#pragma unroll
-  for (int v = 0; v < PER; ++v) {
-    const int u = tid + kLT * v;
-    e[v] = u < nunc ? L.ent[kLCap - 1 - u] : 0u;
-  }
-  lds_barrier();
-#pragma unroll
-  for (int v = 0; v < PER; ++v) {
-    const int u = tid + kLT * v;
-    if (u < nunc && ((e[v] >> 12) & 255u) != (e[v] >> 20)) L.ent[atomicAdd(s_nmov, 1)] = e[v];
-  }
+  if (lane == 0 && moved) atomicAdd(s_xmov, moved);
 }
 
 // ------------------------------------------------------------ sums
-// The rows of a group-sorted entry list (srt: key | leave << 31, eg: local
-// group) added into acc[g][64] by the workgroup's 64 slots of 8 lanes: a
-// slot's contiguous range is summed in fp64 registers while the group stays
-// the same and flushed into acc with LDS atomics when it changes (the sums
-// are exact, so neither the cut nor the order matters).
+// The rows of a group-sorted entry list (srt: key | leave << 31, eg: group,
+// keys local to the rank, rows from Xr) added into the LDS sums by the
+// workgroup's 64 slots of 8 lanes: a slot's contiguous range is summed in
+// fp64 registers while the group stays the same and flushed into the sums
+// with LDS atomics when it changes (the sums are exact, so neither the cut
+// nor the order matters).
 constexpr int kLRunU = 8;
-__device__ __forceinline__ void lloyd_run_sums(const uint32_t* srt, const uint8_t* eg, int ne,
-                                               const uint16_t* __restrict__ Xb, double* acc) {
+__device__ __forceinline__ void lloyd_run_sums(const LloydLds& L, int ne, const uint16_t* __restrict__ Xr) {
   if (ne <= 0) return;
   const int otid = opaque_tid(), lane = otid & 63, wave = __builtin_amdgcn_readfirstlane(otid >> 6);
   const int j = lane & 7, gsl = 8 * wave + (lane >> 3);
@@ -467,16 +510,16 @@ __device__ __forceinline__ void lloyd_run_sums(const uint32_t* srt, const uint8_
 #pragma unroll
     for (int u = 0; u < kLRunU; ++u) {
       const int e = min(b0 + k0 + u, ne - 1);
-      ei[u] = srt[e];
-      gi[u] = eg[e];
-      w[u] = *(const u32x4*)(Xb + (int64_t)(ei[u] & 0x7fffffffu) * 64 + 8 * j);
+      ei[u] = L.srt[e];
+      gi[u] = L.eg[e];
+      w[u] = *(const u32x4*)(Xr + (int64_t)(ei[u] & 0x7fffffffu) * 64 + 8 * j);
     }
   };
   auto flush = [&]() {
-    double* p = acc + cur * 64 + 8 * j;
+    double* p = L.SA + cur * kLSA + j;
 #pragma unroll
-    for (int f = 0; f < 8; ++f) {
-      atomicAdd(p + f, x[f]);
+    for (int f = 0; f < 8; ++f) {  // feature 8 j + f at position 8 f + j
+      atomicAdd(p + 8 * f, x[f]);
       x[f] = 0.0;
     }
   };
@@ -508,18 +551,19 @@ __device__ __forceinline__ void lloyd_run_sums(const uint32_t* srt, const uint8_
   if (cur >= 0) flush();
 }
 
-// Counting sort of up to kLSort entries into srt/eg by local group (the
-// counters ecnt must be zero), given each thread's candidate entries.
+// Counting sort of up to kLSort entries into srt/eg by group (the counters
+// ecnt must be zero), given each thread's candidate entries (gv < 0: none).
 template <int PER>
-__device__ __forceinline__ int lloyd_sort(const LloydLds& L, int Go, const uint32_t (&ev)[PER], const int (&gv)[PER]) {
+__device__ __forceinline__ int lloyd_sort(const LloydLds& L, int Npad, const uint32_t (&ev)[PER],
+                                          const int (&gv)[PER]) {
   const int tid = opaque_tid(), lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 #pragma unroll
   for (int u = 0; u < PER; ++u)
     if (gv[u] >= 0) atomicAdd(&L.ecnt[gv[u]], 1);
   lds_barrier();
-  if (wave == 0) {  // exclusive scan over Go <= 128 groups, two per lane
+  if (wave == 0) {  // exclusive scan over Npad <= 128 groups, two per lane
     const int ga = 2 * lane, gb = ga + 1;
-    const int ca = ga < Go ? L.ecnt[ga] : 0, cb = gb < Go ? L.ecnt[gb] : 0;
+    const int ca = ga < Npad ? L.ecnt[ga] : 0, cb = gb < Npad ? L.ecnt[gb] : 0;
     int incl = ca + cb;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -527,9 +571,9 @@ __device__ __forceinline__ int lloyd_sort(const LloydLds& L, int Go, const uint3
       if (lane >= off) incl += y;
     }
     const int sa = incl - ca - cb;
-    if (ga < Go) L.eoff[ga] = L.ecur[ga] = sa;
-    if (gb < Go) L.eoff[gb] = L.ecur[gb] = sa + ca;
-    if (lane == 63) L.eoff[Go] = incl;
+    if (ga < Npad) L.eoff[ga] = L.ecur[ga] = sa;
+    if (gb < Npad) L.eoff[gb] = L.ecur[gb] = sa + ca;
+    if (lane == 63) L.eoff[Npad] = incl;
   }
   lds_barrier();
 #pragma unroll
@@ -540,66 +584,128 @@ __device__ __forceinline__ int lloyd_sort(const LloydLds& L, int Go, const uint3
       L.eg[pos] = (uint8_t)gv[u];
     }
   lds_barrier();
-  const int ne = L.eoff[Go];
-  if (tid < Go) L.ecnt[tid] = 0;
+  const int ne = L.eoff[Npad];
+  if (tid < Npad) L.ecnt[tid] = 0;
   return ne;
 }
 
-// Owner update of one round: the slice's records (from every rank) touching
-// this rank's groups, summed into S with count deltas in dcnt.
-__device__ void lloyd_apply_records(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go) {
+// The rows of X (the keys in the first round, the values for the
+// aggregation) of all the rank's keys added into the sums of their groups
+// (from bst), with the member counts if `counts`.
+__device__ void lloyd_sums_all(const uint16_t* X, const LloydArgs& a, const LloydLds& L, int64_t s, int k0, int nk,
+                               int Npad, bool counts) {
   const int tid = opaque_tid();
-  __shared__ int pre[17];
-  if (tid < 64) {  // the P record counts at once, then their prefix sums
-    const int c = tid < a.P ? min(max(ld_dev(a.rcnt + s * 16 + tid), 0), a.kpw) : 0;
-    int incl = c;
+  constexpr int PER = kLSort / kLT;
+  uint32_t ev[PER];
+  int gv[PER];
 #pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-      const int y = __shfl_up(incl, off);
-      if ((tid & 63) >= off) incl += y;
-    }
-    if (tid < a.P) pre[tid] = incl - c;
-    if (tid == a.P - 1) pre[a.P] = incl;
+  for (int u = 0; u < PER; ++u) {
+    const int i = tid + kLT * u;
+    ev[u] = (uint32_t)i;
+    gv[u] = i < nk ? (int)L.bst[i] : -1;
+    if (counts && gv[u] >= 0) atomicAdd(&L.dcA[gv[u]], 1);
   }
+  const int ne = lloyd_sort<PER>(L, Npad, ev, gv);
+  lloyd_run_sums(L, ne, X + (s * (int64_t)a.n + k0) * 64);
   lds_barrier();
-  const int total = pre[a.P];
-  const uint16_t* Kbh = a.K + s * (int64_t)a.n * 64;
-  constexpr int PER = kLSort / 2 / kLT;  // records per thread and pass (two entries each)
-  for (int c0 = 0; c0 < total; c0 += kLSort / 2) {
+}
+
+// Later rounds: the rows of the rank's certain keys that changed group (from
+// the bottom of ent) added into the sums, joins + and leaves -.
+__device__ void lloyd_sums_moved(const LloydArgs& a, const LloydLds& L, int64_t s, int k0, int nmov, int Npad) {
+  const int tid = opaque_tid();
+  constexpr int PER = kLSort / 2 / kLT;  // moved keys per thread and pass (two entries each)
+  for (int c0 = 0; c0 < nmov; c0 += kLSort / 2) {
     uint32_t ev[2 * PER];
     int gv[2 * PER];
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
-      const int e = c0 + tid + kLT * u;
+      const int i = c0 + tid + kLT * u;
       gv[2 * u] = gv[2 * u + 1] = -1;
       ev[2 * u] = ev[2 * u + 1] = 0u;
-      if (e < total) {
-        int q = 0;
-        while (q + 1 < a.P && e >= pre[q + 1]) ++q;
-        const uint32_t rc = ld_dev(a.rec + (s * a.P + q) * (int64_t)a.kpw + (e - pre[q]));
-        const uint32_t key = min(rc & 0xffffu, (uint32_t)a.n - 1u);
-        const int o = (int)((rc >> 16) & 255u), nw = (int)(rc >> 24);
-        if (nw < a.N && nw % a.P == r) {
-          gv[2 * u] = nw / a.P;
-          ev[2 * u] = key;
-        }
-        if (o < a.N && o % a.P == r) {
-          gv[2 * u + 1] = o / a.P;
-          ev[2 * u + 1] = key | 0x80000000u;
-        }
+      if (i < nmov) {
+        const uint32_t e = L.ent[i];
+        const int lk = (int)(e & 4095u), old = (int)((e >> 12) & 255u), nw = (int)(e >> 20);
+        gv[2 * u] = nw;
+        ev[2 * u] = (uint32_t)lk;
+        gv[2 * u + 1] = old;
+        ev[2 * u + 1] = (uint32_t)lk | 0x80000000u;
+        atomicAdd(&L.dcA[nw], 1);
+        atomicAdd(&L.dcA[old], -1);
       }
     }
-#pragma unroll
-    for (int u = 0; u < 2 * PER; ++u)
-      if (gv[u] >= 0) atomicAdd(&L.dcnt[gv[u]], (ev[u] >> 31) ? -1 : 1);
-    const int ne = lloyd_sort<2 * PER>(L, Go, ev, gv);
-    lloyd_run_sums(L.srt, L.eg, ne, Kbh, L.S);
+    const int ne = lloyd_sort<2 * PER>(L, Npad, ev, gv);
+    lloyd_run_sums(L, ne, a.K + (s * (int64_t)a.n + k0) * 64);
     lds_barrier();
   }
 }
 
-// Finish the rank's groups after an update: counts, C (an empty group keeps
-// C), R = bf16(C), |r|^2 and its split, published for the slice.
+// ------------------------------------------------------------ exchange
+// The rank's sums and count deltas for the groups it does not own go to its
+// slot of the exchange buffer, and are zeroed for the next round.
+__device__ void lloyd_publish(const LloydArgs& a, const LloydLds& L, int64_t s, int r) {
+  const int tid = opaque_tid();
+  const int Npad = (a.N + 31) & ~31;
+  double* xs = a.xs + (s * a.P + r) * (int64_t)Npad * 64;
+  int32_t* xc = a.xc + (s * a.P + r) * (int64_t)Npad;
+  for (int idx = tid; idx < a.N * 64; idx += kLT) {
+    const int g = idx >> 6, c = idx & 63;
+    if (g % a.P == r) continue;
+    double* p = L.SA + g * kLSA + c;
+    st_dev64(xs + idx, *p);
+    *p = 0.0;
+  }
+  for (int g = tid; g < a.N; g += kLT) {
+    if (g % a.P == r) continue;
+    st_dev(xc + g, L.dcA[g]);
+    L.dcA[g] = 0;
+  }
+}
+
+// After barrier A: the other ranks' sums (and count deltas) for the rank's
+// groups added into its exact sums (and counts).  Each thread loads its kLGU
+// items of one rank at once (one round trip per other rank).
+constexpr int kLGU = 128 * 64 / kLT;  // (group, position) items per thread, Go <= 128
+__device__ void lloyd_gather(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go, bool counts) {
+  const int tid = opaque_tid();
+  const int Npad = (a.N + 31) & ~31;
+  double add[kLGU];
+#pragma unroll
+  for (int u = 0; u < kLGU; ++u) add[u] = 0.0;
+  for (int q = 0; q < a.P; ++q) {
+    if (q == r) continue;
+    const double* xq = a.xs + (s * a.P + q) * (int64_t)Npad * 64;
+    double v[kLGU];
+#pragma unroll
+    for (int u = 0; u < kLGU; ++u) {
+      const int idx = tid + kLT * u, lg = idx >> 6, c = idx & 63;
+      const int g = min(r + a.P * min(lg, Go - 1), a.N - 1);  // clamped: every load is in bounds
+      v[u] = idx < Go * 64 ? ld_dev64(xq + g * 64 + c) : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < kLGU; ++u) add[u] += v[u];
+  }
+#pragma unroll
+  for (int u = 0; u < kLGU; ++u) {
+    const int idx = tid + kLT * u, lg = idx >> 6, c = idx & 63, g = r + a.P * lg;
+    if (lg < Go && g < a.N) L.SA[g * kLSA + c] += add[u];
+  }
+  if (!counts) return;
+  for (int lg = tid; lg < Go; lg += kLT) {
+    const int g = r + a.P * lg;
+    if (g >= a.N) continue;
+    int dc = L.dcA[g];
+    for (int q = 0; q < a.P; ++q)
+      if (q != r) dc += ld_dev(a.xc + (s * a.P + q) * (int64_t)Npad + g);
+    L.cnt[lg] += dc;
+    L.dcA[g] = 0;
+  }
+}
+
+// ------------------------------------------------------------ update
+// Finish the rank's groups after an update: C (an empty group keeps C),
+// R = bf16(C), |r|^2 and its split, published for the slice; the counts too
+// in the last round.
 //
 // The previous C of every item is loaded first, unconditionally: loads and
 // stores share one counter (vmcnt), and a load the compiler cannot track
@@ -614,15 +720,14 @@ __device__ void lloyd_apply_records(const LloydArgs& a, const LloydLds& L, int64
 // bits (one thread per row sums with 8 accumulators).  Rows outside that
 // range take the chain itself.
 constexpr int kLFinU = 128 * 32 / kLT;  // (group, feature pair) items per thread, Go <= 128
-constexpr int kLRowS = 36;              // LDS row stride (words) of the finished bf16 rows
 __device__ __forceinline__ int sq_exp(double x) {  // biased exponent of a square (0 for 0)
-  return (int)((__double_as_longlong(x) >> 52) & 0x7ff);
+  return (int)((__double_as_longlong(x) >> 52) & 2047);
 }
 __device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go, bool last) {
   const int tid = opaque_tid();
   float* Cbh = a.C + s * (int64_t)a.N * 64;
   uint32_t* Rw = (uint32_t*)(a.R + s * (int64_t)a.N * 64);
-  uint32_t* rows = L.srt;  // [Go][kLRowS] bf16 pairs (srt and eg are contiguous: 20 KB)
+  uint32_t* rows = L.X;  // [Go][kLRowS] bf16 pairs
   float2 prev[kLFinU];
 #pragma unroll
   for (int u = 0; u < kLFinU; ++u) {
@@ -630,11 +735,6 @@ __device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, i
     const int g = min(r + a.P * min(lg, Go - 1), a.N - 1);
     prev[u] = *(const float2*)(Cbh + g * 64 + 2 * c2);
   }
-  for (int lg = tid; lg < Go; lg += kLT) {
-    L.cnt[lg] += L.dcnt[lg];
-    L.dcnt[lg] = 0;
-  }
-  lds_barrier();
 #pragma unroll
   for (int u = 0; u < kLFinU; ++u) {
     const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31, g = r + a.P * lg;
@@ -642,8 +742,8 @@ __device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, i
     const int cnt = L.cnt[lg];
     float c0 = prev[u].x, c1 = prev[u].y;
     if (cnt > 0) {
-      c0 = (float)(L.S[lg * 64 + 2 * c2] / (double)cnt);
-      c1 = (float)(L.S[lg * 64 + 2 * c2 + 1] / (double)cnt);
+      c0 = (float)(L.SA[g * kLSA + lloyd_pi(2 * c2)] / (double)cnt);
+      c1 = (float)(L.SA[g * kLSA + lloyd_pi(2 * c2 + 1)] / (double)cnt);
     }
     prev[u] = float2{c0, c1};
     rows[lg * kLRowS + c2] = f32_to_bf16(c0) | (f32_to_bf16(c1) << 16);
@@ -703,39 +803,18 @@ __device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, i
   lds_barrier();
 }
 
-// Value sums of the rank's groups after the last round (Algorithm 1,
-// aggregation): every key of the slice whose final group the rank owns adds
-// its value row into S (reused, zeroed first); then the outputs.
-__device__ void lloyd_values(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go) {
+// ------------------------------------------------------------ aggregation
+// Outputs of the aggregation for the rank's groups (and the attention's padded
+// groups up to a multiple of 32): vsum = (float) of the exact sum, the bf16
+// means transposed (Vt) and the score bias log2(count) / (|scale| log2 e).
+__device__ void lloyd_value_outputs(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go) {
   const int tid = opaque_tid();
-  for (int i = tid; i < Go * 64; i += kLT) L.S[i] = 0.0;
-  lds_barrier();
-  const uint16_t* Vbh = a.V + s * (int64_t)a.n * 64;
-  const int32_t* bel = a.belong + s * (int64_t)a.n;
-  constexpr int PER = kLSort / kLT;
-  for (int c0 = 0; c0 < a.n; c0 += kLSort) {
-    uint32_t ev[PER];
-    int gv[PER];
-#pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int e = c0 + tid + kLT * u;
-      gv[u] = -1;
-      ev[u] = (uint32_t)e;
-      if (e < a.n) {
-        const int g = ld_dev(bel + e);
-        if ((unsigned)g < (unsigned)a.N && g % a.P == r) gv[u] = g / a.P;
-      }
-    }
-    const int ne = lloyd_sort<PER>(L, Go, ev, gv);
-    lloyd_run_sums(L.srt, L.eg, ne, Vbh, L.S);
-    lds_barrier();
-  }
-  const int NpA = (a.N + 31) & ~31;  // the attention's padded group count
+  const int NpA = (a.N + 31) & ~31;
   for (int idx = tid; idx < Go * 64; idx += kLT) {
     const int lg = idx >> 6, c = idx & 63, g = r + a.P * lg;
     if (g >= NpA) continue;
     const bool real = g < a.N;
-    const float vs = real ? (float)L.S[lg * 64 + c] : 0.f;
+    const float vs = real ? (float)L.SA[g * kLSA + lloyd_pi(c)] : 0.f;
     const int cnt = real ? L.cnt[lg] : 0;
     if (a.vsum && real) a.vsum[(s * a.N + g) * 64 + c] = vs;
     if (a.Vt) {
@@ -745,11 +824,11 @@ __device__ void lloyd_values(const LloydArgs& a, const LloydLds& L, int64_t s, i
   }
 }
 
-// ------------------------------------------------------------ the kernel
+// ------------------------------------------------------------ kernel
 template <int NB>
 __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ int s_nmov, s_nunc, s_flag;
+  __shared__ int s_nmov, s_nunc, s_xmov, s_flag;
   __shared__ double s_red[kLW];
   constexpr int Npad = NB * 32;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -758,22 +837,23 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
   const int r = idx % a.P;
   if (s >= a.BH) return;
   const int Go = lloyd_go(Npad, a.P);
-  const LloydLds L = lloyd_layout(smem, Npad, Go);
+  const LloydLds L = lloyd_layout(smem, Npad, a.P);
   const int k0 = r * a.kpw, nk = max(0, min(a.kpw, a.n - k0));
   uint32_t* ctr = a.sync + s * 32;
   int bar = 0;
 
   lloyd_stage_init(a, L, Npad, s, r);
-  for (int i = tid; i < Go * 64; i += kLT) L.S[i] = 0.0;
-  for (int i = tid; i < Go; i += kLT) {
-    L.cnt[i] = 0;
-    L.dcnt[i] = 0;
+  for (int i = tid; i < Npad * kLSA; i += kLT) L.SA[i] = 0.0;
+  for (int i = tid; i < Npad; i += kLT) {
+    L.dcA[i] = 0;
     L.ecnt[i] = 0;
   }
+  for (int i = tid; i < Go; i += kLT) L.cnt[i] = 0;
   lds_barrier();
 
   for (int t = 0; t < a.T; ++t) {
-    const bool first = t == 0, last = t == a.T - 1;
+    const bool first = t == 0;
+    bool last = t == a.T - 1;
     // certification constants from the largest |r|^2 of the slice
     double mx = 0.0;
     for (int g = tid; g < a.N; g += kLT) mx = fmax(mx, L.nrm[g]);
@@ -783,48 +863,62 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
     if (tid == 0) {
       s_nmov = 0;
       s_nunc = 0;
+      s_xmov = 0;
     }
     lds_barrier();
     double nmax = s_red[0];
 #pragma unroll
     for (int w = 1; w < kLW; ++w) nmax = fmax(nmax, s_red[w]);
     const float nmaxf = (float)nmax * (1.0f + 0x1p-20f);
-    const Certify cf = {nmaxf, sqrtf(nmaxf) * (1.0f + 0x1p-20f), a.cm, a.cp};
+    const LloydCert cf = lloyd_cert(nmaxf, sqrtf(nmaxf) * (1.0f + 0x1p-20f), a.cm, a.cp);
 
-    // 1. assignment of the rank's keys
-    lloyd_assign<NB>(a, L, s, k0, nk, first, cf, &s_nmov, &s_nunc);
+    // 1. assignment of the rank's keys and the sums of those that changed group
+    lloyd_assign<NB>(a, L, s, k0, nk, first, (t & 1) != 0, cf, &s_nmov, &s_nunc);
     lds_barrier();
     const int nunc = s_nunc;
     if (nunc) {
-      lloyd_exact(a, L, s, k0, nunc);
-      lds_barrier();
-      lloyd_exact_records(L, nunc, &s_nmov);
+      lloyd_exact(a, L, s, k0, nunc, first, &s_xmov);
       lds_barrier();
     }
-    // records of the keys whose group changed (every key in the first round)
     const int nmov = s_nmov;
-    uint32_t* recr = a.rec + (s * a.P + r) * (int64_t)a.kpw;
-    for (int i = tid; i < nmov; i += kLT) {
-      const uint32_t e = L.ent[i];
-      st_dev(recr + i, (uint32_t)(k0 + (int)(e & 4095u)) | (((e >> 12) & 255u) << 16) | ((e >> 20) << 24));
-    }
-    if (tid == 0) st_dev(a.rcnt + s * 16 + r, nmov);
-    if (last)
-      for (int i = tid; i < nk; i += kLT) st_dev(a.belong + s * (int64_t)a.n + k0 + i, (int32_t)L.bst[i]);
-    // 2. barrier A
+    if (first)  // every key joins its group
+      lloyd_sums_all(a.K, a, L, s, k0, nk, Npad, true);
+    else if (nmov)
+      lloyd_sums_moved(a, L, s, k0, nmov, Npad);
+    // 2. the deltas of the other ranks' groups, then barrier A
+    lloyd_publish(a, L, s, r);
+    if (tid == 0) st_dev(a.xm + s * 16 + r, first ? nk : nmov + s_xmov);
     if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
-    // 3. update of the rank's groups
-    lloyd_apply_records(a, L, s, r, Go);
-    lloyd_finish(a, L, s, r, Go, last);
-    if (last) {
-      if (a.V) lloyd_values(a, L, s, r, Go);
-      break;
+    // 3. update of the rank's groups; a round in which no key of the slice
+    // changed group is a fixed point, so it is the last
+    if (!first && !last) {
+      int moved = 0;
+      for (int q = 0; q < a.P; ++q) moved += ld_dev(a.xm + s * 16 + q);
+      last = moved == 0;
     }
+    lloyd_gather(a, L, s, r, Go, true);
+    lds_barrier();
+    lloyd_finish(a, L, s, r, Go, last);
+    if (last) break;
     // 4. barrier B, then the slice's new representatives
     if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
     lloyd_read_reps(a, L, s);
     lds_barrier();
   }
+  // the groups of the rank's keys
+  for (int i = tid; i < nk; i += kLT) a.belong[s * (int64_t)a.n + k0 + i] = (int32_t)L.bst[i];
+  if (!a.V) return;
+  // aggregation: value sums of the rank's keys per group, exchanged like the
+  // key sums (barrier B first: every rank has read the last round's deltas)
+  for (int i = tid; i < Npad * kLSA; i += kLT) L.SA[i] = 0.0;
+  lds_barrier();
+  lloyd_sums_all(a.V, a, L, s, k0, nk, Npad, false);
+  if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
+  lloyd_publish(a, L, s, r);
+  if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
+  lloyd_gather(a, L, s, r, Go, false);
+  lds_barrier();
+  lloyd_value_outputs(a, L, s, r, Go);
 }
 
 // Clears the barrier counters and marks the status word as belonging to a
@@ -847,6 +941,15 @@ namespace {
 
 using LloydFn = void (*)(LloydArgs);
 const LloydFn kLloydFns[4] = {k_lloyd<1>, k_lloyd<2>, k_lloyd<3>, k_lloyd<4>};
+
+// Most ranks per slice: about one per 256 keys, at most 16, and at most
+// kLMaxWG workgroups in the launch (this also bounds the exchange buffer,
+// whose size must not depend on the device).
+int lloyd_pcap(const Dims& d) {
+  const int64_t bh8x8 = (std::max<int64_t>(d.BH, 1) + 7) / 8 * 8;
+  const int64_t p = std::min<int64_t>(std::min<int64_t>(16, ((int64_t)d.n + 255) / 256), kLMaxWG / bh8x8);
+  return (int)std::max<int64_t>(1, p);
+}
 
 // Compute units of the current device and the workgroups of `fn` (512
 // threads, `lds` bytes of dynamic LDS) each holds at once; cached.
@@ -885,7 +988,7 @@ LloydPlan plan_lloyd(const Dims& d) {
   const int64_t bh8 = (d.BH + 7) / 8;
   // ranks per slice: about one per 256 keys, at most 16, and every workgroup
   // of the launch resident at once
-  int P = (int)std::min<int64_t>(16, std::max<int64_t>(1, ((int64_t)d.n + 255) / 256));
+  int P = lloyd_pcap(d);
   for (; P >= 1; --P) {
     const size_t lds = lloyd_lds_bytes(Npad, P);
     const auto cap = lloyd_capacity(p.nb, lds);
@@ -905,7 +1008,9 @@ LloydPlan plan_lloyd(const Dims& d) {
 
 }  // namespace
 
-size_t lloyd_records(const Dims& d) { return (size_t)d.BH * ((size_t)d.n + 32 * 16); }
+size_t lloyd_exchange_rows(const Dims& d) {
+  return (size_t)d.BH * (size_t)lloyd_pcap(d) * (size_t)((d.N + 31) & ~31);
+}
 
 bool lloyd_usable(const Dims& d) { return plan_lloyd(d).ok; }
 
@@ -948,8 +1053,9 @@ hipError_t launch_lloyd(const Dims& d, const void* K, const void* V, const float
   a.R = (uint16_t*)w.R;
   a.nsplit = w.nsplit;
   a.nrm64 = w.nrm64;
-  a.rec = w.lrec;
-  a.rcnt = w.lrcnt;
+  a.xs = w.lxs;
+  a.xc = w.lxc;
+  a.xm = w.lxm;
   a.sync = w.lsync;
   a.status = w.lstatus;
   a.vsum = vsum;

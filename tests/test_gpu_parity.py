@@ -110,6 +110,27 @@ def test_cluster_bit_exact(oracle_mod, dev, case, path):
     assert_groups_equal(got, ref)
 
 
+def test_cluster_fixed_point_ends_early(oracle_mod, dev, path):
+    """Well separated clusters reach a fixed point (no key changes group) in
+    round 5 or 6 of 12 (each slice its own); the persistent kernel stops a
+    slice there.
+    Groups, counts, centroids and the forward's output must still equal the
+    oracle's 12 full rounds."""
+    say(f"cluster: fixed point before the last round ({path})")
+    Q, K, V = inputs.make_qkv(1, 3, 2500, 64, "bf16", 79, 32, 0.01, 0.01)
+    got, ref = cluster_both(oracle_mod, K, 32, 12, "bf16", dev, trace=True)
+    tb = ref["trace_belong"]  # [iters, B, H, n]
+    for h in range(3):
+        same = [bool(np.array_equal(tb[t, 0, h], tb[t - 1, 0, h])) for t in range(1, 12)]
+        assert any(same[:9]), f"slice {h} reaches no fixed point before round 10: the case does not test the exit"
+    assert_groups_equal(got, ref)
+    O, bel, cnt, cen = ga.forward(Q.to(dev), K.to(dev), V.to(dev), 32, 12, 0.125, return_groups=True)
+    torch.cuda.synchronize()
+    fref = oracle_mod.forward(f64(Q), f64(K), f64(V), 32, 12, 0.125, "bf16")
+    assert_groups_equal((bel.cpu().numpy(), cnt.cpu().numpy(), cen.cpu().numpy()), fref)
+    check_close(O, fref["O"], TOL["bf16"])
+
+
 def test_cluster_with_caller_init(oracle_mod, dev):
     say("cluster with caller init")
     _, K, _ = inputs.make_qkv(2, 1, 700, 64, "bf16", 5, 40, 0.05, 0.3)
