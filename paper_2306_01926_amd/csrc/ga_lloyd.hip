@@ -707,10 +707,11 @@ __device__ void lloyd_gather(const LloydArgs& a, const LloydLds& L, int64_t s, i
 // R = bf16(C), |r|^2 and its split, published for the slice; the counts too
 // in the last round.
 //
-// The previous C of every item is loaded first, unconditionally: loads and
-// stores share one counter (vmcnt), and a load the compiler cannot track
-// (e.g. a conditional one) makes it wait for every earlier store, including
-// the slow device-scope ones, before each later use.
+// The previous C of every item (prev) is loaded before barrier A,
+// unconditionally: its round trip overlaps the wait, and loads and stores
+// share one counter (vmcnt): a load the compiler cannot track (e.g. a
+// conditional one) would make it wait for every earlier store, including the
+// slow device-scope ones, before each later use.
 //
 // |r|^2: the canonical value is the fp64 fma chain over c = 0..63.  Each
 // square of a bf16 component is exact in fp64 (16 significant bits); if the
@@ -723,18 +724,25 @@ constexpr int kLFinU = 128 * 32 / kLT;  // (group, feature pair) items per threa
 __device__ __forceinline__ int sq_exp(double x) {  // biased exponent of a square (0 for 0)
   return (int)((__double_as_longlong(x) >> 52) & 2047);
 }
-__device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go, bool last) {
+// The previous C of the rank's groups, (group, feature pair) items
+// tid + kLT u (clamped loads: every address is in bounds).
+__device__ __forceinline__ void lloyd_prev_c(const LloydArgs& a, int64_t s, int r, int Go, float2 (&prev)[kLFinU]) {
   const int tid = opaque_tid();
-  float* Cbh = a.C + s * (int64_t)a.N * 64;
-  uint32_t* Rw = (uint32_t*)(a.R + s * (int64_t)a.N * 64);
-  uint32_t* rows = L.X;  // [Go][kLRowS] bf16 pairs
-  float2 prev[kLFinU];
+  const float* Cbh = a.C + s * (int64_t)a.N * 64;
 #pragma unroll
   for (int u = 0; u < kLFinU; ++u) {
     const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31;
     const int g = min(r + a.P * min(lg, Go - 1), a.N - 1);
     prev[u] = *(const float2*)(Cbh + g * 64 + 2 * c2);
   }
+}
+
+__device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go, bool last,
+                             float2 (&prev)[kLFinU]) {
+  const int tid = opaque_tid();
+  float* Cbh = a.C + s * (int64_t)a.N * 64;
+  uint32_t* Rw = (uint32_t*)(a.R + s * (int64_t)a.N * 64);
+  uint32_t* rows = L.X;  // [Go][kLRowS] bf16 pairs
 #pragma unroll
   for (int u = 0; u < kLFinU; ++u) {
     const int idx = tid + kLT * u, lg = idx >> 5, c2 = idx & 31, g = r + a.P * lg;
@@ -888,6 +896,8 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
     // 2. the deltas of the other ranks' groups, then barrier A
     lloyd_publish(a, L, s, r);
     if (tid == 0) st_dev(a.xm + s * 16 + r, first ? nk : nmov + s_xmov);
+    float2 prev[kLFinU];
+    lloyd_prev_c(a, s, r, Go, prev);
     if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
     // 3. update of the rank's groups; a round in which no key of the slice
     // changed group is a fixed point, so it is the last
@@ -898,7 +908,7 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
     }
     lloyd_gather(a, L, s, r, Go, true);
     lds_barrier();
-    lloyd_finish(a, L, s, r, Go, last);
+    lloyd_finish(a, L, s, r, Go, last, prev);
     if (last) break;
     // 4. barrier B, then the slice's new representatives
     if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
