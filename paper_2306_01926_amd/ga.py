@@ -13,7 +13,8 @@ import os
 
 import torch
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libga.so")
+# GA_LIB lets the sanitizer test load an instrumented build of the same sources.
+_LIB_PATH = os.environ.get("GA_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libga.so")
 
 GA_F32, GA_BF16 = 0, 1
 STATUS = {0: "GA_OK", 1: "GA_ERR_INVALID_ARG", 2: "GA_ERR_UNSUPPORTED", 3: "GA_ERR_WORKSPACE", 4: "GA_ERR_HIP"}

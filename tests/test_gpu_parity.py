@@ -344,10 +344,12 @@ def test_forward_single_round(oracle_mod, dev):
     check_close(O, ref["O"], TOL["bf16"])
 
 
-def test_concurrent_forwards_separate_workspaces(dev):
-    """Two forwards overlapping on two streams, each with its own workspace,
+@pytest.mark.parametrize("explicit_ws", [True, False], ids=["ws", "cached-ws"])
+def test_concurrent_forwards_separate_workspaces(dev, explicit_ws):
+    """Two forwards overlapping on two streams, each with its own workspace
+    (given, or the binding's cached one, which is kept per device and stream),
     give the results of the same forwards run one after the other."""
-    say("concurrent forwards on two streams")
+    say(f"concurrent forwards on two streams (explicit workspaces: {explicit_ws})")
     args = [(inputs.make_qkv(2, 2, 2500, 64, "bf16", s, 128, 0.05, 0.3), N) for s, N in ((31, 128), (32, 100))]
     args = [(tuple(t.to(dev) for t in qkv), N) for qkv, N in args]
     seq = [ga.forward(*qkv, N, 5, return_groups=True) for qkv, N in args]
@@ -360,7 +362,7 @@ def test_concurrent_forwards_separate_workspaces(dev):
         for i, ((qkv, N), s) in enumerate(zip(args, streams)):
             s.wait_stream(torch.cuda.current_stream(dev))
             with torch.cuda.stream(s):
-                outs[i] = ga.forward(*qkv, N, 5, return_groups=True, ws=wss[i])
+                outs[i] = ga.forward(*qkv, N, 5, return_groups=True, ws=wss[i] if explicit_ws else None)
         torch.cuda.synchronize()
         for a, b in zip(seq, outs):
             for x, y in zip(a, b):
@@ -401,6 +403,15 @@ def test_full_size_n8000_sampled_slices(oracle_mod, dev):
     w = inputs.WORKLOADS["n8000_N128_bf16"]
     say(f"full size {w.name}, sampled slices")
     _sampled_full_size(oracle_mod, dev, w, 0, w.N, [(0, 0), (7, 3), (15, 7)])
+
+
+@pytest.mark.parametrize("N", [32, 64])
+def test_full_size_n20000_small_group_counts(oracle_mod, dev, N):
+    """The two smaller group counts of the n = 20000 workload (the draws of
+    the varying-N test give 256 and 128) at full size."""
+    w = inputs.WORKLOADS["n20000_Nvar_bf16"]
+    say(f"full size {w.name}, N={N}")
+    _sampled_full_size(oracle_mod, dev, w, 2 + N, N, [(1, 2), (2, 5)], queries=256)
 
 
 def test_full_size_n20000_varying_groups(oracle_mod, dev):
