@@ -663,41 +663,47 @@ __device__ void lloyd_publish(const LloydArgs& a, const LloydLds& L, int64_t s, 
 }
 
 // After barrier A: the other ranks' sums (and count deltas) for the rank's
-// groups added into its exact sums (and counts).  Each thread loads its kLGU
-// items of one rank at once (one round trip per other rank).
-constexpr int kLGU = 128 * 64 / kLT;  // (group, position) items per thread, Go <= 128
+// groups added into its exact sums (and counts).  The thread's (item, other
+// rank) pairs are loaded kLGB at a time, all of a batch before any is added,
+// so that a slice with few ranks needs one round trip.
+constexpr int kLGB = 16;  // loads in flight per thread
 __device__ void lloyd_gather(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go, bool counts) {
   const int tid = opaque_tid();
   const int Npad = (a.N + 31) & ~31;
-  double add[kLGU];
+  const int U = (Go * 64 + kLT - 1) / kLT;  // items of this thread (some past Go * 64)
+  const int pairs = U * (a.P - 1);
+  const double* xs = a.xs + s * a.P * (int64_t)Npad * 64;
+  int u = 0, q0 = 0;  // pair p = q0 U + u: item u of other rank q0 (ranks past r shifted by one)
+  for (int p0 = 0; p0 < pairs; p0 += kLGB) {
+    double v[kLGB];
+    int at[kLGB];  // LDS position of the item, -1 past the end (the items are the thread's own: no atomics)
 #pragma unroll
-  for (int u = 0; u < kLGU; ++u) add[u] = 0.0;
-  for (int q = 0; q < a.P; ++q) {
-    if (q == r) continue;
-    const double* xq = a.xs + (s * a.P + q) * (int64_t)Npad * 64;
-    double v[kLGU];
-#pragma unroll
-    for (int u = 0; u < kLGU; ++u) {
+    for (int b = 0; b < kLGB; ++b) {
+      const int q = min(q0 + (q0 >= r), a.P - 1);
       const int idx = tid + kLT * u, lg = idx >> 6, c = idx & 63;
       const int g = min(r + a.P * min(lg, Go - 1), a.N - 1);  // clamped: every load is in bounds
-      v[u] = idx < Go * 64 ? ld_dev64(xq + g * 64 + c) : 0.0;
+      at[b] = p0 + b < pairs && lg < Go && r + a.P * lg < a.N ? g * kLSA + c : -1;
+      v[b] = at[b] >= 0 ? ld_dev64(xs + ((int64_t)q * Npad + g) * 64 + c) : 0.0;
+      if (++u == U) {
+        u = 0;
+        ++q0;
+      }
     }
 #pragma unroll
-    for (int u = 0; u < kLGU; ++u) add[u] += v[u];
-  }
-#pragma unroll
-  for (int u = 0; u < kLGU; ++u) {
-    const int idx = tid + kLT * u, lg = idx >> 6, c = idx & 63, g = r + a.P * lg;
-    if (lg < Go && g < a.N) L.SA[g * kLSA + c] += add[u];
+    for (int b = 0; b < kLGB; ++b)
+      if (at[b] >= 0) L.SA[at[b]] += v[b];
   }
   if (!counts) return;
+  // count deltas: one (group, other rank) pair per thread, added with LDS atomics
+  for (int pr = tid; pr < Go * (a.P - 1); pr += kLT) {
+    const int lg = pr % Go, q0 = pr / Go, q = q0 + (q0 >= r), g = r + a.P * lg;
+    if (g < a.N) atomicAdd(&L.dcA[g], ld_dev(a.xc + (s * a.P + q) * (int64_t)Npad + g));
+  }
+  lds_barrier();
   for (int lg = tid; lg < Go; lg += kLT) {
     const int g = r + a.P * lg;
     if (g >= a.N) continue;
-    int dc = L.dcA[g];
-    for (int q = 0; q < a.P; ++q)
-      if (q != r) dc += ld_dev(a.xc + (s * a.P + q) * (int64_t)Npad + g);
-    L.cnt[lg] += dc;
+    L.cnt[lg] += L.dcA[g];
     L.dcA[g] = 0;
   }
 }
