@@ -611,9 +611,45 @@ __device__ void lloyd_sums_all(const uint16_t* X, const LloydArgs& a, const Lloy
 }
 
 // Later rounds: the rows of the rank's certain keys that changed group (from
-// the bottom of ent) added into the sums, joins + and leaves -.
+// the bottom of ent) added into the sums, joins + and leaves -.  Up to kLDirect
+// keys go straight to LDS atomics (eight lanes per row, every row loaded
+// before any is added: one round trip, no sort); more are sorted by group and
+// summed in registers first.
+constexpr int kLPU = 4;                    // rows per lane group in the direct path
+constexpr int kLDirect = kLW * 8 * kLPU;  // moved keys the direct path takes
 __device__ void lloyd_sums_moved(const LloydArgs& a, const LloydLds& L, int64_t s, int k0, int nmov, int Npad) {
   const int tid = opaque_tid();
+  if (nmov <= kLDirect) {
+    const int lane = tid & 63, wave = tid >> 6, j = lane & 7, sub = lane >> 3;
+    const uint16_t* Kr = a.K + (s * (int64_t)a.n + k0) * 64;
+    uint32_t e[kLPU];
+    u32x4 w[kLPU];
+#pragma unroll
+    for (int u = 0; u < kLPU; ++u) {
+      const int i = min(wave * 8 * kLPU + 8 * u + sub, nmov - 1);  // clamped: in the list, rows in bounds
+      e[u] = L.ent[i];
+      w[u] = *(const u32x4*)(Kr + (int64_t)(e[u] & 4095u) * 64 + 8 * j);
+    }
+#pragma unroll
+    for (int u = 0; u < kLPU; ++u) {
+      if (wave * 8 * kLPU + 8 * u + sub >= nmov) break;
+      const int old = (int)((e[u] >> 12) & 255u), nw = (int)(e[u] >> 20);
+      double* pn = L.SA + nw * kLSA + j;
+      double* po = L.SA + old * kLSA + j;
+#pragma unroll
+      for (int f = 0; f < 8; ++f) {  // feature 8 j + f at position 8 f + j
+        const double x = (double)bf16_to_f32((w[u][f >> 1] >> (16 * (f & 1))) & 0xffffu);
+        atomicAdd(pn + 8 * f, x);
+        atomicAdd(po + 8 * f, -x);
+      }
+      if (j == 0) {
+        atomicAdd(&L.dcA[nw], 1);
+        atomicAdd(&L.dcA[old], -1);
+      }
+    }
+    lds_barrier();
+    return;
+  }
   constexpr int PER = kLSort / 2 / kLT;  // moved keys per thread and pass (two entries each)
   for (int c0 = 0; c0 < nmov; c0 += kLSort / 2) {
     uint32_t ev[2 * PER];
@@ -724,8 +760,8 @@ __device__ void lloyd_gather(const LloydArgs& a, const LloydLds& L, int64_t s, i
 // nonzero squares of a row span at most 31 binades, every partial sum in any
 // order is a multiple of the smallest square's last bit and below 2^53 of it,
 // so every partial sum is exact and any summation order gives the chain's
-// bits (one thread per row sums with 8 accumulators).  Rows outside that
-// range take the chain itself.
+// bits (eight lanes per row sum eight squares each, then a shuffle tree).
+// Rows outside that range take the chain itself.
 constexpr int kLFinU = 128 * 32 / kLT;  // (group, feature pair) items per thread, Go <= 128
 __device__ __forceinline__ int sq_exp(double x) {  // biased exponent of a square (0 for 0)
   return (int)((__double_as_longlong(x) >> 52) & 2047);
@@ -763,40 +799,43 @@ __device__ void lloyd_finish(const LloydArgs& a, const LloydLds& L, int64_t s, i
     rows[lg * kLRowS + c2] = f32_to_bf16(c0) | (f32_to_bf16(c1) << 16);
   }
   lds_barrier();
-  // per group (one thread): |r|^2, its split, the count
-  for (int lg = tid; lg < Go; lg += kLT) {
-    const int g = r + a.P * lg;
-    if (g >= a.N) continue;
-    u32x4 w[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) w[k] = *(const u32x4*)(rows + lg * kLRowS + 4 * k);
-    double acc[8];
+  // per group (eight lanes, eight features each): |r|^2, its split, the count
+  for (int base = 0; base < Go * 8; base += kLT) {
+    const int t = base + tid, lg = t >> 3, j = t & 7, g = r + a.P * lg;
+    const bool ok = lg < Go && g < a.N;
+    const u32x4 w = ok ? *(const u32x4*)(rows + lg * kLRowS + 4 * j) : u32x4{0u, 0u, 0u, 0u};
+    double acc = 0.0;
     int emax = 0, emin = 4096;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      acc[k] = 0.0;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t bits = (e & 1) ? (w[k][e >> 1] >> 16) : (w[k][e >> 1] & 0xffffu);
-        const double rc = (double)bf16_to_f32(bits);
-        const double q = rc * rc;  // exact
-        acc[k] += q;
-        if (q != 0.0) {
-          emax = max(emax, sq_exp(q));
-          emin = min(emin, sq_exp(q));
-        }
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t bits = (e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu);
+      const double rc = (double)bf16_to_f32(bits);
+      const double q = rc * rc;  // exact
+      acc += q;
+      if (q != 0.0) {
+        emax = max(emax, sq_exp(q));
+        emin = min(emin, sq_exp(q));
       }
     }
-    double nrm = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
+#pragma unroll
+    for (int off = 1; off < 8; off <<= 1) {  // the group's eight lanes are consecutive lanes of one wave
+      acc += __shfl_xor(acc, off);
+      emax = max(emax, __shfl_xor(emax, off));
+      emin = min(emin, __shfl_xor(emin, off));
+    }
+    if (!ok || j != 0) continue;
+    double nrm = acc;
     if (emin != 4096 && emax - emin > 31) {  // not provably exact: the chain itself
       nrm = 0.0;
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
+      for (int k = 0; k < 8; ++k) {
+        const u32x4 wk = *(const u32x4*)(rows + lg * kLRowS + 4 * k);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const double rc = (double)bf16_to_f32((e & 1) ? (w[k][e >> 1] >> 16) : (w[k][e >> 1] & 0xffffu));
+          const double rc = (double)bf16_to_f32((e & 1) ? (wk[e >> 1] >> 16) : (wk[e >> 1] & 0xffffu));
           nrm = fma(rc, rc, nrm);
         }
+      }
     }
     uint16_t sp[8];
     write_nsplit(nrm, sp);
