@@ -20,11 +20,16 @@ def hipcc() -> str:
     return shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 
 
+# Device-code flags of every source: packed FP32 instructions off; MFMA results
+# in ordinary VGPRs (the fused backward kernel places its long-lived
+# accumulators in AGPRs explicitly).
+DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17",
+                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-mfma-vgpr-form", "-I", os.path.join(ROOT, "include")]
+
+
 def build(verbose: bool = False) -> str:
-    cmd = [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-mllvm", "-amdgpu-mfma-vgpr-form",
-           "-I", os.path.join(ROOT, "include"), *SOURCES, "-o", LIB + ".tmp"]
+    cmd = [hipcc(), *DEVICE_FLAGS, "-fPIC", "-shared", *SOURCES, "-o", LIB + ".tmp"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + r.stderr[-6000:])

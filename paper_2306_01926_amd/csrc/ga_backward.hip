@@ -15,21 +15,32 @@
 //   dr_j = scale sum_i dp_ij q_i  ->  dK_k = dr_{a_k} / c_{a_k},
 //   dmu_j = sum_i w_ij G_i        ->  dV_k = dmu_{a_k} / c_{a_k}.
 //
-// Kernels (N <= 256, padded to Npad = 32 NB groups):
+// Kernels (N <= 256, padded to Npad = 32 NB groups).  N <= 128:
+//   k_bwd_fused   per (slice, query chunk), one wave per SIMD: the slice's
+//                 group rows staged from the fp32 centroids and sums; per
+//                 32-query tile (lane = query) MFMA scores, the group softmax,
+//                 MFMA dw, D, dp, MFMA dQ; w and dp handed through LDS (read
+//                 back transposed, lane = group) to the MFMA reductions
+//                 dr += dp Q and dmu += w G, whose sums for every group stay
+//                 in accumulation registers over the chunk; the four waves'
+//                 sums added in a fixed order
+// N > 128 (every group's sums do not fit in registers):
 //   k_bwd_prep    per slice: R = bf16(centroid) rows and transposed, bf16
 //                 value means, log2(count) (-inf for an empty group)
-//   k_bwd_query   per 32-query tile (lane = query): MFMA scores, the group
-//                 softmax, MFMA dw, D, dp, MFMA dQ; stores each query's
-//                 softmax shift plus log2 of its sum (so that a weight is one
-//                 exp2) and D (N > 128: three passes over the 32-group blocks
-//                 instead of all scores in registers)
+//   k_bwd_query   per 32-query tile (lane = query): the query side as above
+//                 in three passes over the 32-group blocks (shift; sum and
+//                 D; dp and dQ), recomputing the block's MFMAs; stores each
+//                 query's softmax shift plus log2 of its sum (so that a
+//                 weight is one exp2) and D
 //   k_bwd_group   per (32-group block, query chunk): the same scores and dw
 //                 in the transposed layout (lane = group), so that the dp and
 //                 w registers are directly the A operand of the MFMA
-//                 reductions dr += dp Q and dmu += w G; the four waves'
-//                 partials are added in a fixed order ((w0 + w2) + (w1 + w3))
+//                 reductions; the four waves' partials are added in a fixed
+//                 order ((w0 + w2) + (w1 + w3))
+// Both:
 //   k_bwd_finish  per group: the chunk partials added in a fixed order,
-//                 scaled: scale dr / c and dmu / c, as bf16 rows
+//                 scaled: scale dr / c and dmu / c, as bf16 rows (skipped
+//                 with one chunk per slice: the chunk's kernel forms them)
 //   k_bwd_keys    per key: the rows of its group to dK, dV (bf16)
 // Every reduction has a fixed order, so repeated calls give identical bits.
 #include <hip/hip_runtime.h>
@@ -47,6 +58,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kBs = 72;       // LDS row stride (bf16) of group rows and wave tiles
 // Query chunks per slice in k_bwd_group: as few as give about kBwdTargetWgs
@@ -64,7 +77,10 @@ int bwd_chunks(int64_t BH, int NB) {
 __device__ __forceinline__ uint32_t bf16_bits(float x) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x);  // round to nearest even
 }
-__device__ __forceinline__ uint32_t pack2(float lo, float hi) { return bf16_bits(lo) | (bf16_bits(hi) << 16); }
+// two values rounded to bf16 (nearest even) in one v_cvt_pk_bf16_f32
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
 __device__ __forceinline__ f32x16 mfma(const u32x4& a, const u32x4& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
                                                  0, 0);
@@ -230,65 +246,7 @@ __global__ __launch_bounds__(256) void k_bwd_query(const uint16_t* __restrict__ 
       }
     };
     float Ms_, inv, Dq, Lq;  // Lq: the shift plus log2 of the sum (+inf if every group is empty)
-    if constexpr (NB <= 4) {
-      // all blocks' weights held in registers; each block's dw is formed
-      // twice (for D, then for dp) rather than held
-      f32x16 x[NB];
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        x[b] = zero16();
-        const uint16_t* rr = Rs + (32 * b + q) * kBs + 32 * h;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) x[b] = mfma(*(const u32x4*)(rr + 8 * s), qf[s], x[b]);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) x[b][v] = fmaf(x[b][v], sl2e, lc[32 * b + 8 * (v >> 2) + 4 * h + (v & 3)]);
-      }
-      auto dw_block = [&](int b) __attribute__((always_inline)) {
-        f32x16 d = zero16();
-        const uint16_t* mr = Ms + (32 * b + q) * kBs + 32 * h;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) d = mfma(*(const u32x4*)(mr + 8 * s), gf[s], d);
-        return d;
-      };
-      float M = -INFINITY;
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) M = fmaxf(M, x[b][v]);
-      M = fmaxf(M, __shfl_xor(M, 32));
-      const bool any = M != -INFINITY;  // some group is non-empty
-      Ms_ = any ? M : 0.f;
-      float S = 0.f;
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          x[b][v] = __builtin_amdgcn_exp2f(x[b][v] - Ms_);  // e (0 for an empty group)
-          S += x[b][v];
-        }
-      S += __shfl_xor(S, 32);
-      inv = any ? 1.0f / S : 0.f;
-      Lq = any ? Ms_ + log2f(S) : INFINITY;
-      Dq = 0.f;
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const f32x16 d = dw_block(b);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          x[b][v] *= inv;  // w
-          Dq = fmaf(x[b][v], d[v], Dq);
-        }
-      }
-      Dq += __shfl_xor(Dq, 32);
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const f32x16 d = dw_block(b);
-        float dp[16];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) dp[v] = x[b][v] * (d[v] - Dq);
-        dq_block(b, dp);
-      }
-    } else {
+    {
       // more groups than fit in registers: three passes over the blocks
       // (shift; sum and D; dp and dQ), the MFMAs recomputed in each
       float M = -INFINITY;
@@ -530,6 +488,318 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
   }
 }
 
+// ------------------------------------------------------------------ fused path
+// N <= 128 (NB <= 4 blocks of 32 groups): one launch does the work of
+// k_bwd_prep, k_bwd_query and k_bwd_group.  Each wave computes a tile's
+// weights w and dp once, in the query layout of k_bwd_query (lane = query),
+// uses dp for dQ as there, and hands w and dp to the reductions over queries
+// (dr += dp Q, dmu += w dO) through LDS: per group block it writes the two
+// 32 x 32 bf16 tiles row-major (row = query) and reads them back with transpose
+// reads as MFMA A operands (lane = group).  The dr / dmu accumulators of all
+// NB blocks stay in registers for the workgroup's whole query range (64 NB
+// per lane, accumulation registers), so a SIMD holds one wave.
+//
+// Group order inside a block: lane (query, h) holds the weights of groups
+// 8 a + 4 h + j (register 4 a + j of a score accumulator); they go to columns
+// 16 h + 4 a + j of the wave's tile (two 16-byte writes per tensor), so column
+// c, and the accumulator row c it feeds, is group fgroup(c) of the block.
+__device__ __forceinline__ int fgroup(int c) { return 8 * ((c >> 2) & 3) + 4 * (c >> 4) + (c & 3); }
+constexpr int kWs = 40;  // LDS row stride (bf16) of the w / dp tiles
+constexpr int kFusedWgs = 256;  // workgroups to aim for: one per MI355X compute unit
+
+// Query chunks per slice of the fused kernel: about kFusedWgs workgroups, each
+// with at least 8 tiles (two per wave).  A function of the shape only.
+int fused_chunks(int64_t BH, int n) {
+  const int64_t tiles = ((int64_t)n + 31) / 32;
+  int64_t c = (kFusedWgs + BH - 1) / BH;
+  const int64_t cmax = tiles / 8 > 1 ? tiles / 8 : 1;
+  return (int)(c < cmax ? c : cmax);
+}
+
+// acc += a b (MFMA 32x32x16 bf16) with the accumulator in accumulation
+// registers (AGPRs): the other MFMAs of the fused kernel keep their results in
+// ordinary VGPRs, which the per-lane sums of all groups would not fit beside.
+// The leading s_nop gives the two wait states a VALU write of an operand (or
+// of the zeroed accumulator) needs before an MFMA reads it; a chain of these
+// on one accumulator (source C = destination, the same registers) needs none.
+// The compiler does not look inside the statement, so nothing else may read an
+// accumulator before agpr_settle() has waited out the MFMA latency (at least
+// 18 wait states for a 16-pass MFMA): the fused kernel issues it at the end of
+// every tile, after that tile's last accumulation, so any copy the compiler
+// makes of an accumulator (at the loop exit) comes after it.  A CPU test reads
+// the compiled kernel and checks that no instruction touches an accumulation
+// register between one of these MFMAs and the next agpr_settle().
+__device__ __forceinline__ void mfma_agpr(f32x16& acc, const u32x4& a, const u32x4& b) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void agpr_settle() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"); }
+
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// 1-D grid of BH chunks workgroups, 256 threads (4 waves, one per SIMD).
+// Workgroup (bh, c) takes the query tiles [c T / chunks, (c + 1) T / chunks)
+// of slice bh, wave w every 4th of them; it writes its sums of dp q and w dO
+// per group to part[bh][c] (or, the only chunk, the rows k_bwd_finish would
+// form from them to gk / gv).
+template <int NB>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_bwd_fused(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ G, const float* __restrict__ centroid,
+    const int32_t* __restrict__ count, const float* __restrict__ vsum, int n, int N, int chunks, float scale,
+    float sl2e, uint16_t* __restrict__ dQ, float* __restrict__ part, uint16_t* __restrict__ gk,
+    uint16_t* __restrict__ gv) {
+  constexpr int Npad = NB * 32;
+  constexpr int kGroupB = 2 * Npad * kBs * 2 + Npad * 4;       // Rs, Ms, lc
+  constexpr int kWaveB = 2 * 32 * kBs * 2 + 2 * 32 * kWs * 2;  // Qt, Gt, WPd, WPw
+  constexpr int kRedB = NB * 2 * 32 * 64 * 4;
+  constexpr int kLdsB = kGroupB + 4 * kWaveB > kRedB ? kGroupB + 4 * kWaveB : kRedB;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kLdsB];
+  uint16_t* Rs = (uint16_t*)lds;
+  uint16_t* Ms = Rs + Npad * kBs;
+  float* lc = (float*)(Ms + Npad * kBs);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
+  const int64_t bh = blockIdx.x / chunks;
+  const int chunk = blockIdx.x % chunks;
+  uint16_t* Qw = (uint16_t*)(lds + kGroupB + wave * kWaveB);
+  uint16_t* Gw = Qw + 32 * kBs;
+  uint16_t* Wd = Gw + 32 * kBs;  // dp tile [32 queries][kWs]
+  uint16_t* Ww = Wd + 32 * kWs;  // w tile
+
+  // the slice's group rows, as k_bwd_prep forms them: R = bf16(centroid),
+  // value means bf16(vsum / count) (0 for an empty group), log2(count)
+  // (-inf for an empty group); thread x: group x / 16, features 4 (x % 16) ..
+  {
+    constexpr int kIt = Npad * 16 / 256;
+    float4 cv[kIt], sv[kIt];
+    int cnt[kIt];
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
+      const int x = tid + 256 * i, g = x >> 4;
+      const int64_t row = bh * N + min(g, N - 1);
+      cnt[i] = count[row];
+      cv[i] = *(const float4*)(centroid + row * 64 + 4 * (x & 15));
+      sv[i] = *(const float4*)(vsum + row * 64 + 4 * (x & 15));
+    }
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
+      const int x = tid + 256 * i, g = x >> 4, c = 4 * (x & 15);
+      const bool in = g < N;
+      const int k = in ? cnt[i] : 0;
+      const float4 r = in ? cv[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+      float4 m = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (k > 0) m = make_float4(sv[i].x / (float)k, sv[i].y / (float)k, sv[i].z / (float)k, sv[i].w / (float)k);
+      *(u32x2*)(Rs + g * kBs + c) = u32x2{pack2(r.x, r.y), pack2(r.z, r.w)};
+      *(u32x2*)(Ms + g * kBs + c) = u32x2{pack2(m.x, m.y), pack2(m.z, m.w)};
+      if (c == 0) lc[g] = k > 0 ? log2f((float)k) : -INFINITY;
+    }
+  }
+  __syncthreads();
+
+  const int64_t ntiles = ((int64_t)n + 31) / 32;
+  const int64_t c0 = chunk * ntiles / chunks, c1 = (chunk + 1) * ntiles / chunks;
+  const uint16_t* Qb = Q + bh * (int64_t)n * 64;
+  const uint16_t* Gb = G + bh * (int64_t)n * 64;
+  // acc[b][2 k + fb]: k = 0 dr, 1 dmu of group block b, features 32 fb ..;
+  // register v of lane (feature f, h) is group fgroup(8 (v / 4) + 4 h + v % 4)
+  f32x16 acc[NB][4];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) acc[b][k] = zero16();
+  // transpose-read addressing (block lane 4 j + s: row j, columns + 4 s)
+  const int trr = (lane & 15) >> 2, trc = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  u32x4 qn[4], gn[4];
+  load_row_frags(Qb, min((c0 + wave) * 32 + q, (int64_t)n - 1), qn);
+  load_row_frags(Gb, min((c0 + wave) * 32 + q, (int64_t)n - 1), gn);
+  for (int64_t t = c0 + wave; t < c1; t += 4) {
+    const int64_t qi = t * 32 + q;
+    u32x4 qf[4], gf[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      qf[s] = qn[s];
+      gf[s] = gn[s];
+    }
+    load_row_frags(Qb, min(qi + 128, (int64_t)n - 1), qn);
+    load_row_frags(Gb, min(qi + 128, (int64_t)n - 1), gn);
+    __builtin_amdgcn_sched_barrier(0);
+    // the tile's rows, row-major, for the transposed B operands of the reductions
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      *(u32x4*)(Qw + q * kBs + 32 * h + 8 * s) = qf[s];
+      *(u32x4*)(Gw + q * kBs + 32 * h + 8 * s) = gf[s];
+    }
+    // scores (log2 domain, count bias added) of every block: rows g, column q
+    f32x16 x[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      x[b] = zero16();
+      const uint16_t* rr = Rs + (32 * b + q) * kBs + 32 * h;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) x[b] = mfma(*(const u32x4*)(rr + 8 * s), qf[s], x[b]);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) x[b][v] = fmaf(x[b][v], sl2e, lc[32 * b + 8 * (v >> 2) + 4 * h + (v & 3)]);
+    }
+    // block b's dw_gq = mu_g . G_q, formed when needed (twice) rather than held
+    auto dw_block = [&](int b) __attribute__((always_inline)) {
+      f32x16 d = zero16();
+      const uint16_t* mr = Ms + (32 * b + q) * kBs + 32 * h;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) d = mfma(*(const u32x4*)(mr + 8 * s), gf[s], d);
+      return d;
+    };
+    float M = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) M = fmaxf(M, x[b][v]);
+    M = fmaxf(M, __shfl_xor(M, 32));
+    const bool any = M != -INFINITY;  // some group is non-empty
+    const float Ms_ = any ? M : 0.f;
+    // e = 2^(x - shift) (0 for an empty group), its sum and sum e dw
+    float S = 0.f, SD = 0.f;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const f32x16 d = dw_block(b);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        x[b][v] = __builtin_amdgcn_exp2f(x[b][v] - Ms_);
+        S += x[b][v];
+        SD = fmaf(x[b][v], d[v], SD);
+      }
+    }
+    S += __shfl_xor(S, 32);
+    SD += __shfl_xor(SD, 32);
+    // a padded query (past n) gets weight 0: it adds nothing to the sums
+    const float inv = any && qi < n ? 1.0f / S : 0.f;
+    const float Dq = SD * inv;  // D = sum_g w dw
+    // B operands of the reductions: lane (feature 32 fb + f, h) holds
+    // queries 16 u + 8 h + 0 .. 7 of the tile (two transpose reads each)
+    u32x4 bq[2][2], bg[2][2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int fb = 0; fb < 2; ++fb) {
+        const int o = (16 * u + 8 * h + trr) * kBs + 32 * fb + trc;
+        const u32x2 q0 = lds_tr16(Qw + o), q1 = lds_tr16(Qw + o + 4 * kBs);
+        const u32x2 g0 = lds_tr16(Gw + o), g1 = lds_tr16(Gw + o + 4 * kBs);
+        bq[u][fb] = u32x4{q0[0], q0[1], q1[0], q1[1]};
+        bg[u][fb] = u32x4{g0[0], g0[1], g1[0], g1[1]};
+      }
+    f32x16 o0 = zero16(), o1 = zero16();
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const f32x16 d = dw_block(b);
+      float dp[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        x[b][v] *= inv;  // w
+        dp[v] = x[b][v] * (d[v] - Dq);
+      }
+      u32x4 pd[2], pw[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        pd[u] = u32x4{pack2(dp[8 * u], dp[8 * u + 1]), pack2(dp[8 * u + 2], dp[8 * u + 3]),
+                      pack2(dp[8 * u + 4], dp[8 * u + 5]), pack2(dp[8 * u + 6], dp[8 * u + 7])};
+        pw[u] = u32x4{pack2(x[b][8 * u], x[b][8 * u + 1]), pack2(x[b][8 * u + 2], x[b][8 * u + 3]),
+                      pack2(x[b][8 * u + 4], x[b][8 * u + 5]), pack2(x[b][8 * u + 6], x[b][8 * u + 7])};
+      }
+      // dQ^T[f][q] += sum_g r_gf dp_gq: A = R^T (transpose reads of the group
+      // rows: groups 32 b + 16 u + 4 h + 0..3, then + 8), B = dp
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int o = (32 * b + 16 * u + 4 * h + trr) * kBs + trc;
+        const u32x2 a0l = lds_tr16(Rs + o), a0h = lds_tr16(Rs + o + 8 * kBs);
+        const u32x2 a1l = lds_tr16(Rs + o + 32), a1h = lds_tr16(Rs + o + 8 * kBs + 32);
+        o0 = mfma(u32x4{a0l[0], a0l[1], a0h[0], a0h[1]}, pd[u], o0);
+        o1 = mfma(u32x4{a1l[0], a1l[1], a1h[0], a1h[1]}, pd[u], o1);
+      }
+      // the block's w and dp tiles, row = query, column 16 h + v (group fgroup)
+      *(u32x4*)(Wd + q * kWs + 16 * h) = pd[0];
+      *(u32x4*)(Wd + q * kWs + 16 * h + 8) = pd[1];
+      *(u32x4*)(Ww + q * kWs + 16 * h) = pw[0];
+      *(u32x4*)(Ww + q * kWs + 16 * h + 8) = pw[1];
+      wave_sync();
+      // dr += dp Q, dmu += w dO: A = the tiles read transposed (lane = group
+      // column, queries 16 u + 8 h + 0 .. 7)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int o = (16 * u + 8 * h + trr) * kWs + trc;
+        const u32x2 d0 = lds_tr16(Wd + o), d1 = lds_tr16(Wd + o + 4 * kWs);
+        const u32x2 w0 = lds_tr16(Ww + o), w1 = lds_tr16(Ww + o + 4 * kWs);
+        const u32x4 ad = {d0[0], d0[1], d1[0], d1[1]}, aw = {w0[0], w0[1], w1[0], w1[1]};
+        mfma_agpr(acc[b][0], ad, bq[u][0]);
+        mfma_agpr(acc[b][1], ad, bq[u][1]);
+        mfma_agpr(acc[b][2], aw, bg[u][0]);
+        mfma_agpr(acc[b][3], aw, bg[u][1]);
+      }
+      wave_sync();
+    }
+    // dQ rows through the wave's dp tile area: lane (q, h) holds features 8 k + 4 h + j
+    uint16_t* Ot = Wd;  // [32][kBs] fits in the two tiles
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      *(u32x2*)(Ot + q * kBs + 8 * k + 4 * h) = u32x2{pack2(scale * o0[4 * k], scale * o0[4 * k + 1]),
+                                                      pack2(scale * o0[4 * k + 2], scale * o0[4 * k + 3])};
+      *(u32x2*)(Ot + q * kBs + 32 + 8 * k + 4 * h) = u32x2{pack2(scale * o1[4 * k], scale * o1[4 * k + 1]),
+                                                           pack2(scale * o1[4 * k + 2], scale * o1[4 * k + 3])};
+    }
+    wave_sync();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = 8 * k + (lane >> 3), ch = lane & 7;
+      const int64_t qo = t * 32 + row;
+      if (qo < n) *(u32x4*)(dQ + (bh * (int64_t)n + qo) * 64 + 8 * ch) = *(const u32x4*)(Ot + row * kBs + 8 * ch);
+    }
+    wave_sync();
+    agpr_settle();
+  }
+  // the four waves' sums per block, in a fixed order per block: step k, wave
+  // w adds its block (w + k) % 4 (the first writes it), so block b is
+  // ((p_b + p_b+1) + p_b+2) + p_b+3 (wave indices mod 4)
+  __syncthreads();  // every wave is done with its tiles
+  float* red = (float*)lds;  // [NB][2][32][64]: dr, dmu rows (group fgroup(row)) of each block
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (((wave + k) & 3) != b) continue;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int fb = 0; fb < 2; ++fb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            float* p = red + ((b * 2 + kk) * 32 + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * fb + q;
+            *p = k == 0 ? acc[b][2 * kk + fb][v] : *p + acc[b][2 * kk + fb][v];
+          }
+    }
+    __syncthreads();
+  }
+  if (chunks == 1) {
+    // the only chunk: the rows k_bwd_finish would form from it (the same
+    // operations: its sum over one partial is 0 + s = s)
+    for (int e = tid; e < Npad * 64; e += 256) {
+      const int b = e / (32 * 64), row = (e >> 6) & 31, f = e & 63, g = 32 * b + fgroup(row);
+      if (g >= N) continue;
+      const float sr = 0.f + red[((b * 2) * 32 + row) * 64 + f];
+      const float sm = 0.f + red[((b * 2 + 1) * 32 + row) * 64 + f];
+      const int cnt = count[bh * N + g];
+      gk[(bh * Npad + g) * 64 + f] = (uint16_t)bf16_bits(cnt > 0 ? scale * sr / (float)cnt : 0.f);
+      gv[(bh * Npad + g) * 64 + f] = (uint16_t)bf16_bits(cnt > 0 ? sm / (float)cnt : 0.f);
+    }
+    return;
+  }
+  float* out = part + ((bh * chunks + chunk) * 2) * (int64_t)Npad * 64;
+  for (int e = tid; e < 2 * Npad * 64; e += 256) {
+    const int kk = e / (Npad * 64), r = e % (Npad * 64);
+    const int b = r / (32 * 64), row = (r >> 6) & 31, f = r & 63, g = 32 * b + fgroup(row);
+    out[(int64_t)kk * Npad * 64 + g * 64 + f] = red[((b * 2 + kk) * 32 + row) * 64 + f];
+  }
+}
+
 // grid (Npad / 4, BH), 256 threads: thread = (group, feature) of 4 groups.
 // gk = scale sum_chunks dr / c, gv = sum_chunks dmu / c (0 for an empty
 // group), rounded to bf16 once: the rows every member key receives.
@@ -587,7 +857,8 @@ size_t backward_workspace_layout(const Dims& d, BackwardWorkspace* w, void* base
   void* MU = take((size_t)d.BH * Npad * 64 * 2);
   void* LC = take((size_t)d.BH * Npad * 4);
   void* ST = take((size_t)d.BH * d.n * 8);
-  void* PART = take((size_t)d.BH * bwd_chunks(d.BH, Npad / 32) * 2 * Npad * 64 * 4);
+  const int chunks = Npad <= 128 ? fused_chunks(d.BH, d.n) : bwd_chunks(d.BH, Npad / 32);
+  void* PART = take((size_t)d.BH * chunks * 2 * Npad * 64 * 4);
   void* GK = take((size_t)d.BH * Npad * 64 * 4);
   void* GV = take((size_t)d.BH * Npad * 64 * 4);
   if (w) *w = BackwardWorkspace{(uint16_t*)R, (uint16_t*)RT, (uint16_t*)MU, (float*)LC, ST, (float*)PART,
@@ -600,6 +871,32 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
                            void* dK, void* dV, const BackwardWorkspace& w, hipStream_t st) {
   const int Npad = bwd_npad(d.N), rts = bwd_rts(d.N), NB = Npad / 32;
   const float sl2e = scale * 1.4426950408889634f;
+  if (NB <= 4) {
+    const int chunks = fused_chunks(d.BH, d.n);
+    {
+      TimedLaunch tl("bwd_fused", st);
+#define GA_BWD_F(NBV)                                                                                              \
+  hipLaunchKernelGGL(k_bwd_fused<NBV>, dim3((unsigned)(d.BH * chunks)), dim3(256), 0, st, (const uint16_t*)Q,      \
+                     (const uint16_t*)dO, centroid, count, vsum, d.n, d.N, chunks, scale, sl2e, (uint16_t*)dQ,    \
+                     w.part, (uint16_t*)w.gk, (uint16_t*)w.gv)
+      switch (NB) {
+        case 1: GA_BWD_F(1); break;
+        case 2: GA_BWD_F(2); break;
+        case 3: GA_BWD_F(3); break;
+        default: GA_BWD_F(4); break;
+      }
+#undef GA_BWD_F
+    }
+    if (chunks > 1) {
+      TimedLaunch tl("bwd_finish", st);
+      hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 4), (unsigned)d.BH), dim3(256), 0, st, w.part, count,
+                         d.N, Npad, chunks, scale, (uint16_t*)w.gk, (uint16_t*)w.gv);
+    }
+    TimedLaunch tl("bwd_keys", st);
+    hipLaunchKernelGGL(k_bwd_keys, dim3((unsigned)((d.n + 31) / 32), (unsigned)d.BH), dim3(256), 0, st, belong,
+                       (const uint16_t*)w.gk, (const uint16_t*)w.gv, d.n, d.N, Npad, (uint16_t*)dK, (uint16_t*)dV);
+    return hipGetLastError();
+  }
   {
     TimedLaunch tl("bwd_prep", st);
     hipLaunchKernelGGL(k_bwd_prep, dim3((unsigned)NB, (unsigned)d.BH), dim3(256), 0, st, centroid, count, vsum, d.N,
@@ -617,10 +914,6 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
                      (const uint16_t*)dO, w.R, w.RT, w.MU, w.LC, d.n, rts, scale, sl2e, tpw, (uint16_t*)dQ,       \
                      (float2*)w.stats)
     switch (NB) {
-      case 1: GA_BWD_Q(1); break;
-      case 2: GA_BWD_Q(2); break;
-      case 3: GA_BWD_Q(3); break;
-      case 4: GA_BWD_Q(4); break;
       case 5: GA_BWD_Q(5); break;
       case 6: GA_BWD_Q(6); break;
       case 7: GA_BWD_Q(7); break;
@@ -636,10 +929,6 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
                      (const uint16_t*)Q, (const uint16_t*)dO, w.R, w.MU, w.LC, (const float2*)w.stats, d.n, d.BH,  \
                      chunks, sl2e, w.part, count, d.N, scale, (uint16_t*)w.gk, (uint16_t*)w.gv)
     switch (NB) {
-      case 1: GA_BWD_G(1); break;
-      case 2: GA_BWD_G(2); break;
-      case 3: GA_BWD_G(3); break;
-      case 4: GA_BWD_G(4); break;
       case 5: GA_BWD_G(5); break;
       case 6: GA_BWD_G(6); break;
       case 7: GA_BWD_G(7); break;

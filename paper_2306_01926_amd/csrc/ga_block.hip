@@ -66,9 +66,11 @@ __device__ __forceinline__ int woff(int r, int q) { return r * 128 + ((q ^ wkey(
 // then holds output feature 16 h + i.
 __device__ __forceinline__ int wrow(int rho) { return 16 * ((rho >> 2) & 1) + 4 * (rho >> 3) + (rho & 3); }
 
+// two values rounded to bf16 (nearest even) in one v_cvt_pk_bf16_f32
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
-  const __bf16 a = (__bf16)lo, b = (__bf16)hi;  // round to nearest even
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // grid: ceil(tiles / 8) * 8 workgroups of 256 threads; tiles = tiles_m * tiles_o.

@@ -133,11 +133,13 @@ def test_backward_slice_with_every_group_empty(oracle_mod, dev, N):
         assert torch.count_nonzero(X[0, 1]) == 0
 
 
-def test_backward_one_query_chunk_per_slice(oracle_mod, dev):
-    """128 slices x 4 group blocks fill the GPU with one query chunk per slice,
-    so the group kernel forms the dK / dV rows itself (no separate finish);
-    n = 2000 also gives the query kernel's waves several tiles each."""
-    B, H, n, N = 16, 8, 2000, 128
+@pytest.mark.parametrize("B,H,n,N", [(32, 8, 300, 128), (16, 8, 600, 200), (16, 8, 2000, 128)])
+def test_backward_one_query_chunk_per_slice(oracle_mod, dev, B, H, n, N):
+    """Enough slices that each gets one query chunk, so the chunk's kernel
+    forms the dK / dV rows itself (no separate finish): 256 slices for the
+    fused kernel (N <= 128), 128 slices x 7 group blocks for the group-side
+    kernel (N > 128); then 128 slices at N = 128 (two chunks per slice, several
+    tiles per wave, the finish kernel adds them)."""
     say(f"backward, one query chunk per slice (B={B}, H={H}, n={n}, N={N})")
     Q, K, V = inputs.make_qkv(B, H, n, 64, "bf16", 31, 64, 0.05, 0.3)
     rng = np.random.default_rng(32)
