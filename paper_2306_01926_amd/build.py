@@ -21,8 +21,7 @@ def hipcc() -> str:
 
 
 # Device-code flags of every source: packed FP32 instructions off; MFMA results
-# in ordinary VGPRs (the fused backward kernel places its long-lived
-# accumulators in AGPRs explicitly).
+# in ordinary VGPRs.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                 "-mllvm", "-amdgpu-mfma-vgpr-form", "-I", os.path.join(ROOT, "include")]

@@ -16,15 +16,15 @@
 //   dmu_j = sum_i w_ij G_i        ->  dV_k = dmu_{a_k} / c_{a_k}.
 //
 // Kernels (N <= 256, padded to Npad = 32 NB groups).  N <= 128:
-//   k_bwd_fused   per (slice, query chunk), one wave per SIMD: the slice's
-//                 group rows staged from the fp32 centroids and sums; per
-//                 32-query tile (lane = query) MFMA scores, the group softmax,
-//                 MFMA dw, D, dp, MFMA dQ; w and dp handed through LDS (read
-//                 back transposed, lane = group) to the MFMA reductions
-//                 dr += dp Q and dmu += w G, whose sums for every group stay
-//                 in accumulation registers over the chunk; the four waves'
-//                 sums added in a fixed order
-// N > 128 (every group's sums do not fit in registers):
+//   k_bwd_fused   per (slice, query chunk), 8 waves: the slice's group rows
+//                 staged from the fp32 centroids and sums; per step of 128
+//                 queries, each wave takes 16 (lane = query): MFMA scores,
+//                 the group softmax, MFMA dw, D, dp, MFMA dQ, and writes its
+//                 w and dp rows to LDS; then each wave adds the step into its
+//                 part of dr += dp Q or dmu += w G (32 groups x 64 features,
+//                 operands read back transposed), held in registers over the
+//                 chunk
+// N > 128 (two kernels; the group side recomputes the scores):
 //   k_bwd_prep    per slice: R = bf16(centroid) rows and transposed, bf16
 //                 value means, log2(count) (-inf for an empty group)
 //   k_bwd_query   per 32-query tile (lane = query): the query side as above
@@ -488,315 +488,295 @@ __global__ __launch_bounds__(256) void k_bwd_group(const uint16_t* __restrict__ 
   }
 }
 
-// ------------------------------------------------------------------ fused path
+// ---------------------------------------------------------------- fused path
 // N <= 128 (NB <= 4 blocks of 32 groups): one launch does the work of
-// k_bwd_prep, k_bwd_query and k_bwd_group.  Each wave computes a tile's
-// weights w and dp once, in the query layout of k_bwd_query (lane = query),
-// uses dp for dQ as there, and hands w and dp to the reductions over queries
-// (dr += dp Q, dmu += w dO) through LDS: per group block it writes the two
-// 32 x 32 bf16 tiles row-major (row = query) and reads them back with transpose
-// reads as MFMA A operands (lane = group).  The dr / dmu accumulators of all
-// NB blocks stay in registers for the workgroup's whole query range (64 NB
-// per lane, accumulation registers), so a SIMD holds one wave.
+// k_bwd_prep, k_bwd_query and k_bwd_group.  A workgroup of 8 waves (two per
+// SIMD) takes a slice's query chunk in steps of 128 queries:
+//   1. each wave takes 16 of them (lane = query): MFMA 16x16x32 scores and dw
+//      against the slice's groups, the group softmax, D, dp, MFMA dQ; it
+//      writes its w and dp rows (every group) and its q and dO rows to LDS;
+//   2. after a barrier, wave (t, p) adds the step's 128 queries into its part
+//      of the sums: t = 0 dr += dp Q, t = 1 dmu += w dO, for the 32 groups of
+//      tile column block p and all 64 features (MFMA 32x32x16, both operands
+//      read with transpose reads: lane = group, lane = feature);
+// then a second barrier.  Each (sum, group, feature) has one owning wave, so
+// the chunk's sums need no reduction across waves.
 //
-// Group order inside a block: lane (query, h) holds the weights of groups
-// 8 a + 4 h + j (register 4 a + j of a score accumulator); they go to columns
-// 16 h + 4 a + j of the wave's tile (two 16-byte writes per tensor), so column
-// c, and the accumulator row c it feeds, is group fgroup(c) of the block.
-__device__ __forceinline__ int fgroup(int c) { return 8 * ((c >> 2) & 3) + 4 * (c >> 4) + (c & 3); }
-constexpr int kWs = 40;  // LDS row stride (bf16) of the w / dp tiles
+// Group order in the w / dp rows: lane (query, kq) holds groups
+// 16 b + 4 kq + v (block b of 16, register v of a score accumulator), written
+// contiguously at column 8 NB kq + 4 b + v; fcol_group() inverts that.
+__device__ __forceinline__ int fcol_group(int c, int nb8) {
+  const int kq = c / nb8, r = c % nb8;
+  return 16 * (r >> 2) + 4 * kq + (r & 3);
+}
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f32x4 mfma16(const u32x4& a, const u32x4& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                 0, 0);
+}
 constexpr int kFusedWgs = 256;  // workgroups to aim for: one per MI355X compute unit
+constexpr int kStepQ = 128;     // queries per step (8 waves x 16)
+
+// LDS rows without padding: each row's 16-byte chunks are permuted by XOR
+// with a function of the row, chosen so that the accesses of the fused kernel
+// touch each bank once per 256-byte cycle (16 lanes of a 16-byte access, 32
+// lanes of an 8-byte or transpose access):
+//   fR: 128-byte rows of R / value means, read 16 rows x one chunk (scores)
+//       and 8 rows x two chunks (transpose reads for dQ);
+//   fQ: 128-byte rows (q / dO, and w / dp rows of 64), written 16 rows x one
+//       chunk, read 4 rows x 4 chunks (transpose reads);
+//   fW: 256-byte w / dp rows, the same accesses.
+__device__ __forceinline__ int fR(int r) { return (((r >> 1) & 3) << 1) | ((r >> 3) & 1); }
+__device__ __forceinline__ int fQ(int r) { return (((r >> 1) & 1) << 2) | (((r >> 2) & 1) << 1) | ((r >> 3) & 1); }
+__device__ __forceinline__ int fW(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+// element offset of column c (bf16, a multiple of 4) of row r: rows of len elements, chunk permutation f
+__device__ __forceinline__ int swz(int r, int len, int c, int f) { return r * len + ((((c >> 3) ^ f) << 3) | (c & 7)); }
 
 // Query chunks per slice of the fused kernel: about kFusedWgs workgroups, each
-// with at least 8 tiles (two per wave).  A function of the shape only.
+// with at least two steps.  A function of the shape only.
 int fused_chunks(int64_t BH, int n) {
-  const int64_t tiles = ((int64_t)n + 31) / 32;
+  const int64_t steps = ((int64_t)n + kStepQ - 1) / kStepQ;
   int64_t c = (kFusedWgs + BH - 1) / BH;
-  const int64_t cmax = tiles / 8 > 1 ? tiles / 8 : 1;
+  const int64_t cmax = steps / 2 > 1 ? steps / 2 : 1;
   return (int)(c < cmax ? c : cmax);
 }
 
-// acc += a b (MFMA 32x32x16 bf16) with the accumulator in accumulation
-// registers (AGPRs): the other MFMAs of the fused kernel keep their results in
-// ordinary VGPRs, which the per-lane sums of all groups would not fit beside.
-// The leading s_nop gives the two wait states a VALU write of an operand (or
-// of the zeroed accumulator) needs before an MFMA reads it; a chain of these
-// on one accumulator (source C = destination, the same registers) needs none.
-// The compiler does not look inside the statement, so nothing else may read an
-// accumulator before agpr_settle() has waited out the MFMA latency (at least
-// 18 wait states for a 16-pass MFMA): the fused kernel issues it at the end of
-// every tile, after that tile's last accumulation, so any copy the compiler
-// makes of an accumulator (at the loop exit) comes after it.  A CPU test reads
-// the compiled kernel and checks that no instruction touches an accumulation
-// register between one of these MFMAs and the next agpr_settle().
-__device__ __forceinline__ void mfma_agpr(f32x16& acc, const u32x4& a, const u32x4& b) {
-  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
-__device__ __forceinline__ void agpr_settle() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"); }
-
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// 1-D grid of BH chunks workgroups, 256 threads (4 waves, one per SIMD).
-// Workgroup (bh, c) takes the query tiles [c T / chunks, (c + 1) T / chunks)
-// of slice bh, wave w every 4th of them; it writes its sums of dp q and w dO
-// per group to part[bh][c] (or, the only chunk, the rows k_bwd_finish would
-// form from them to gk / gv).
+// 1-D grid of BH chunks workgroups, 512 threads.  Workgroup (bh, c) takes the
+// steps [c S / chunks, (c + 1) S / chunks) of slice bh; it writes its sums of
+// dp q and w dO per group to part[bh][c] (or, the only chunk, the rows
+// k_bwd_finish would form from them to gk / gv).
 template <int NB>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_bwd_fused(
-    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ G, const float* __restrict__ centroid,
-    const int32_t* __restrict__ count, const float* __restrict__ vsum, int n, int N, int chunks, float scale,
-    float sl2e, uint16_t* __restrict__ dQ, float* __restrict__ part, uint16_t* __restrict__ gk,
-    uint16_t* __restrict__ gv) {
-  constexpr int Npad = NB * 32;
-  constexpr int kGroupB = 2 * Npad * kBs * 2 + Npad * 4;       // Rs, Ms, lc
-  constexpr int kWaveB = 2 * 32 * kBs * 2 + 2 * 32 * kWs * 2;  // Qt, Gt, WPd, WPw
-  constexpr int kRedB = NB * 2 * 32 * 64 * 4;
-  constexpr int kLdsB = kGroupB + 4 * kWaveB > kRedB ? kGroupB + 4 * kWaveB : kRedB;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[kLdsB];
-  uint16_t* Rs = (uint16_t*)lds;
-  uint16_t* Ms = Rs + Npad * kBs;
-  float* lc = (float*)(Ms + Npad * kBs);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, q = lane & 31;
+__global__ __launch_bounds__(512) void k_bwd_fused(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ G,
+                                                   const float* __restrict__ centroid,
+                                                   const int32_t* __restrict__ count, const float* __restrict__ vsum,
+                                                   int n, int N, int chunks, float scale, float sl2e,
+                                                   uint16_t* __restrict__ dQ, float* __restrict__ part,
+                                                   uint16_t* __restrict__ gk, uint16_t* __restrict__ gv) {
+  constexpr int Npad = NB * 32, NB16 = 2 * NB, nb8 = 8 * NB;
+  // LDS rows without padding, their 16-byte chunks permuted per row (fsw):
+  // every access below (16-byte rows of 8 lanes, transpose reads of 4 rows x
+  // 32 bytes) then touches each bank once
+  constexpr int kWs = Npad <= 64 ? 64 : 128;  // row length (bf16) of the w / dp rows
+  auto fWP = [](int r) { return kWs == 128 ? fW(r) : fQ(r); };
+  __shared__ __attribute__((aligned(16))) uint16_t Rs[Npad * 64];
+  __shared__ __attribute__((aligned(16))) uint16_t Ms[Npad * 64];
+  __shared__ __attribute__((aligned(16))) float lc[Npad];
+  __shared__ __attribute__((aligned(16))) uint16_t WP[2][kStepQ * kWs];  // dp, w rows of the step
+  __shared__ __attribute__((aligned(16))) uint16_t QT[2][kStepQ * 64];  // q, dO rows of the step
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i = lane & 15, kq = lane >> 4;  // MFMA 16x16x32 lane: row / column i, k-group kq
   const int64_t bh = blockIdx.x / chunks;
   const int chunk = blockIdx.x % chunks;
-  uint16_t* Qw = (uint16_t*)(lds + kGroupB + wave * kWaveB);
-  uint16_t* Gw = Qw + 32 * kBs;
-  uint16_t* Wd = Gw + 32 * kBs;  // dp tile [32 queries][kWs]
-  uint16_t* Ww = Wd + 32 * kWs;  // w tile
 
   // the slice's group rows, as k_bwd_prep forms them: R = bf16(centroid),
   // value means bf16(vsum / count) (0 for an empty group), log2(count)
   // (-inf for an empty group); thread x: group x / 16, features 4 (x % 16) ..
   {
-    constexpr int kIt = Npad * 16 / 256;
+    constexpr int kIt = (Npad * 16 + 511) / 512;
     float4 cv[kIt], sv[kIt];
     int cnt[kIt];
 #pragma unroll
-    for (int i = 0; i < kIt; ++i) {
-      const int x = tid + 256 * i, g = x >> 4;
+    for (int it = 0; it < kIt; ++it) {
+      const int x = min(tid + 512 * it, Npad * 16 - 1), g = x >> 4;
       const int64_t row = bh * N + min(g, N - 1);
-      cnt[i] = count[row];
-      cv[i] = *(const float4*)(centroid + row * 64 + 4 * (x & 15));
-      sv[i] = *(const float4*)(vsum + row * 64 + 4 * (x & 15));
+      cnt[it] = count[row];
+      cv[it] = *(const float4*)(centroid + row * 64 + 4 * (x & 15));
+      sv[it] = *(const float4*)(vsum + row * 64 + 4 * (x & 15));
     }
 #pragma unroll
-    for (int i = 0; i < kIt; ++i) {
-      const int x = tid + 256 * i, g = x >> 4, c = 4 * (x & 15);
+    for (int it = 0; it < kIt; ++it) {
+      const int x = tid + 512 * it, g = x >> 4, c = 4 * (x & 15);
+      if (x >= Npad * 16) break;
       const bool in = g < N;
-      const int k = in ? cnt[i] : 0;
-      const float4 r = in ? cv[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+      const int k = in ? cnt[it] : 0;
+      const float4 r = in ? cv[it] : make_float4(0.f, 0.f, 0.f, 0.f);
       float4 m = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (k > 0) m = make_float4(sv[i].x / (float)k, sv[i].y / (float)k, sv[i].z / (float)k, sv[i].w / (float)k);
-      *(u32x2*)(Rs + g * kBs + c) = u32x2{pack2(r.x, r.y), pack2(r.z, r.w)};
-      *(u32x2*)(Ms + g * kBs + c) = u32x2{pack2(m.x, m.y), pack2(m.z, m.w)};
+      if (k > 0)
+        m = make_float4(sv[it].x / (float)k, sv[it].y / (float)k, sv[it].z / (float)k, sv[it].w / (float)k);
+      *(u32x2*)(Rs + swz(g, 64, c, fR(g))) = u32x2{pack2(r.x, r.y), pack2(r.z, r.w)};
+      *(u32x2*)(Ms + swz(g, 64, c, fR(g))) = u32x2{pack2(m.x, m.y), pack2(m.z, m.w)};
       if (c == 0) lc[g] = k > 0 ? log2f((float)k) : -INFINITY;
     }
   }
   __syncthreads();
 
-  const int64_t ntiles = ((int64_t)n + 31) / 32;
-  const int64_t c0 = chunk * ntiles / chunks, c1 = (chunk + 1) * ntiles / chunks;
+  const int64_t nsteps = ((int64_t)n + kStepQ - 1) / kStepQ;
+  const int64_t s0 = chunk * nsteps / chunks, s1 = (chunk + 1) * nsteps / chunks;
   const uint16_t* Qb = Q + bh * (int64_t)n * 64;
   const uint16_t* Gb = G + bh * (int64_t)n * 64;
-  // acc[b][2 k + fb]: k = 0 dr, 1 dmu of group block b, features 32 fb ..;
-  // register v of lane (feature f, h) is group fgroup(8 (v / 4) + 4 h + v % 4)
-  f32x16 acc[NB][4];
+  // the fold's part: t = 0 dr (dp, q), 1 dmu (w, dO); columns 32 p .. of the w / dp rows
+  const int ft = wave >> 2, fp = wave & 3;
+  const uint16_t* fA = WP[ft];
+  const uint16_t* fB = QT[ft];
+  f32x16 acc0 = zero16(), acc1 = zero16();  // features 0..31, 32..63
+  // transpose-read addressing (16-lane block: lane 4 j + s reads row j at columns + 4 s)
+  const int trr = (lane & 15) >> 2, trc = 16 * ((lane >> 4) & 1) + 4 * (lane & 3), h = lane >> 5;
+  // lane (i, kq): features 8 kq .. and 32 + 8 kq .. of its query row
+  auto load_q = [&](const uint16_t* X, int64_t row, u32x4 (&f)[2]) __attribute__((always_inline)) {
+    f[0] = *(const u32x4*)(X + row * 64 + 8 * kq);
+    f[1] = *(const u32x4*)(X + row * 64 + 32 + 8 * kq);
+  };
+  // per-lane LDS offsets (the rows' chunk permutations); the loops add
+  // whole rows, which keep the permutation
+  const int oS0 = swz(i, 64, 8 * kq, fR(i)), oS1 = swz(i, 64, 32 + 8 * kq, fR(i));  // score / dw A operands
+  int oT[4];  // dQ A operands: rows 4 kq + trr (+ 32 u, + 16), features 16 fb + 4 (lane % 4)
 #pragma unroll
-  for (int b = 0; b < NB; ++b)
-#pragma unroll
-    for (int k = 0; k < 4; ++k) acc[b][k] = zero16();
-  // transpose-read addressing (block lane 4 j + s: row j, columns + 4 s)
-  const int trr = (lane & 15) >> 2, trc = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  u32x4 qn[4], gn[4];
-  load_row_frags(Qb, min((c0 + wave) * 32 + q, (int64_t)n - 1), qn);
-  load_row_frags(Gb, min((c0 + wave) * 32 + q, (int64_t)n - 1), gn);
-  for (int64_t t = c0 + wave; t < c1; t += 4) {
-    const int64_t qi = t * 32 + q;
-    u32x4 qf[4], gf[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      qf[s] = qn[s];
-      gf[s] = gn[s];
+  for (int fb = 0; fb < 4; ++fb) oT[fb] = swz(4 * kq + trr, 64, 16 * fb + 4 * (lane & 3), fR(4 * kq + trr));
+  const int row = 16 * wave + i;  // this lane's row of the step
+  const int oQ0 = swz(row, 64, 8 * kq, fQ(row)), oQ1 = swz(row, 64, 32 + 8 * kq, fQ(row));  // q / dO rows
+  // the reductions' transpose reads: rows 8 h + trr (+ 4, + 16 ks)
+  const int ra = 8 * h + trr;
+  const int oA[2] = {swz(ra, kWs, 32 * fp + trc, fWP(ra)), swz(ra + 4, kWs, 32 * fp + trc, fWP(ra + 4))};
+  const int oB[4] = {swz(ra, 64, trc, fQ(ra)), swz(ra + 4, 64, trc, fQ(ra + 4)), swz(ra, 64, 32 + trc, fQ(ra)),
+                     swz(ra + 4, 64, 32 + trc, fQ(ra + 4))};
+  u32x4 qn[2], gn[2];
+  {
+    const int64_t r = min(s0 * kStepQ + 16 * wave + i, (int64_t)n - 1);
+    load_q(Qb, r, qn);
+    load_q(Gb, r, gn);
+  }
+  for (int64_t st = s0; st < s1; ++st) {
+    const int64_t qi = st * kStepQ + 16 * wave + i;  // this lane's query
+    u32x4 qf[2] = {qn[0], qn[1]}, gf[2] = {gn[0], gn[1]};
+    {
+      const int64_t r = min(qi + kStepQ, (int64_t)n - 1);
+      load_q(Qb, r, qn);
+      load_q(Gb, r, gn);
     }
-    load_row_frags(Qb, min(qi + 128, (int64_t)n - 1), qn);
-    load_row_frags(Gb, min(qi + 128, (int64_t)n - 1), gn);
     __builtin_amdgcn_sched_barrier(0);
-    // the tile's rows, row-major, for the transposed B operands of the reductions
+    // ---- 1. this wave's 16 queries against every group
+    // scores (log2 domain, count bias added): x[b][v] is group 16 b + 4 kq + v
+    f32x4 x[NB16], dw[NB16];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      *(u32x4*)(Qw + q * kBs + 32 * h + 8 * s) = qf[s];
-      *(u32x4*)(Gw + q * kBs + 32 * h + 8 * s) = gf[s];
+    for (int b = 0; b < NB16; ++b) {
+      x[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dw[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const int o = (s ? oS1 : oS0) + 16 * b * 64;
+        x[b] = mfma16(*(const u32x4*)(Rs + o), qf[s], x[b]);
+        dw[b] = mfma16(*(const u32x4*)(Ms + o), gf[s], dw[b]);
+      }
+      const float4 l4 = *(const float4*)(lc + 16 * b + 4 * kq);
+      x[b][0] = fmaf(x[b][0], sl2e, l4.x);
+      x[b][1] = fmaf(x[b][1], sl2e, l4.y);
+      x[b][2] = fmaf(x[b][2], sl2e, l4.z);
+      x[b][3] = fmaf(x[b][3], sl2e, l4.w);
     }
-    // scores (log2 domain, count bias added) of every block: rows g, column q
-    f32x16 x[NB];
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      x[b] = zero16();
-      const uint16_t* rr = Rs + (32 * b + q) * kBs + 32 * h;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) x[b] = mfma(*(const u32x4*)(rr + 8 * s), qf[s], x[b]);
-#pragma unroll
-      for (int v = 0; v < 16; ++v) x[b][v] = fmaf(x[b][v], sl2e, lc[32 * b + 8 * (v >> 2) + 4 * h + (v & 3)]);
-    }
-    // block b's dw_gq = mu_g . G_q, formed when needed (twice) rather than held
-    auto dw_block = [&](int b) __attribute__((always_inline)) {
-      f32x16 d = zero16();
-      const uint16_t* mr = Ms + (32 * b + q) * kBs + 32 * h;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) d = mfma(*(const u32x4*)(mr + 8 * s), gf[s], d);
-      return d;
-    };
     float M = -INFINITY;
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
+    for (int b = 0; b < NB16; ++b)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) M = fmaxf(M, x[b][v]);
+      for (int v = 0; v < 4; ++v) M = fmaxf(M, x[b][v]);
+    M = fmaxf(M, __shfl_xor(M, 16));
     M = fmaxf(M, __shfl_xor(M, 32));
     const bool any = M != -INFINITY;  // some group is non-empty
     const float Ms_ = any ? M : 0.f;
-    // e = 2^(x - shift) (0 for an empty group), its sum and sum e dw
     float S = 0.f, SD = 0.f;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const f32x16 d = dw_block(b);
+    for (int b = 0; b < NB16; ++b)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        x[b][v] = __builtin_amdgcn_exp2f(x[b][v] - Ms_);
+      for (int v = 0; v < 4; ++v) {
+        x[b][v] = __builtin_amdgcn_exp2f(x[b][v] - Ms_);  // 0 for an empty group
         S += x[b][v];
-        SD = fmaf(x[b][v], d[v], SD);
+        SD = fmaf(x[b][v], dw[b][v], SD);
       }
-    }
+    S += __shfl_xor(S, 16);
     S += __shfl_xor(S, 32);
+    SD += __shfl_xor(SD, 16);
     SD += __shfl_xor(SD, 32);
     // a padded query (past n) gets weight 0: it adds nothing to the sums
     const float inv = any && qi < n ? 1.0f / S : 0.f;
     const float Dq = SD * inv;  // D = sum_g w dw
-    // B operands of the reductions: lane (feature 32 fb + f, h) holds
-    // queries 16 u + 8 h + 0 .. 7 of the tile (two transpose reads each)
-    u32x4 bq[2][2], bg[2][2];
+    uint32_t pw[2 * NB16], pd[2 * NB16];
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int b = 0; b < NB16; ++b) {
+      float w[4], dp[4];
 #pragma unroll
-      for (int fb = 0; fb < 2; ++fb) {
-        const int o = (16 * u + 8 * h + trr) * kBs + 32 * fb + trc;
-        const u32x2 q0 = lds_tr16(Qw + o), q1 = lds_tr16(Qw + o + 4 * kBs);
-        const u32x2 g0 = lds_tr16(Gw + o), g1 = lds_tr16(Gw + o + 4 * kBs);
-        bq[u][fb] = u32x4{q0[0], q0[1], q1[0], q1[1]};
-        bg[u][fb] = u32x4{g0[0], g0[1], g1[0], g1[1]};
+      for (int v = 0; v < 4; ++v) {
+        w[v] = x[b][v] * inv;
+        dp[v] = w[v] * (dw[b][v] - Dq);
       }
-    f32x16 o0 = zero16(), o1 = zero16();
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const f32x16 d = dw_block(b);
-      float dp[16];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        x[b][v] *= inv;  // w
-        dp[v] = x[b][v] * (d[v] - Dq);
-      }
-      u32x4 pd[2], pw[2];
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        pd[u] = u32x4{pack2(dp[8 * u], dp[8 * u + 1]), pack2(dp[8 * u + 2], dp[8 * u + 3]),
-                      pack2(dp[8 * u + 4], dp[8 * u + 5]), pack2(dp[8 * u + 6], dp[8 * u + 7])};
-        pw[u] = u32x4{pack2(x[b][8 * u], x[b][8 * u + 1]), pack2(x[b][8 * u + 2], x[b][8 * u + 3]),
-                      pack2(x[b][8 * u + 4], x[b][8 * u + 5]), pack2(x[b][8 * u + 6], x[b][8 * u + 7])};
-      }
-      // dQ^T[f][q] += sum_g r_gf dp_gq: A = R^T (transpose reads of the group
-      // rows: groups 32 b + 16 u + 4 h + 0..3, then + 8), B = dp
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int o = (32 * b + 16 * u + 4 * h + trr) * kBs + trc;
-        const u32x2 a0l = lds_tr16(Rs + o), a0h = lds_tr16(Rs + o + 8 * kBs);
-        const u32x2 a1l = lds_tr16(Rs + o + 32), a1h = lds_tr16(Rs + o + 8 * kBs + 32);
-        o0 = mfma(u32x4{a0l[0], a0l[1], a0h[0], a0h[1]}, pd[u], o0);
-        o1 = mfma(u32x4{a1l[0], a1l[1], a1h[0], a1h[1]}, pd[u], o1);
-      }
-      // the block's w and dp tiles, row = query, column 16 h + v (group fgroup)
-      *(u32x4*)(Wd + q * kWs + 16 * h) = pd[0];
-      *(u32x4*)(Wd + q * kWs + 16 * h + 8) = pd[1];
-      *(u32x4*)(Ww + q * kWs + 16 * h) = pw[0];
-      *(u32x4*)(Ww + q * kWs + 16 * h + 8) = pw[1];
-      wave_sync();
-      // dr += dp Q, dmu += w dO: A = the tiles read transposed (lane = group
-      // column, queries 16 u + 8 h + 0 .. 7)
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int o = (16 * u + 8 * h + trr) * kWs + trc;
-        const u32x2 d0 = lds_tr16(Wd + o), d1 = lds_tr16(Wd + o + 4 * kWs);
-        const u32x2 w0 = lds_tr16(Ww + o), w1 = lds_tr16(Ww + o + 4 * kWs);
-        const u32x4 ad = {d0[0], d0[1], d1[0], d1[1]}, aw = {w0[0], w0[1], w1[0], w1[1]};
-        mfma_agpr(acc[b][0], ad, bq[u][0]);
-        mfma_agpr(acc[b][1], ad, bq[u][1]);
-        mfma_agpr(acc[b][2], aw, bg[u][0]);
-        mfma_agpr(acc[b][3], aw, bg[u][1]);
-      }
-      wave_sync();
+      pw[2 * b] = pack2(w[0], w[1]);
+      pw[2 * b + 1] = pack2(w[2], w[3]);
+      pd[2 * b] = pack2(dp[0], dp[1]);
+      pd[2 * b + 1] = pack2(dp[2], dp[3]);
     }
-    // dQ rows through the wave's dp tile area: lane (q, h) holds features 8 k + 4 h + j
-    uint16_t* Ot = Wd;  // [32][kBs] fits in the two tiles
+    // dQ^T[f][q] = sum_g r_gf dp_gq over 32-group steps u (blocks 2 u, 2 u + 1):
+    // A = R^T (transpose reads: groups 32 u + 4 kq + 0..3, then + 16), B = dp
+    f32x4 o[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      *(u32x2*)(Ot + q * kBs + 8 * k + 4 * h) = u32x2{pack2(scale * o0[4 * k], scale * o0[4 * k + 1]),
-                                                      pack2(scale * o0[4 * k + 2], scale * o0[4 * k + 3])};
-      *(u32x2*)(Ot + q * kBs + 32 + 8 * k + 4 * h) = u32x2{pack2(scale * o1[4 * k], scale * o1[4 * k + 1]),
-                                                           pack2(scale * o1[4 * k + 2], scale * o1[4 * k + 3])};
+    for (int fb = 0; fb < 4; ++fb) o[fb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const u32x4 bd = {pd[4 * u], pd[4 * u + 1], pd[4 * u + 2], pd[4 * u + 3]};
+#pragma unroll
+      for (int fb = 0; fb < 4; ++fb) {
+        const u32x2 al = lds_tr16(Rs + oT[fb] + 32 * u * 64);
+        const u32x2 ah = lds_tr16(Rs + oT[fb] + (32 * u + 16) * 64);
+        o[fb] = mfma16(u32x4{al[0], al[1], ah[0], ah[1]}, bd, o[fb]);
+      }
     }
-    wave_sync();
+    // dQ: lane (query i, kq) holds features 16 fb + 4 kq + v
+    if (qi < n) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int row = 8 * k + (lane >> 3), ch = lane & 7;
-      const int64_t qo = t * 32 + row;
-      if (qo < n) *(u32x4*)(dQ + (bh * (int64_t)n + qo) * 64 + 8 * ch) = *(const u32x4*)(Ot + row * kBs + 8 * ch);
+      for (int fb = 0; fb < 4; ++fb)
+        *(u32x2*)(dQ + (bh * (int64_t)n + qi) * 64 + 16 * fb + 4 * kq) =
+            u32x2{pack2(scale * o[fb][0], scale * o[fb][1]), pack2(scale * o[fb][2], scale * o[fb][3])};
     }
-    wave_sync();
-    agpr_settle();
-  }
-  // the four waves' sums per block, in a fixed order per block: step k, wave
-  // w adds its block (w + k) % 4 (the first writes it), so block b is
-  // ((p_b + p_b+1) + p_b+2) + p_b+3 (wave indices mod 4)
-  __syncthreads();  // every wave is done with its tiles
-  float* red = (float*)lds;  // [NB][2][32][64]: dr, dmu rows (group fgroup(row)) of each block
+    // the step's rows for the reductions
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
+    for (int c = 0; c < NB; ++c) {
+      const int o = swz(row, kWs, nb8 * kq + 8 * c, fWP(row));
+      *(u32x4*)(WP[0] + o) = u32x4{pd[4 * c], pd[4 * c + 1], pd[4 * c + 2], pd[4 * c + 3]};
+      *(u32x4*)(WP[1] + o) = u32x4{pw[4 * c], pw[4 * c + 1], pw[4 * c + 2], pw[4 * c + 3]};
+    }
+    *(u32x4*)(QT[0] + oQ0) = qf[0];
+    *(u32x4*)(QT[0] + oQ1) = qf[1];
+    *(u32x4*)(QT[1] + oQ0) = gf[0];
+    *(u32x4*)(QT[1] + oQ1) = gf[1];
+    __syncthreads();
+    // ---- 2. wave (t, p): sums over the step's queries, 16 per MFMA step:
+    // A = the w / dp rows read transposed (lane = column 32 p + m, queries
+    // 16 ks + 8 h + 0..7), B = the q / dO rows read transposed (lane = feature)
+    if (fp < NB) {
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      if (((wave + k) & 3) != b) continue;
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int fb = 0; fb < 2; ++fb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            float* p = red + ((b * 2 + kk) * 32 + 8 * (v >> 2) + 4 * h + (v & 3)) * 64 + 32 * fb + q;
-            *p = k == 0 ? acc[b][2 * kk + fb][v] : *p + acc[b][2 * kk + fb][v];
-          }
+      for (int ks = 0; ks < kStepQ / 16; ++ks) {
+        const int r = 16 * ks + 8 * h + trr;
+        const u32x2 a0 = lds_tr16(fA + oA[0] + 16 * ks * kWs), a1 = lds_tr16(fA + oA[1] + 16 * ks * kWs);
+        const u32x2 b0 = lds_tr16(fB + oB[0] + 16 * ks * 64), b1 = lds_tr16(fB + oB[1] + 16 * ks * 64);
+        const u32x2 b2 = lds_tr16(fB + oB[2] + 16 * ks * 64), b3 = lds_tr16(fB + oB[3] + 16 * ks * 64);
+        const u32x4 av = {a0[0], a0[1], a1[0], a1[1]};
+        acc0 = mfma(av, u32x4{b0[0], b0[1], b1[0], b1[1]}, acc0);
+        acc1 = mfma(av, u32x4{b2[0], b2[1], b3[0], b3[1]}, acc1);
+      }
     }
     __syncthreads();
   }
+  // wave (t, p): register v of lane (feature f, h) is column 32 p + 8 (v / 4) + 4 h + v % 4
+  if (fp >= NB) return;
+  const int f = lane & 31;
   if (chunks == 1) {
     // the only chunk: the rows k_bwd_finish would form from it (the same
     // operations: its sum over one partial is 0 + s = s)
-    for (int e = tid; e < Npad * 64; e += 256) {
-      const int b = e / (32 * 64), row = (e >> 6) & 31, f = e & 63, g = 32 * b + fgroup(row);
+    uint16_t* out = ft == 0 ? gk : gv;
+    const float sc = ft == 0 ? scale : 1.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int g = fcol_group(32 * fp + 8 * (v >> 2) + 4 * h + (v & 3), nb8);
       if (g >= N) continue;
-      const float sr = 0.f + red[((b * 2) * 32 + row) * 64 + f];
-      const float sm = 0.f + red[((b * 2 + 1) * 32 + row) * 64 + f];
       const int cnt = count[bh * N + g];
-      gk[(bh * Npad + g) * 64 + f] = (uint16_t)bf16_bits(cnt > 0 ? scale * sr / (float)cnt : 0.f);
-      gv[(bh * Npad + g) * 64 + f] = (uint16_t)bf16_bits(cnt > 0 ? sm / (float)cnt : 0.f);
+      out[(bh * Npad + g) * 64 + f] = (uint16_t)bf16_bits(cnt > 0 ? sc * (0.f + acc0[v]) / (float)cnt : 0.f);
+      out[(bh * Npad + g) * 64 + 32 + f] = (uint16_t)bf16_bits(cnt > 0 ? sc * (0.f + acc1[v]) / (float)cnt : 0.f);
     }
     return;
   }
-  float* out = part + ((bh * chunks + chunk) * 2) * (int64_t)Npad * 64;
-  for (int e = tid; e < 2 * Npad * 64; e += 256) {
-    const int kk = e / (Npad * 64), r = e % (Npad * 64);
-    const int b = r / (32 * 64), row = (r >> 6) & 31, f = r & 63, g = 32 * b + fgroup(row);
-    out[(int64_t)kk * Npad * 64 + g * 64 + f] = red[((b * 2 + kk) * 32 + row) * 64 + f];
+  float* out = part + ((bh * chunks + chunk) * 2 + ft) * (int64_t)Npad * 64;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int g = fcol_group(32 * fp + 8 * (v >> 2) + 4 * h + (v & 3), nb8);
+    out[g * 64 + f] = acc0[v];
+    out[g * 64 + 32 + f] = acc1[v];
   }
 }
 
@@ -876,7 +856,7 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
     {
       TimedLaunch tl("bwd_fused", st);
 #define GA_BWD_F(NBV)                                                                                              \
-  hipLaunchKernelGGL(k_bwd_fused<NBV>, dim3((unsigned)(d.BH * chunks)), dim3(256), 0, st, (const uint16_t*)Q,      \
+  hipLaunchKernelGGL(k_bwd_fused<NBV>, dim3((unsigned)(d.BH * chunks)), dim3(512), 0, st, (const uint16_t*)Q,      \
                      (const uint16_t*)dO, centroid, count, vsum, d.n, d.N, chunks, scale, sl2e, (uint16_t*)dQ,    \
                      w.part, (uint16_t*)w.gk, (uint16_t*)w.gv)
       switch (NB) {

@@ -62,6 +62,7 @@ CASES = [
     (1, 2, 300, 16, 3, 12, (0.05, 0.3)),
     (2, 2, 1000, 64, 4, 64, (0.05, 0.3)),
     (1, 1, 97, 33, 3, 8, (0.1, 0.1)),     # ragged tail, N not a multiple of 32
+    (1, 2, 600, 80, 3, 80, (0.05, 0.3)),    # three 32-group blocks
     (1, 2, 700, 100, 3, 100, (0.05, 0.3)),
     (1, 1, 500, 128, 3, 128, (0.05, 0.3)),
     (1, 1, 64, 1, 1, 4, (0.1, 0.1)),      # one group
