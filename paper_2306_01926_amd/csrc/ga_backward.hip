@@ -532,6 +532,22 @@ __device__ __forceinline__ int fW(int r) { return ((r & 3) << 2) | ((r >> 2) & 3
 // element offset of column c (bf16, a multiple of 4) of row r: rows of len elements, chunk permutation f
 __device__ __forceinline__ int swz(int r, int len, int c, int f) { return r * len + ((((c >> 3) ^ f) << 3) | (c & 7)); }
 
+// max / sum over the lanes l, l ^ 16, l ^ 32, l ^ 48 with the cross-row lane
+// swaps of gfx950 (VALU; each swap leaves a lane its own value and its
+// partner's, in row order, so all four lanes get the same bits)
+__device__ __forceinline__ float xrow_max(float v) {
+  auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(t[0]), __uint_as_float(t[1]));
+  t = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(t[0]), __uint_as_float(t[1]));
+}
+__device__ __forceinline__ float xrow_sum(float v) {
+  auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(t[0]) + __uint_as_float(t[1]);
+  t = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(t[0]) + __uint_as_float(t[1]);
+}
+
 // Query chunks per slice of the fused kernel: about kFusedWgs workgroups, each
 // with at least two steps.  A function of the shape only.
 int fused_chunks(int64_t BH, int n) {
@@ -668,8 +684,7 @@ __global__ __launch_bounds__(512) void k_bwd_fused(const uint16_t* __restrict__ 
     for (int b = 0; b < NB16; ++b)
 #pragma unroll
       for (int v = 0; v < 4; ++v) M = fmaxf(M, x[b][v]);
-    M = fmaxf(M, __shfl_xor(M, 16));
-    M = fmaxf(M, __shfl_xor(M, 32));
+    M = xrow_max(M);
     const bool any = M != -INFINITY;  // some group is non-empty
     const float Ms_ = any ? M : 0.f;
     float S = 0.f, SD = 0.f;
@@ -681,10 +696,8 @@ __global__ __launch_bounds__(512) void k_bwd_fused(const uint16_t* __restrict__ 
         S += x[b][v];
         SD = fmaf(x[b][v], dw[b][v], SD);
       }
-    S += __shfl_xor(S, 16);
-    S += __shfl_xor(S, 32);
-    SD += __shfl_xor(SD, 16);
-    SD += __shfl_xor(SD, 32);
+    S = xrow_sum(S);
+    SD = xrow_sum(SD);
     // a padded query (past n) gets weight 0: it adds nothing to the sums
     const float inv = any && qi < n ? 1.0f / S : 0.f;
     const float Dq = SD * inv;  // D = sum_g w dw
@@ -780,41 +793,69 @@ __global__ __launch_bounds__(512) void k_bwd_fused(const uint16_t* __restrict__ 
   }
 }
 
-// grid (Npad / 4, BH), 256 threads: thread = (group, feature) of 4 groups.
+// grid (Npad / 16, BH), 256 threads: thread = (group, 4 features) of 16 groups.
 // gk = scale sum_chunks dr / c, gv = sum_chunks dmu / c (0 for an empty
 // group), rounded to bf16 once: the rows every member key receives.
 __global__ __launch_bounds__(256) void k_bwd_finish(const float* __restrict__ part, const int32_t* __restrict__ count,
                                                     int N, int Npad, int chunks, float scale, uint16_t* __restrict__ gk,
                                                     uint16_t* __restrict__ gv) {
+  constexpr int kMaxC = 8;
   const int64_t bh = blockIdx.y;
-  const int g = blockIdx.x * 4 + (threadIdx.x >> 6), f = threadIdx.x & 63;
+  const int g = blockIdx.x * 16 + (threadIdx.x >> 4), f = 4 * (threadIdx.x & 15);
   if (g >= N) return;
-  float sr = 0.f, sm = 0.f;
-  for (int c = 0; c < chunks; ++c) {
-    const float* p = part + ((bh * chunks + c) * 2) * (int64_t)Npad * 64;
-    sr += p[g * 64 + f];
-    sm += p[(int64_t)Npad * 64 + g * 64 + f];
+  float4 sr = make_float4(0.f, 0.f, 0.f, 0.f), sm = sr;
+  for (int c0 = 0; c0 < chunks; c0 += kMaxC) {
+    float4 pr[kMaxC], pm[kMaxC];
+#pragma unroll
+    for (int c = 0; c < kMaxC; ++c) {  // up to kMaxC chunks' loads issued before their sums
+      if (c0 + c < chunks) {
+        const float* p = part + ((bh * chunks + c0 + c) * 2) * (int64_t)Npad * 64 + g * 64 + f;
+        pr[c] = *(const float4*)p;
+        pm[c] = *(const float4*)(p + (int64_t)Npad * 64);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < kMaxC; ++c) {  // in chunk order
+      if (c0 + c < chunks) {
+        sr.x += pr[c].x; sr.y += pr[c].y; sr.z += pr[c].z; sr.w += pr[c].w;
+        sm.x += pm[c].x; sm.y += pm[c].y; sm.z += pm[c].z; sm.w += pm[c].w;
+      }
+    }
   }
   const int cnt = count[bh * N + g];
-  gk[(bh * Npad + g) * 64 + f] = (uint16_t)bf16_bits(cnt > 0 ? scale * sr / (float)cnt : 0.f);
-  gv[(bh * Npad + g) * 64 + f] = (uint16_t)bf16_bits(cnt > 0 ? sm / (float)cnt : 0.f);
+  const float k = (float)cnt;
+  u32x2 ok = {0u, 0u}, ov = {0u, 0u};
+  if (cnt > 0) {
+    ok = u32x2{pack2(scale * sr.x / k, scale * sr.y / k), pack2(scale * sr.z / k, scale * sr.w / k)};
+    ov = u32x2{pack2(sm.x / k, sm.y / k), pack2(sm.z / k, sm.w / k)};
+  }
+  *(u32x2*)(gk + (bh * Npad + g) * 64 + f) = ok;
+  *(u32x2*)(gv + (bh * Npad + g) * 64 + f) = ov;
 }
 
-// grid (ceil(n / 32), BH), 256 threads: 8 lanes per key row (16 bytes each).
+// grid (ceil(n / 32), BH), 256 threads: threads 0..127 write dK, 128..255 dV;
+// 8 lanes per key row (16 bytes each), two keys per thread (k and k + 16),
+// both keys' loads issued before the stores.
 __global__ __launch_bounds__(256) void k_bwd_keys(const int32_t* __restrict__ belong, const uint16_t* __restrict__ gk,
                                                   const uint16_t* __restrict__ gv, int n, int N, int Npad,
                                                   uint16_t* __restrict__ dK, uint16_t* __restrict__ dV) {
   const int64_t bh = blockIdx.y;
-  const int k = blockIdx.x * 32 + (threadIdx.x >> 3), ch = threadIdx.x & 7;
-  if (k >= n) return;
-  const int g = belong[bh * n + k];
-  u32x4 ok = {0u, 0u, 0u, 0u}, ov = {0u, 0u, 0u, 0u};
-  if ((unsigned)g < (unsigned)N) {
-    ok = *(const u32x4*)(gk + (bh * Npad + g) * 64 + 8 * ch);
-    ov = *(const u32x4*)(gv + (bh * Npad + g) * 64 + 8 * ch);
+  const int t = threadIdx.x & 127, which = threadIdx.x >> 7;
+  const int k0 = blockIdx.x * 32 + (t >> 3), ch = t & 7;
+  const uint16_t* src = which ? gv : gk;
+  uint16_t* dst = which ? dV : dK;
+  int g[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) g[u] = k0 + 16 * u < n ? belong[bh * n + k0 + 16 * u] : -1;
+  u32x4 o[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    o[u] = u32x4{0u, 0u, 0u, 0u};
+    if ((unsigned)g[u] < (unsigned)N) o[u] = *(const u32x4*)(src + (bh * Npad + g[u]) * 64 + 8 * ch);
   }
-  *(u32x4*)(dK + (bh * n + k) * 64 + 8 * ch) = ok;
-  *(u32x4*)(dV + (bh * n + k) * 64 + 8 * ch) = ov;
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+    if (k0 + 16 * u < n) *(u32x4*)(dst + (bh * n + k0 + 16 * u) * 64 + 8 * ch) = o[u];
 }
 
 int bwd_npad(int N) { return (N + 31) / 32 * 32; }
@@ -869,7 +910,7 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
     }
     if (chunks > 1) {
       TimedLaunch tl("bwd_finish", st);
-      hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 4), (unsigned)d.BH), dim3(256), 0, st, w.part, count,
+      hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 16), (unsigned)d.BH), dim3(256), 0, st, w.part, count,
                          d.N, Npad, chunks, scale, (uint16_t*)w.gk, (uint16_t*)w.gv);
     }
     TimedLaunch tl("bwd_keys", st);
@@ -918,8 +959,8 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
   }
   if (chunks > 1) {  // (one chunk: k_bwd_group wrote the rows itself)
     TimedLaunch tl("bwd_finish", st);
-    hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 4), (unsigned)d.BH), dim3(256), 0, st, w.part, count, d.N,
-                       Npad, chunks, scale, (uint16_t*)w.gk, (uint16_t*)w.gv);
+    hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 16), (unsigned)d.BH), dim3(256), 0, st, w.part, count,
+                       d.N, Npad, chunks, scale, (uint16_t*)w.gk, (uint16_t*)w.gv);
   }
   TimedLaunch tl("bwd_keys", st);
   hipLaunchKernelGGL(k_bwd_keys, dim3((unsigned)((d.n + 31) / 32), (unsigned)d.BH), dim3(256), 0, st, belong,
