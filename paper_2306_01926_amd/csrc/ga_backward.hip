@@ -873,17 +873,18 @@ size_t backward_workspace_layout(const Dims& d, BackwardWorkspace* w, void* base
     off += (bytes + 255) & ~(size_t)255;
     return base ? (char*)base + o : nullptr;
   };
-  void* R = take((size_t)d.BH * Npad * 64 * 2);
-  void* RT = take((size_t)d.BH * 64 * rts * 2);
-  void* MU = take((size_t)d.BH * Npad * 64 * 2);
-  void* LC = take((size_t)d.BH * Npad * 4);
-  void* ST = take((size_t)d.BH * d.n * 8);
-  const int chunks = Npad <= 128 ? fused_chunks(d.BH, d.n) : bwd_chunks(d.BH, Npad / 32);
+  const bool fused = Npad <= 128;  // the fused kernel stages the group rows itself and keeps no statistics
+  void* R = fused ? nullptr : take((size_t)d.BH * Npad * 64 * 2);
+  void* RT = fused ? nullptr : take((size_t)d.BH * 64 * rts * 2);
+  void* MU = fused ? nullptr : take((size_t)d.BH * Npad * 64 * 2);
+  void* LC = fused ? nullptr : take((size_t)d.BH * Npad * 4);
+  void* ST = fused ? nullptr : take((size_t)d.BH * d.n * 8);
+  const int chunks = fused ? fused_chunks(d.BH, d.n) : bwd_chunks(d.BH, Npad / 32);
   void* PART = take((size_t)d.BH * chunks * 2 * Npad * 64 * 4);
-  void* GK = take((size_t)d.BH * Npad * 64 * 4);
-  void* GV = take((size_t)d.BH * Npad * 64 * 4);
+  void* GK = take((size_t)d.BH * Npad * 64 * 2);  // bf16 rows
+  void* GV = take((size_t)d.BH * Npad * 64 * 2);
   if (w) *w = BackwardWorkspace{(uint16_t*)R, (uint16_t*)RT, (uint16_t*)MU, (float*)LC, ST, (float*)PART,
-                                (float*)GK, (float*)GV};
+                                (uint16_t*)GK, (uint16_t*)GV};
   return off;
 }
 
@@ -899,7 +900,7 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
 #define GA_BWD_F(NBV)                                                                                              \
   hipLaunchKernelGGL(k_bwd_fused<NBV>, dim3((unsigned)(d.BH * chunks)), dim3(512), 0, st, (const uint16_t*)Q,      \
                      (const uint16_t*)dO, centroid, count, vsum, d.n, d.N, chunks, scale, sl2e, (uint16_t*)dQ,    \
-                     w.part, (uint16_t*)w.gk, (uint16_t*)w.gv)
+                     w.part, w.gk, w.gv)
       switch (NB) {
         case 1: GA_BWD_F(1); break;
         case 2: GA_BWD_F(2); break;
@@ -911,11 +912,11 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
     if (chunks > 1) {
       TimedLaunch tl("bwd_finish", st);
       hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 16), (unsigned)d.BH), dim3(256), 0, st, w.part, count,
-                         d.N, Npad, chunks, scale, (uint16_t*)w.gk, (uint16_t*)w.gv);
+                         d.N, Npad, chunks, scale, w.gk, w.gv);
     }
     TimedLaunch tl("bwd_keys", st);
     hipLaunchKernelGGL(k_bwd_keys, dim3((unsigned)((d.n + 31) / 32), (unsigned)d.BH), dim3(256), 0, st, belong,
-                       (const uint16_t*)w.gk, (const uint16_t*)w.gv, d.n, d.N, Npad, (uint16_t*)dK, (uint16_t*)dV);
+                       w.gk, w.gv, d.n, d.N, Npad, (uint16_t*)dK, (uint16_t*)dV);
     return hipGetLastError();
   }
   {
@@ -948,7 +949,7 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
 #define GA_BWD_G(NBV)                                                                                              \
   hipLaunchKernelGGL(k_bwd_group<NBV>, dim3((unsigned)((NBV * chunks * d.BH + 7) / 8 * 8)), dim3(256), 0, st,     \
                      (const uint16_t*)Q, (const uint16_t*)dO, w.R, w.MU, w.LC, (const float2*)w.stats, d.n, d.BH,  \
-                     chunks, sl2e, w.part, count, d.N, scale, (uint16_t*)w.gk, (uint16_t*)w.gv)
+                     chunks, sl2e, w.part, count, d.N, scale, w.gk, w.gv)
     switch (NB) {
       case 5: GA_BWD_G(5); break;
       case 6: GA_BWD_G(6); break;
@@ -960,11 +961,11 @@ hipError_t launch_backward(const Dims& d, const void* Q, const void* dO, const i
   if (chunks > 1) {  // (one chunk: k_bwd_group wrote the rows itself)
     TimedLaunch tl("bwd_finish", st);
     hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(Npad / 16), (unsigned)d.BH), dim3(256), 0, st, w.part, count,
-                       d.N, Npad, chunks, scale, (uint16_t*)w.gk, (uint16_t*)w.gv);
+                       d.N, Npad, chunks, scale, w.gk, w.gv);
   }
   TimedLaunch tl("bwd_keys", st);
   hipLaunchKernelGGL(k_bwd_keys, dim3((unsigned)((d.n + 31) / 32), (unsigned)d.BH), dim3(256), 0, st, belong,
-                     (const uint16_t*)w.gk, (const uint16_t*)w.gv, d.n, d.N, Npad, (uint16_t*)dK, (uint16_t*)dV);
+                     w.gk, w.gv, d.n, d.N, Npad, (uint16_t*)dK, (uint16_t*)dV);
   return hipGetLastError();
 }
 

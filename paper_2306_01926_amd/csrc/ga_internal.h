@@ -154,14 +154,14 @@ hipError_t launch_merge_plan(const Dims& d, const void* Q, const void* K, const 
 
 // Backward pass (ga_backward.hip), bf16, N <= backward_max_groups().
 struct BackwardWorkspace {
-  uint16_t* R;   // [BH][Npad][64] bf16 representatives
+  uint16_t* R;   // [BH][Npad][64] bf16 representatives (R .. stats: N > 128 only)
   uint16_t* RT;  // [BH][64][Npad + 4] the same, transposed
   uint16_t* MU;  // [BH][Npad][64] bf16 value means
   float* LC;     // [BH][Npad] log2(count), -inf for an empty group
   void* stats;   // [BH][n] float2: softmax shift + log2(sum) (log2 domain), D = dO . o per query
   float* part;   // [BH][chunks][2][Npad][64] per-chunk sums of dp q and w dO
-  float* gk;     // [BH][Npad][64] scale dr / count
-  float* gv;     // [BH][Npad][64] dmu / count
+  uint16_t* gk;  // [BH][Npad][64] bf16 scale dr / count
+  uint16_t* gv;  // [BH][Npad][64] bf16 dmu / count
 };
 int backward_max_groups();
 size_t backward_workspace_layout(const Dims& d, BackwardWorkspace* w, void* base);  // returns bytes
