@@ -569,9 +569,8 @@ __global__ __launch_bounds__(512) void k_bwd_fused(const uint16_t* __restrict__ 
                                                    uint16_t* __restrict__ dQ, float* __restrict__ part,
                                                    uint16_t* __restrict__ gk, uint16_t* __restrict__ gv) {
   constexpr int Npad = NB * 32, NB16 = 2 * NB, nb8 = 8 * NB;
-  // LDS rows without padding, their 16-byte chunks permuted per row (fsw):
-  // every access below (16-byte rows of 8 lanes, transpose reads of 4 rows x
-  // 32 bytes) then touches each bank once
+  // LDS rows without padding, their chunks permuted by fR (R, value means),
+  // fQ (q / dO rows) and fWP (w / dp rows: fW for 256-byte rows, fQ for 128)
   constexpr int kWs = Npad <= 64 ? 64 : 128;  // row length (bf16) of the w / dp rows
   auto fWP = [](int r) { return kWs == 128 ? fW(r) : fQ(r); };
   __shared__ __attribute__((aligned(16))) uint16_t Rs[Npad * 64];
@@ -755,7 +754,6 @@ __global__ __launch_bounds__(512) void k_bwd_fused(const uint16_t* __restrict__ 
     if (fp < NB) {
 #pragma unroll
       for (int ks = 0; ks < kStepQ / 16; ++ks) {
-        const int r = 16 * ks + 8 * h + trr;
         const u32x2 a0 = lds_tr16(fA + oA[0] + 16 * ks * kWs), a1 = lds_tr16(fA + oA[1] + 16 * ks * kWs);
         const u32x2 b0 = lds_tr16(fB + oB[0] + 16 * ks * 64), b1 = lds_tr16(fB + oB[1] + 16 * ks * 64);
         const u32x2 b2 = lds_tr16(fB + oB[2] + 16 * ks * 64), b3 = lds_tr16(fB + oB[3] + 16 * ks * 64);
