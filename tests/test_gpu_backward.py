@@ -65,6 +65,7 @@ CASES = [
     (1, 2, 600, 80, 3, 80, (0.05, 0.3)),    # three 32-group blocks
     (1, 2, 700, 100, 3, 100, (0.05, 0.3)),
     (1, 1, 500, 128, 3, 128, (0.05, 0.3)),
+    (1, 1, 3000, 64, 3, 64, (0.05, 0.3)),   # one slice: 12 query chunks, added by the finish in two batches of 8
     (1, 1, 64, 1, 1, 4, (0.1, 0.1)),      # one group
     (1, 2, 900, 200, 3, 200, (0.05, 0.3)),  # more groups than the one-pass query kernel holds
     (1, 1, 1500, 256, 3, 256, (0.05, 0.3)),  # largest N
