@@ -445,10 +445,12 @@ __device__ __forceinline__ void lloyd_assign(const LloydArgs& a, const LloydLds&
 // Exact fallback for the uncertain keys (queued from the top of ent): the
 // wave takes kLExactB keys at a time and decides them in fp64; after the
 // first round it adds the rows of those that changed group (fp64, from the
-// LDS copy) into the sums.
+// LDS copy) into the sums.  The keys are dealt from the last wave down (the
+// moved-key sums, which may run beside this phase, are dealt from wave 0 up).
 __device__ void lloyd_exact(const LloydArgs& a, const LloydLds& L, int64_t s, int k0, int nunc, bool first,
                             int* s_xmov) {
-  const int otid = opaque_tid(), lane = otid & 63, wave = __builtin_amdgcn_readfirstlane(otid >> 6);
+  const int otid = opaque_tid(), lane = otid & 63;
+  const int wave = kLW - 1 - __builtin_amdgcn_readfirstlane(otid >> 6);
   const uint16_t* Kbh = a.K + s * (int64_t)a.n * 64;
   double* kd = (double*)L.X + wave * kLExactB * 64;
   const int per = (nunc + kLW - 1) / kLW;
@@ -678,21 +680,40 @@ __device__ void lloyd_sums_moved(const LloydArgs& a, const LloydLds& L, int64_t 
 
 // ------------------------------------------------------------ exchange
 // The rank's sums and count deltas for the groups it does not own go to its
-// slot of the exchange buffer, and are zeroed for the next round.
+// slot of the exchange buffer, and are zeroed for the next round.  Those
+// groups are enumerated directly (the m-th in ascending order is member
+// m mod (P-1) of block m / (P-1), skipping member r), one row per wave and
+// step, kLPubB rows per wave read from LDS before any is stored.
+constexpr int kLPubB = 2;
 __device__ void lloyd_publish(const LloydArgs& a, const LloydLds& L, int64_t s, int r) {
-  const int tid = opaque_tid();
+  if (a.P == 1) return;
+  const int tid = opaque_tid(), lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int Npad = (a.N + 31) & ~31;
   double* xs = a.xs + (s * a.P + r) * (int64_t)Npad * 64;
   int32_t* xc = a.xc + (s * a.P + r) * (int64_t)Npad;
-  for (int idx = tid; idx < a.N * 64; idx += kLT) {
-    const int g = idx >> 6, c = idx & 63;
-    if (g % a.P == r) continue;
-    double* p = L.SA + g * kLSA + c;
-    st_dev64(xs + idx, *p);
-    *p = 0.0;
+  const int Pm = a.P - 1, Gn = a.N - (r < a.N ? (a.N - 1 - r) / a.P + 1 : 0);
+  auto other = [&](int m) __attribute__((always_inline)) {
+    const int i = m % Pm;
+    return (m / Pm) * a.P + i + (i >= r ? 1 : 0);
+  };
+  for (int m0 = wave; m0 < Gn; m0 += kLW * kLPubB) {
+    double v[kLPubB];
+    int at[kLPubB];
+#pragma unroll
+    for (int b = 0; b < kLPubB; ++b) {
+      const int m = m0 + kLW * b;  // wave-uniform
+      at[b] = m < Gn ? other(m) : -1;
+      v[b] = L.SA[max(at[b], 0) * kLSA + lane];
+    }
+#pragma unroll
+    for (int b = 0; b < kLPubB; ++b) {
+      if (at[b] < 0) break;
+      st_dev64(xs + at[b] * 64 + lane, v[b]);
+      L.SA[at[b] * kLSA + lane] = 0.0;
+    }
   }
-  for (int g = tid; g < a.N; g += kLT) {
-    if (g % a.P == r) continue;
+  for (int m = tid; m < Gn; m += kLT) {
+    const int g = other(m);
     st_dev(xc + g, L.dcA[g]);
     L.dcA[g] = 0;
   }
@@ -700,41 +721,69 @@ __device__ void lloyd_publish(const LloydArgs& a, const LloydLds& L, int64_t s, 
 
 // After barrier A: the other ranks' sums (and count deltas) for the rank's
 // groups added into its exact sums (and counts).  The thread's (item, other
-// rank) pairs are loaded kLGB at a time, all of a batch before any is added,
-// so that a slice with few ranks needs one round trip.
-constexpr int kLGB = 16;  // loads in flight per thread
-__device__ void lloyd_gather(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go, bool counts) {
-  const int tid = opaque_tid();
+// rank) pairs are loaded kLGB at a time, all of a batch before any is added;
+// the count deltas (group lg = tid mod 128 of other ranks tid / 128 + 4 k)
+// and, with `want_moved`, every rank's count of keys that changed group (the
+// slice's total is returned) are requested with the first batch, so that a
+// slice with few ranks needs one round trip.  Every load address is clamped
+// into the slice's buffers; loads past the end are not used.
+constexpr int kLGB = 8;  // loads in flight per thread
+__device__ __forceinline__ int lloyd_gather(const LloydArgs& a, const LloydLds& L, int64_t s, int r, int Go,
+                                            bool counts, bool want_moved) {
+  const int tid = opaque_tid(), lane = tid & 63;
   const int Npad = (a.N + 31) & ~31;
   const int U = (Go * 64 + kLT - 1) / kLT;  // items of this thread (some past Go * 64)
   const int pairs = U * (a.P - 1);
   const double* xs = a.xs + s * a.P * (int64_t)Npad * 64;
   int u = 0, q0 = 0;  // pair p = q0 U + u: item u of other rank q0 (ranks past r shifted by one)
-  for (int p0 = 0; p0 < pairs; p0 += kLGB) {
-    double v[kLGB];
-    int at[kLGB];  // LDS position of the item, -1 past the end (the items are the thread's own: no atomics)
+  double v[kLGB];
+  int at[kLGB];  // LDS position of the item, -1 past the end (the items are the thread's own: no atomics)
+  auto issue = [&](int p0) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < kLGB; ++b) {
       const int q = min(q0 + (q0 >= r), a.P - 1);
       const int idx = tid + kLT * u, lg = idx >> 6, c = idx & 63;
-      const int g = min(r + a.P * min(lg, Go - 1), a.N - 1);  // clamped: every load is in bounds
+      const int g = min(r + a.P * min(lg, Go - 1), a.N - 1);
       at[b] = p0 + b < pairs && lg < Go && r + a.P * lg < a.N ? g * kLSA + c : -1;
-      v[b] = at[b] >= 0 ? ld_dev64(xs + ((int64_t)q * Npad + g) * 64 + c) : 0.0;
+      v[b] = ld_dev64(xs + ((int64_t)q * Npad + g) * 64 + c);
       if (++u == U) {
         u = 0;
-        ++q0;
+        q0 = min(q0 + 1, a.P - 2);
       }
     }
+  };
+  auto add = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < kLGB; ++b)
       if (at[b] >= 0) L.SA[at[b]] += v[b];
+  };
+  if (pairs > 0) issue(0);
+  const int xmv = want_moved ? ld_dev(a.xm + s * 16 + min(lane & 15, a.P - 1)) : 0;
+  constexpr int kCK = 4;  // other ranks per thread for the count deltas (P <= 16)
+  int cdel[kCK], cg[kCK];
+  const int clg = tid & 127, cg0 = r + a.P * clg;
+#pragma unroll
+  for (int k = 0; k < kCK; ++k) {
+    const int qo = (tid >> 7) + 4 * k, q = min(qo + (qo >= r), a.P - 1);
+    cdel[k] = counts && a.P > 1 ? ld_dev(a.xc + (s * a.P + q) * (int64_t)Npad + min(cg0, a.N - 1)) : 0;
+    cg[k] = counts && qo < a.P - 1 && clg < Go && cg0 < a.N ? cg0 : -1;
   }
-  if (!counts) return;
-  // count deltas: one (group, other rank) pair per thread, added with LDS atomics
-  for (int pr = tid; pr < Go * (a.P - 1); pr += kLT) {
-    const int lg = pr % Go, q0 = pr / Go, q = q0 + (q0 >= r), g = r + a.P * lg;
-    if (g < a.N) atomicAdd(&L.dcA[g], ld_dev(a.xc + (s * a.P + q) * (int64_t)Npad + g));
+  if (pairs > 0) add();
+  for (int p0 = kLGB; p0 < pairs; p0 += kLGB) {
+    issue(p0);
+    add();
   }
+  int moved = 1;
+  if (want_moved) {  // every 16 lanes sum the P ranks' counts
+    int m = (lane & 15) < a.P ? xmv : 0;
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) m += __shfl_xor(m, off);
+    moved = __builtin_amdgcn_readfirstlane(m);
+  }
+  if (!counts) return moved;
+#pragma unroll
+  for (int k = 0; k < kCK; ++k)
+    if (cg[k] >= 0) atomicAdd(&L.dcA[cg[k]], cdel[k]);
   lds_barrier();
   for (int lg = tid; lg < Go; lg += kLT) {
     const int g = r + a.P * lg;
@@ -742,6 +791,7 @@ __device__ void lloyd_gather(const LloydArgs& a, const LloydLds& L, int64_t s, i
     L.cnt[lg] += L.dcA[g];
     L.dcA[g] = 0;
   }
+  return moved;
 }
 
 // ------------------------------------------------------------ update
@@ -928,12 +978,15 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
     // 1. assignment of the rank's keys and the sums of those that changed group
     lloyd_assign<NB>(a, L, s, k0, nk, first, (t & 1) != 0, cf, &s_nmov, &s_nunc);
     lds_barrier();
-    const int nunc = s_nunc;
+    const int nunc = s_nunc, nmov = s_nmov;
+    // after the first round, with few moved keys (their sums take the direct
+    // path, which uses no LDS scratch), the exact fallback and the moved-key
+    // sums run side by side: both add exact values into the sums
+    const bool side = !first && nmov <= kLDirect;
     if (nunc) {
       lloyd_exact(a, L, s, k0, nunc, first, &s_xmov);
-      lds_barrier();
+      if (!side || nmov == 0) lds_barrier();
     }
-    const int nmov = s_nmov;
     if (first)  // every key joins its group
       lloyd_sums_all(a.K, a, L, s, k0, nk, Npad, true);
     else if (nmov)
@@ -946,12 +999,7 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
     if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
     // 3. update of the rank's groups; a round in which no key of the slice
     // changed group is a fixed point, so it is the last
-    if (!first && !last) {
-      int moved = 0;
-      for (int q = 0; q < a.P; ++q) moved += ld_dev(a.xm + s * 16 + q);
-      last = moved == 0;
-    }
-    lloyd_gather(a, L, s, r, Go, true);
+    if (lloyd_gather(a, L, s, r, Go, true, !first && !last) == 0) last = true;
     lds_barrier();
     lloyd_finish(a, L, s, r, Go, last, prev);
     if (last) break;
@@ -971,7 +1019,7 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
   if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
   lloyd_publish(a, L, s, r);
   if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
-  lloyd_gather(a, L, s, r, Go, false);
+  lloyd_gather(a, L, s, r, Go, false, false);
   lds_barrier();
   lloyd_value_outputs(a, L, s, r, Go);
 }
