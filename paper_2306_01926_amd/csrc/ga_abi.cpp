@@ -15,6 +15,14 @@
 
 #include "ga_internal.h"
 
+float ga::cert_widen() {
+  const char* e = getenv("GA_CERT_WIDEN");
+  if (!e) return 1.0f;
+  char* end = nullptr;
+  const double v = strtod(e, &end);
+  return end != e && v >= 1.0 && v <= 65536.0 ? (float)v : 1.0f;
+}
+
 namespace {
 
 thread_local std::string g_last_error;

@@ -72,6 +72,11 @@ class TimedLaunch {
 };
 
 int vt_stride(int N);  // row stride (elements) of Vt
+// Factor that widens the certification bound of the MFMA scores: GA_CERT_WIDEN
+// in the environment (read at every launch), 1 to 65536, default 1.  A wider
+// bound only sends more keys to the exact fp64 decision, so the results do not
+// change; the tests use it to run the exact path on every key.
+float cert_widen();
 size_t workspace_layout(const Dims& d, Workspace* ws, void* base);  // returns bytes
 // Layout of the allocation-free forward (persistent grouping + bf16 attention):
 // only C, R, nrm64, nsplit, belong, count, Vt, ginit and the grouping kernel's

@@ -2099,8 +2099,8 @@ hipError_t launch_assign(const Dims& d, const void* K, const void* R, const uint
     // sequential model, 2x margin; the split itself is within 2^-24 |r|^2);
     // packing the register index into the low 4 mantissa bits moves a value by
     // < 2^(4 - 23) of its magnitude.
-    const float cm = (float)(kD + 4) * 0x1p-23f * (1.0f + 0x1p-10f);
-    const float cp = 0x1p-19f * (1.0f + 0x1p-10f);
+    const float cm = (float)(kD + 4) * 0x1p-23f * (1.0f + 0x1p-10f) * cert_widen();
+    const float cp = 0x1p-19f * (1.0f + 0x1p-10f) * cert_widen();
     const AssignPlan p = plan_assign(d, first);
     if (p.fused) *parts_out = (int)p.parts;
     const dim3 grid((unsigned)p.parts, (unsigned)d.BH), block(256);

@@ -1148,8 +1148,8 @@ hipError_t launch_lloyd(const Dims& d, const void* K, const void* V, const float
   a.T = iters;
   // certification constants: see launch_assign (MFMA accumulation error and
   // the 4 packed index bits)
-  a.cm = (float)(kD + 4) * 0x1p-23f * (1.0f + 0x1p-10f);
-  a.cp = 0x1p-19f * (1.0f + 0x1p-10f);
+  a.cm = (float)(kD + 4) * 0x1p-23f * (1.0f + 0x1p-10f) * cert_widen();
+  a.cp = 0x1p-19f * (1.0f + 0x1p-10f) * cert_widen();
   a.belong = belong;
   a.count = count;
   a.C = C;

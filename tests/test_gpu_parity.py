@@ -131,6 +131,30 @@ def test_cluster_fixed_point_ends_early(oracle_mod, dev, path):
     check_close(O, fref["O"], TOL["bf16"])
 
 
+EXACT_ALL_CASES = [
+    # B, H, n, N, iters: ranks per slice 8 (n = 2000), 4 and 16 (the last with
+    # N not a multiple of 32) on the one-launch path
+    (1, 2, 2000, 64, 4),
+    (2, 2, 1000, 128, 3),
+    (1, 1, 4000, 100, 3),
+]
+
+
+@pytest.mark.parametrize("case", EXACT_ALL_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_cluster_exact_decision_for_every_key(oracle_mod, dev, case, path, monkeypatch):
+    """With the certification bound widened 65536 times (GA_CERT_WIDEN) the
+    MFMA scores certify almost no key, so nearly every key of every round
+    takes the exact fp64 decision (and, after the first round, adds its own
+    row if it moves, beside the sums of the few certain moved keys).  The
+    groups, counts and centroids must still equal the oracle's bit for bit."""
+    B, H, n, N, iters = case
+    monkeypatch.setenv("GA_CERT_WIDEN", "65536")
+    say(f"cluster, exact decision for every key: {case} ({path})")
+    _, K, _ = inputs.make_qkv(B, H, n, 64, "bf16", 300 + n + N, max(8, N), 0.05, 0.3)
+    got, ref = cluster_both(oracle_mod, K, N, iters, "bf16", dev)
+    assert_groups_equal(got, ref)
+
+
 def test_cluster_with_caller_init(oracle_mod, dev):
     say("cluster with caller init")
     _, K, _ = inputs.make_qkv(2, 1, 700, 64, "bf16", 5, 40, 0.05, 0.3)
