@@ -244,7 +244,7 @@ __device__ __forceinline__ double lds_row_norm(const LloydLds& L, int g) {
 // k_{floor(j n / N)} (R = C exactly) or the given init (R = bf16(C)); padded
 // groups get zero rows and the largest bf16 as |r|^2 (they never win).  The
 // owners write C for their groups.
-__device__ void lloyd_stage_init(const LloydArgs& a, const LloydLds& L, int Npad, int64_t s, int r) {
+__device__ void lloyd_stage_init(const LloydArgs& a, const LloydLds& L, int Npad, int64_t s, int r, double* red) {
   const int tid = threadIdx.x;
   const uint16_t* Kbh = a.K + s * (int64_t)a.n * 64;
   const float* ibh = a.init ? a.init + s * (int64_t)a.N * 64 : nullptr;
@@ -288,10 +288,17 @@ __device__ void lloyd_stage_init(const LloydArgs& a, const LloydLds& L, int Npad
       *(u32x4*)(L.Ns + g * 8) = u32x4{0x7f7fu, 0u, 0u, 0u};
     }
   }
+  // the largest |r|^2 (padded groups hold 0), one value per wave of groups
+  if (tid < ((Npad + 63) & ~63)) {  // whole waves; lanes past Npad repeat group Npad - 1
+    double m = L.nrm[min(tid, Npad - 1)];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmax(m, __shfl_xor(m, off));
+    if ((tid & 63) == 0) red[tid >> 6] = m;
+  }
 }
 
 // Later rounds: the slice's representatives published by their owners.
-__device__ void lloyd_read_reps(const LloydArgs& a, const LloydLds& L, int64_t s) {
+__device__ void lloyd_read_reps(const LloydArgs& a, const LloydLds& L, int64_t s, double* red) {
   constexpr int kU = 128 * 8 / kLT;  // 16-byte chunks of R per thread, N <= 128
   const int tid = opaque_tid();
   const uint32_t* Rw = (const uint32_t*)(a.R + s * (int64_t)a.N * 64);
@@ -319,6 +326,13 @@ __device__ void lloyd_read_reps(const LloydArgs& a, const LloydLds& L, int64_t s
   if (tid < a.N) {
     *(u32x4*)(L.Ns + tid * 8) = u32x4{n0, n1, 0u, 0u};
     L.nrm[tid] = nr;
+  }
+  // the largest |r|^2, one value per wave of groups (threads past N hold group N - 1's)
+  if (tid < ((a.N + 63) & ~63)) {
+    double m = nr;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmax(m, __shfl_xor(m, off));
+    if ((tid & 63) == 0) red[tid >> 6] = m;
   }
 }
 
@@ -934,7 +948,7 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
   __shared__ int s_nmov, s_nunc, s_xmov, s_flag;
   __shared__ double s_red[kLW];
   constexpr int Npad = NB * 32;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x;
   const int bx = blockIdx.x, idx = bx >> 3;
   const int64_t s = (int64_t)(idx / a.P) * 8 + (bx & 7);
   const int r = idx % a.P;
@@ -945,7 +959,12 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
   uint32_t* ctr = a.sync + s * 32;
   int bar = 0;
 
-  lloyd_stage_init(a, L, Npad, s, r);
+  if (tid == 0) {  // the round's key counters (cleared again after each barrier A)
+    s_nmov = 0;
+    s_nunc = 0;
+    s_xmov = 0;
+  }
+  lloyd_stage_init(a, L, Npad, s, r, s_red);
   for (int i = tid; i < Npad * kLSA; i += kLT) L.SA[i] = 0.0;
   for (int i = tid; i < Npad; i += kLT) {
     L.dcA[i] = 0;
@@ -957,21 +976,10 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
   for (int t = 0; t < a.T; ++t) {
     const bool first = t == 0;
     bool last = t == a.T - 1;
-    // certification constants from the largest |r|^2 of the slice
-    double mx = 0.0;
-    for (int g = tid; g < a.N; g += kLT) mx = fmax(mx, L.nrm[g]);
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
-    if (lane == 0) s_red[wave] = mx;
-    if (tid == 0) {
-      s_nmov = 0;
-      s_nunc = 0;
-      s_xmov = 0;
-    }
-    lds_barrier();
+    // certification constants from the largest |r|^2 of the slice (one value
+    // per wave of groups, left by lloyd_stage_init / lloyd_read_reps)
     double nmax = s_red[0];
-#pragma unroll
-    for (int w = 1; w < kLW; ++w) nmax = fmax(nmax, s_red[w]);
+    if (Npad > 64) nmax = fmax(nmax, s_red[1]);
     const float nmaxf = (float)nmax * (1.0f + 0x1p-20f);
     const LloydCert cf = lloyd_cert(nmaxf, sqrtf(nmaxf) * (1.0f + 0x1p-20f), a.cm, a.cp);
 
@@ -997,6 +1005,11 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
     float2 prev[kLFinU];
     lloyd_prev_c(a, s, r, Go, prev);
     if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
+    if (tid == 0) {  // every use of this round's key counters is behind the barrier
+      s_nmov = 0;
+      s_nunc = 0;
+      s_xmov = 0;
+    }
     // 3. update of the rank's groups; a round in which no key of the slice
     // changed group is a fixed point, so it is the last
     if (lloyd_gather(a, L, s, r, Go, true, !first && !last) == 0) last = true;
@@ -1005,7 +1018,7 @@ __global__ __launch_bounds__(kLT) void k_lloyd(LloydArgs a) {
     if (last) break;
     // 4. barrier B, then the slice's new representatives
     if (!slice_barrier(ctr, a.status, a.P, bar++, &s_flag)) return;
-    lloyd_read_reps(a, L, s);
+    lloyd_read_reps(a, L, s, s_red);
     lds_barrier();
   }
   // the groups of the rank's keys
