@@ -95,6 +95,9 @@ CLUSTER_CASES = [
     ("bf16", 1, 1, 2000, 256, 3, 256, (0.05, 0.3)),
     ("bf16", 1, 1, 1500, 1024, 2, 256, (0.05, 0.3)), # largest N
     ("bf16", 1, 1, 4000, 100, 4, 300, (0.3, 0.3)),   # N not a multiple of 32, heavy overlap
+    ("bf16", 1, 2, 700, 50, 4, 64, (0.05, 0.3)),    # 3 ranks per slice on the one-launch path
+    ("bf16", 1, 1, 1200, 70, 4, 96, (0.05, 0.3)),   # 5 ranks
+    ("bf16", 1, 1, 1700, 128, 4, 160, (0.05, 0.3)), # 7 ranks, N = 128
     ("f32", 1, 1, 512, 32, 5, 32, (0.05, 0.05)),     # the fp32 workload at full size
     ("f32", 1, 2, 200, 20, 4, 30, (0.05, 0.3)),
     ("f32", 1, 1, 130, 130, 2, 8, (0.1, 0.1)),
